@@ -1,0 +1,444 @@
+"""Pins of the fp64 oracle against facts fixed by the paper and by mathematics.
+
+Each pin raises AssertionError when the oracle disagrees. They are collected as
+tests in test_oracle_pins.py and re-run against deliberately mutated copies of the
+oracle in test_oracle_mutations.py (every plausible mistake must trip a pin).
+
+Independent routes used here (none re-types the oracle's own loop):
+  * hand-derived exact values of Eq. (2)-(3) (tests/golden/*.json)
+  * closed forms: beta=0/alpha=1 keeps the state; beta=1, q=k, |k|=1 returns v;
+    alpha=0 gives beta (k.q) v
+  * the matrix form S <- alpha S (I - beta k k^T) + beta v k^T of a chain
+  * the WY / triangular-solve closed form of the recurrence on a tree
+    (delta from numpy.linalg.solve over the ancestor-masked Gram system)
+  * numpy.convolve for the causal convolution along a chain
+  * structural invariants: identical sibling subtrees, commit == node state,
+    permutation equivariance over value rows, head independence, off-path poisoning
+"""
+from __future__ import annotations
+
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+
+import oracle
+from lumo_synth import configs, trees
+from lumo_synth.configs import Workload
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def load_golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def make_wl(parents, *, d_k, d_v, h_k=1, h_v=1, n_layers=1, n_rows=None, channels=4,
+            op_dtype=0, max_path=None):
+    parents = [np.asarray(p, dtype=np.int32) for p in parents]
+    n_rows = np.array([len(p) for p in parents] if n_rows is None else n_rows, dtype=np.int32)
+    mp = max_path or max(int(trees.depths(p).max()) + 1 for p in parents)
+    return Workload(name="custom", n_req=len(parents), n_layers=n_layers, h_k=h_k, h_v=h_v,
+                    d_k=d_k, d_v=d_v, op_dtype=op_dtype, parents=parents, n_rows=n_rows,
+                    accepted=np.full(len(parents), -1, np.int32), max_path=mp,
+                    channels=channels)
+
+
+def random_arrays(wl, rng, *, alpha_direct=False):
+    """float32 operands in the boundary layouts (row = physical slot)."""
+    L, R = wl.n_layers, wl.total_rows
+    k = rng.standard_normal((L, R, wl.h_k, wl.d_k))
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    a = dict(
+        q=rng.standard_normal((L, R, wl.h_k, wl.d_k)).astype(np.float32),
+        k=k.astype(np.float32),
+        v=rng.standard_normal((L, R, wl.h_v, wl.d_v)).astype(np.float32),
+        beta=(1 / (1 + np.exp(-rng.standard_normal((L, R, wl.h_v))))).astype(np.float32),
+        state0=(0.1 * rng.standard_normal((wl.n_req, L, wl.h_v, wl.d_k, wl.d_v))).astype(np.float32),
+    )
+    z = rng.standard_normal((L, R, wl.h_v))
+    a["g"] = (np.exp(-np.logaddexp(0, z)) if alpha_direct else -np.logaddexp(0, z)).astype(np.float32)
+    return a
+
+
+def _rows(wl, r):
+    return oracle.plan.rows_of(wl.parents[r], int(wl.row_off[r]))
+
+
+def _alpha(wl, a, l, row, h, alpha_direct):
+    g = float(a["g"][l, row, h])
+    return g if alpha_direct else float(np.exp(np.float64(g)))
+
+
+# --------------------------------------------------------------------------- hand values
+
+def pin_hand_scalar():
+    gd = load_golden("hand_scalar.json")
+    wl = make_wl([gd["parent"]], d_k=1, d_v=1)
+    rows = _rows(wl, 0)
+    a = dict(q=np.zeros((1, 3, 1, 1), np.float32), k=np.zeros((1, 3, 1, 1), np.float32),
+             v=np.zeros((1, 3, 1, 1), np.float32), g=np.zeros((1, 3, 1), np.float32),
+             beta=np.zeros((1, 3, 1), np.float32),
+             state0=np.full((1, 1, 1, 1, 1), float(Fraction(gd["state0"])), np.float32))
+    for i, nd in enumerate(gd["nodes"]):
+        rw = rows[i]
+        a["q"][0, rw, 0, 0] = float(Fraction(nd["q"]))
+        a["k"][0, rw, 0, 0] = float(Fraction(nd["k"]))
+        a["v"][0, rw, 0, 0] = float(Fraction(nd["v"]))
+        a["g"][0, rw, 0] = float(Fraction(nd["alpha"]))
+        a["beta"][0, rw, 0] = float(Fraction(nd["beta"]))
+    wl.arrays = a
+    o, st = oracle.verify_nodes(wl, 0, 0, 0, [0, 1, 2], gate_is_alpha=True, want_state=True)
+    for i, nd in enumerate(gd["nodes"]):
+        assert o[i, 0] == float(Fraction(nd["o"])), (nd["name"], o[i, 0])
+        assert st[i, 0, 0] == float(Fraction(nd["state"])), (nd["name"], st[i, 0, 0])
+
+
+def pin_hand_2x2():
+    gd = load_golden("hand_2x2.json")
+    wl = make_wl([[-1]], d_k=2, d_v=2)
+    a = dict(q=np.array(gd["q"], np.float32).reshape(1, 1, 1, 2),
+             k=np.array(gd["k"], np.float32).reshape(1, 1, 1, 2),
+             v=np.array(gd["v"], np.float32).reshape(1, 1, 1, 2),
+             g=np.full((1, 1, 1), gd["alpha"], np.float32),
+             beta=np.full((1, 1, 1), gd["beta"], np.float32),
+             state0=np.array(gd["state0_key_major"], np.float32).reshape(1, 1, 1, 2, 2))
+    wl.arrays = a
+    o, st = oracle.verify_nodes(wl, 0, 0, 0, [0], gate_is_alpha=True, want_state=True)
+    assert np.array_equal(o[0], np.array(gd["o"], np.float64)), o
+    assert np.array_equal(st[0], np.array(gd["state_key_major"], np.float64)), st
+
+
+# --------------------------------------------------------------------------- closed forms
+
+def pin_beta0_alpha1_identity():
+    """beta = 0 and alpha = 1: the state is returned bit for bit, o = S0 q."""
+    rng = np.random.default_rng(11)
+    wl = make_wl([trees.FIG1_PARENT], d_k=8, d_v=6)
+    a = random_arrays(wl, rng, alpha_direct=True)
+    a["beta"][:] = 0.0
+    a["g"][:] = 1.0
+    wl.arrays = a
+    nodes = list(range(7))
+    o, st = oracle.verify_nodes(wl, 0, 0, 0, nodes, gate_is_alpha=True, want_state=True)
+    S0 = a["state0"][0, 0, 0].astype(np.float64)
+    rows = _rows(wl, 0)
+    for i in nodes:
+        assert np.array_equal(st[i], S0)
+        want = S0.T @ a["q"][0, rows[i], 0].astype(np.float64)
+        np.testing.assert_allclose(o[i], want, rtol=0, atol=1e-14)
+
+
+def pin_delta_rule_writes_v():
+    """beta = 1, q = k with |k| = 1 exactly: o = v whatever alpha and the parent state."""
+    rng = np.random.default_rng(12)
+    wl = make_wl([trees.FIG1_PARENT], d_k=4, d_v=5)
+    a = random_arrays(wl, rng)
+    signs = rng.choice([-0.5, 0.5], size=a["k"].shape).astype(np.float32)
+    a["k"] = signs                      # (+-1/2, ..., +-1/2) has norm exactly 1 at d_k = 4
+    a["q"] = signs.copy()
+    a["beta"][:] = 1.0
+    wl.arrays = a
+    o = oracle.verify_nodes(wl, 0, 0, 0, list(range(7)))
+    rows = _rows(wl, 0)
+    for i in range(7):
+        np.testing.assert_allclose(o[i], a["v"][0, rows[i], 0], rtol=0, atol=1e-13)
+
+
+def pin_alpha0_forgets():
+    """alpha = 0: R = beta v k^T, o = beta (k . q) v, independent of the ancestry."""
+    rng = np.random.default_rng(13)
+    wl = make_wl([trees.FIG1_PARENT], d_k=6, d_v=3)
+    a = random_arrays(wl, rng, alpha_direct=True)
+    a["g"][:] = 0.0
+    wl.arrays = a
+    o = oracle.verify_nodes(wl, 0, 0, 0, list(range(7)), gate_is_alpha=True)
+    rows = _rows(wl, 0)
+    for i in range(7):
+        rw = rows[i]
+        k = a["k"][0, rw, 0].astype(np.float64)
+        q = a["q"][0, rw, 0].astype(np.float64)
+        want = float(a["beta"][0, rw, 0]) * float(k @ q) * a["v"][0, rw, 0].astype(np.float64)
+        np.testing.assert_allclose(o[i], want, rtol=1e-13, atol=1e-15)
+
+
+# --------------------------------------------------------------------------- independent forms
+
+def chain_matrix_form(S0_key_major, alphas, betas, ks, vs, qs):
+    """Sequential scan in the form S <- alpha S (I - beta k k^T) + beta v k^T, o = S q."""
+    R = S0_key_major.T.astype(np.float64).copy()
+    dk = R.shape[1]
+    outs, states = [], []
+    for a, b, k, v, q in zip(alphas, betas, ks, vs, qs):
+        R = a * R @ (np.eye(dk) - b * np.outer(k, k)) + b * np.outer(v, k)
+        outs.append(R @ q)
+        states.append(R.T.copy())
+    return np.array(outs), np.array(states)
+
+
+def tree_wy_form(parent, S0_key_major, alphas, betas, K, V, Q):
+    """Closed form R_t = gamma_t R0 + sum_{s anc-or-self t} Gamma(s->t) delta_s k_s^T.
+
+    delta solves the ancestor-masked unit-triangular system
+      delta_t + beta_t sum_{s strict anc t} Gamma(s->t) (k_s.k_t) delta_s
+          = beta_t (v_t - gamma_t R0 k_t)
+    with gamma_t the product of alpha along root..t and Gamma(s->t) the product over
+    the nodes after s up to t. Solved with numpy.linalg.solve; outputs
+      o_t = gamma_t R0 q_t + sum_{s anc-or-self t} Gamma(s->t) (k_s.q_t) delta_s.
+    """
+    n = len(parent)
+    R0 = S0_key_major.T.astype(np.float64)
+    anc = [oracle.plan.ancestry(parent, t) for t in range(n)]
+
+    def Gam(s, t):
+        path = anc[t]
+        return float(np.prod([alphas[x] for x in path[path.index(s) + 1:]]))
+
+    gamma = np.array([float(np.prod([alphas[x] for x in anc[t]])) for t in range(n)])
+    A = np.eye(n)
+    for t in range(n):
+        for s in anc[t][:-1]:
+            A[t, s] = betas[t] * Gam(s, t) * float(K[s] @ K[t])
+    rhs = np.stack([betas[t] * (V[t] - gamma[t] * (R0 @ K[t])) for t in range(n)])
+    delta = np.linalg.solve(A, rhs)
+    O = np.stack([gamma[t] * (R0 @ Q[t]) + sum(Gam(s, t) * float(K[s] @ Q[t]) * delta[s]
+                                               for s in anc[t]) for t in range(n)])
+    return O
+
+
+def _node_operands(wl, a, r, l, h, alpha_direct=False):
+    rows = _rows(wl, r)
+    hk = h // (wl.h_v // wl.h_k)
+    n = len(wl.parents[r])
+    al = [_alpha(wl, a, l, rows[i], h, alpha_direct) for i in range(n)]
+    be = [float(a["beta"][l, rows[i], h]) for i in range(n)]
+    K = np.stack([a["k"][l, rows[i], hk].astype(np.float64) for i in range(n)])
+    Q = np.stack([a["q"][l, rows[i], hk].astype(np.float64) for i in range(n)])
+    V = np.stack([a["v"][l, rows[i], h].astype(np.float64) for i in range(n)])
+    return al, be, K, Q, V
+
+
+def pin_chain_equals_matrix_scan():
+    rng = np.random.default_rng(21)
+    wl = make_wl([trees.chain(9)], d_k=7, d_v=5, h_k=1, h_v=2)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    for h in range(2):
+        al, be, K, Q, V = _node_operands(wl, a, 0, 0, h)
+        want_o, want_s = chain_matrix_form(a["state0"][0, 0, h], al, be, K, V, Q)
+        o, st = oracle.verify_nodes(wl, 0, 0, h, list(range(9)), want_state=True)
+        np.testing.assert_allclose(o, want_o, rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(st, want_s, rtol=1e-12, atol=1e-13)
+
+
+def pin_tree_equals_wy_closed_form():
+    rng = np.random.default_rng(22)
+    par = trees.random_tree(rng, 20, 6, trees.bmax_uniform(3))
+    wl = make_wl([par, trees.FIG1_PARENT], d_k=6, d_v=5, h_k=2, h_v=4, n_layers=2,
+                 n_rows=[22, 8])
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    for (r, l, h) in [(0, 0, 0), (0, 1, 3), (1, 1, 1), (1, 0, 2)]:
+        al, be, K, Q, V = _node_operands(wl, a, r, l, h)
+        want = tree_wy_form(wl.parents[r], a["state0"][r, l, h], al, be, K, V, Q)
+        o = oracle.verify_nodes(wl, r, l, h, list(range(len(wl.parents[r]))))
+        np.testing.assert_allclose(o, want, rtol=1e-11, atol=1e-12)
+
+
+def pin_paths_equal_chain_scans():
+    """Every node's output equals the chain scan of its own root-to-node path."""
+    rng = np.random.default_rng(23)
+    par = trees.random_tree(rng, 16, 5, trees.bmax_uniform(4))
+    wl = make_wl([par], d_k=5, d_v=4)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    al, be, K, Q, V = _node_operands(wl, a, 0, 0, 0)
+    o = oracle.verify_nodes(wl, 0, 0, 0, list(range(16)))
+    for path in oracle.plan.paths(par):
+        ch_o, _ = chain_matrix_form(a["state0"][0, 0, 0], [al[x] for x in path],
+                                    [be[x] for x in path], K[path], V[path], Q[path])
+        for pos, node in enumerate(path):
+            np.testing.assert_allclose(o[node], ch_o[pos], rtol=1e-12, atol=1e-13)
+
+
+# --------------------------------------------------------------------------- invariants
+
+def pin_identical_sibling_subtrees():
+    """Two sibling subtrees carrying identical operands give bit-identical outputs."""
+    par = [-1, 0, 0, 1, 2, 3, 4, 1, 2]   # subtrees of 1 and 2 mirror each other: 1->{3,7}, 3->5; 2->{4,8}, 4->6
+    rng = np.random.default_rng(31)
+    wl = make_wl([par], d_k=6, d_v=6, h_k=1, h_v=2)
+    a = random_arrays(wl, rng)
+    rows = _rows(wl, 0)
+    for x, y in ((1, 2), (3, 4), (5, 6), (7, 8)):
+        for key in ("q", "k", "v", "g", "beta"):
+            a[key][:, rows[y]] = a[key][:, rows[x]]
+    wl.arrays = a
+    for h in range(2):
+        o = oracle.verify_nodes(wl, 0, 0, h, list(range(9)))
+        for x, y in ((1, 2), (3, 4), (5, 6), (7, 8)):
+            assert np.array_equal(o[x], o[y])
+
+
+def pin_commit_equals_node_state():
+    """Replaying the accepted path reproduces that node's verified state bit for bit."""
+    rng = np.random.default_rng(32)
+    par = trees.random_tree(rng, 12, 5, trees.bmax_uniform(3))
+    wl = make_wl([par], d_k=5, d_v=7, h_k=1, h_v=2, n_layers=2, max_path=5)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    for node in range(12):
+        st_c, po, pl = oracle.commit(wl, accepted=[node])
+        assert list(po[0][:pl[0]]) == oracle.plan.ancestry(par, node)
+        for l in range(2):
+            for h in range(2):
+                _, st = oracle.verify_nodes(wl, 0, l, h, [node], want_state=True)
+                assert np.array_equal(st_c[0, l, h], st[0])
+    st_c, po, pl = oracle.commit(wl, accepted=[-1])
+    assert pl[0] == 0 and np.all(po == -1)
+    assert np.array_equal(st_c, a["state0"].astype(np.float64))
+
+
+def pin_value_row_permutation():
+    rng = np.random.default_rng(33)
+    wl = make_wl([trees.FIG1_PARENT], d_k=5, d_v=6)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    o = oracle.verify_nodes(wl, 0, 0, 0, list(range(7)))
+    perm = rng.permutation(6)
+    b = {k: v.copy() for k, v in a.items()}
+    b["v"] = a["v"][..., perm]
+    b["state0"] = a["state0"][..., perm]
+    o2 = oracle.verify_nodes(wl, 0, 0, 0, list(range(7)), arrays=b)
+    assert np.array_equal(o2, o[:, perm])
+
+
+def pin_head_independence():
+    rng = np.random.default_rng(34)
+    wl = make_wl([trees.FIG1_PARENT], d_k=4, d_v=4, h_k=2, h_v=4)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    base = [oracle.verify_nodes(wl, 0, 0, h, list(range(7))) for h in range(4)]
+    b = {k: v.copy() for k, v in a.items()}
+    b["v"][:, :, 3] += 1.0
+    b["state0"][:, :, 3] *= 2
+    b["k"][:, :, 1] = b["k"][:, :, 1][..., ::-1].copy()   # key head 1 feeds value heads 2, 3
+    for h in range(2):
+        assert np.array_equal(oracle.verify_nodes(wl, 0, 0, h, list(range(7)), arrays=b), base[h])
+    assert not np.array_equal(oracle.verify_nodes(wl, 0, 0, 2, list(range(7)), arrays=b), base[2])
+
+
+def pin_head_grouping():
+    """Value head h reads key head h // (h_v / h_k) (contiguous groups)."""
+    rng = np.random.default_rng(35)
+    wl = make_wl([[-1, 0]], d_k=3, d_v=3, h_k=2, h_v=4)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    for h in range(4):
+        al, be, K, Q, V = _node_operands(wl, a, 0, 0, h)
+        want, _ = chain_matrix_form(a["state0"][0, 0, h], al, be, K, V, Q)
+        np.testing.assert_allclose(oracle.verify_nodes(wl, 0, 0, h, [0, 1]), want, rtol=1e-12)
+
+
+def pin_off_path_poison():
+    """NaN operands on rows off the accepted path leave the published state unchanged."""
+    rng = np.random.default_rng(36)
+    wl = make_wl([trees.FIG1_PARENT], d_k=4, d_v=4, max_path=4)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    st, po, pl = oracle.commit(wl, accepted=[4])
+    b = {k: v.copy() for k, v in a.items()}
+    rows = _rows(wl, 0)
+    for node in (2, 3, 5, 6):
+        for key in ("k", "v", "g", "beta", "q"):
+            b[key][:, rows[node]] = np.nan
+    st2, _, _ = oracle.commit(wl, accepted=[4], arrays=b)
+    assert np.array_equal(st, st2)
+
+
+def pin_fig1_worked_commit():
+    """Fig. 1: accepting d publishes S(m a d): the replay of m, a, d from S0."""
+    wl = configs.build("tiny", with_conv=False)
+    st, po, pl = oracle.commit(wl)
+    gd = load_golden("fig1_descriptor.json")
+    assert list(po[0][:pl[0]]) == gd["accepted_path"] and pl[0] == gd["accepted_len"]
+    al, be, K, Q, V = _node_operands(wl, wl.arrays, 0, 0, 0)
+    p = gd["accepted_path"]
+    _, states = chain_matrix_form(wl.arrays["state0"][0, 0, 0], [al[x] for x in p],
+                                  [be[x] for x in p], K[p], V[p], Q[p])
+    np.testing.assert_allclose(st[0, 0, 0], states[-1], rtol=1e-12, atol=1e-13)
+
+
+# --------------------------------------------------------------------------- convolution
+
+def _conv_wl(par, C=5, n_layers=1):
+    wl = make_wl([par], d_k=1, d_v=1, channels=C, n_layers=n_layers)
+    rng = np.random.default_rng(41)
+    wl.arrays = dict(x=rng.standard_normal((n_layers, wl.total_rows, C)).astype(np.float32),
+                     hist=rng.standard_normal((1, n_layers, 3, C)).astype(np.float32),
+                     w=rng.uniform(-0.5, 0.5, (n_layers, C, 4)).astype(np.float32))
+    return wl
+
+
+def pin_conv_identity_tap():
+    wl = _conv_wl(trees.FIG1_PARENT)
+    wl.arrays["w"][:] = np.array([0, 0, 0, 1], np.float32)
+    y = oracle.conv_all(wl, act=0)
+    rows = _rows(wl, 0)
+    for i in range(7):
+        assert np.array_equal(y[0, rows[i]], wl.arrays["x"][0, rows[i]].astype(np.float64))
+
+
+def pin_conv_oldest_tap_indexing():
+    """Tap 0 sees the third ancestor, or committed history entry `depth` when shallower."""
+    wl = _conv_wl(trees.FIG1_PARENT)
+    wl.arrays["w"][:] = np.array([1, 0, 0, 0], np.float32)
+    y = oracle.conv_all(wl, act=0)
+    rows = _rows(wl, 0)
+    d = trees.depths(trees.FIG1_PARENT)
+    for i in range(7):
+        if d[i] >= 3:
+            want = wl.arrays["x"][0, rows[oracle.plan.ancestry(trees.FIG1_PARENT, i)[-4]]]
+        else:
+            want = wl.arrays["hist"][0, 0, d[i]]
+        assert np.array_equal(y[0, rows[i]], want.astype(np.float64))
+
+
+def pin_conv_chain_equals_numpy_convolve():
+    n = 9
+    wl = _conv_wl(trees.chain(n), C=3, n_layers=2)
+    bias = np.random.default_rng(42).standard_normal((2, 3)).astype(np.float32)
+    y = oracle.conv_all(wl, act=0, bias=bias)
+    rows = _rows(wl, 0)
+    for l in range(2):
+        for c in range(3):
+            seq = np.concatenate([wl.arrays["hist"][0, l, :, c],
+                                  wl.arrays["x"][l, rows, c]]).astype(np.float64)
+            taps = wl.arrays["w"][l, c].astype(np.float64)
+            full = np.convolve(seq, taps[::-1], mode="full")[3:3 + n] + bias[l, c]
+            np.testing.assert_allclose(y[l, rows, c], full, rtol=1e-13, atol=1e-14)
+
+
+def pin_conv_silu():
+    wl = _conv_wl(trees.chain(3), C=4)
+    y0 = oracle.conv_all(wl, act=0)
+    y1 = oracle.conv_all(wl, act=1)
+    rows = _rows(wl, 0)
+    z = y0[0, rows]
+    np.testing.assert_allclose(y1[0, rows], z * 0.5 * (1 + np.tanh(z / 2)), rtol=1e-13, atol=1e-15)
+
+
+def pin_conv_hist_publish():
+    wl = _conv_wl(trees.FIG1_PARENT, C=3)
+    rows = _rows(wl, 0)
+    for acc, L in ((-1, 0), (0, 1), (1, 2), (4, 3), (6, 4)):
+        path, plen = oracle.plan.accepted_path(trees.FIG1_PARENT, acc, 4)
+        out = oracle.conv_hist_publish(wl, np.array([path]), np.array([plen]))
+        seq = list(wl.arrays["hist"][0, 0]) + [wl.arrays["x"][0, rows[x]] for x in path[:plen]]
+        assert plen == L
+        assert np.array_equal(out[0, 0], np.array(seq[-3:], np.float64))
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]

@@ -1,0 +1,66 @@
+"""Plant plausible mistakes in copies of the oracle and check that a pin trips.
+
+Each mutation edits one expression of oracle/lumo_oracle.c (a dropped term, a wrong
+sign, a wrong index, a transposed operand, a reversed tap order, a skipped node),
+compiles the copy with gcc into a temporary directory and runs every pin against it.
+The real oracle is never modified.
+"""
+import os
+import shutil
+import subprocess
+
+import pytest
+
+import oracle
+import pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "lumo_oracle.c")
+
+MUTATIONS = {
+    "drop_decay": ("for (long e = 0; e < (long)dv * dk; ++e) R[e] *= a;",
+                   "for (long e = 0; e < (long)dv * dk; ++e) R[e] *= 1.0;"),
+    "drop_beta": ("Rk[j] = b * (vv[j] - s);", "Rk[j] = (vv[j] - s);"),
+    "sign_flip": ("Rk[j] = b * (vv[j] - s);", "Rk[j] = b * (vv[j] + s);"),
+    "decay_after_dot": ("    /* R' = alpha R */\n    for (long e = 0; e < (long)dv * dk; ++e) R[e] *= a;\n",
+                        "    for (long e = 0; e < (long)dv * dk; ++e) R[e] *= 1.0;\n"),
+    "transposed_state": ("R[(long)j * d->d_k + i] = (double)state[base + (long)i * d->d_v + j];",
+                         "R[(long)j * d->d_k + i] = (double)state[base + (long)j * d->d_k + i];"),
+    "head_modulo": ("const int hk = h / (d->h_v / d->h_k);\n    const long kb",
+                    "const int hk = h % d->h_k;\n    const long kb"),
+    "skip_root_update": ("for (int p = 0; p < len; ++p)\n            gdn_node_update(",
+                         "for (int p = 1; p < len; ++p)\n            gdn_node_update("),
+    "output_from_parent": ("for (int j = 0; j < dv; ++j)\n        for (int i = 0; i < dk; ++i) R[(long)j * dk + i] += Rk[j] * kv[i];",
+                           "for (int j = 0; j < dv; ++j)\n        for (int i = 0; i < dk; ++i) R[(long)j * dk + i] += 0.0 * Rk[j] * kv[i];"),
+    "query_head_zero": ("const long qb = (((long)l * d->total_rows + row) * d->h_k + hk) * dk;",
+                        "const long qb = (((long)l * d->total_rows + row) * d->h_k + 0) * dk;"),
+    "query_row_of_parent": ("gdn_output(d, s.R, l, row[targets[t]], h,",
+                            "gdn_output(d, s.R, l, row[s.path[len > 1 ? len - 2 : 0]], h,"),
+    "reversed_taps": ("acc += (double)w[((long)l * channels + c) * 4 + t] * xv;",
+                      "acc += (double)w[((long)l * channels + c) * 4 + (3 - t)] * xv;"),
+    "window_off_by_one": ("const int pos = 3 + len - 4 + t;", "const int pos = 3 + len - 3 + t;"),
+    "hist_publish_shift": ("const int pos = L + e;", "const int pos = L + e - 1 < 0 ? 0 : L + e - 1;"),
+    "commit_skips_last": ("for (int p = 0; p < path_len[r]; ++p)", "for (int p = 0; p + 1 < path_len[r]; ++p)"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_mutation_is_caught(tmp_path, name):
+    old, new = MUTATIONS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique/found"
+    mutated = tmp_path / "mut.c"
+    mutated.write_text(src.replace(old, new))
+    so = tmp_path / "libmut.so"
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-o",
+                           str(so), str(mutated), "-lm"])
+    caught = []
+    oracle.use_library(str(so))
+    try:
+        for pin in pins.ALL_PINS:
+            try:
+                pin()
+            except (AssertionError, ValueError):
+                caught.append(pin.__name__)
+    finally:
+        oracle.use_library(None)
+    assert caught, f"no pin detects mutation {name}"
