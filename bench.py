@@ -1,0 +1,208 @@
+"""Benchmark of one speculative verification step of tree GDN on one MI355X.
+
+A step is one pass of the whole hot path over the batch: tree causal-conv gather,
+path verification of every node, and publication of the accepted path (device path
+derivation, replay into the native state, conv-history update). Consecutive steps
+form a serving loop: each verify reads the state the previous commit published.
+
+Prints one JSON line: head-node updates per second (tree nodes x layers x value
+heads, each node counted once), the roofline of the dominant kernel (verify) with
+its duration measured by HIP events on the launch stream, the other kernels'
+durations, and the fp64 CPU oracle timed on a bounded sample of the same workload.
+
+  python bench.py [--steps K] [--warmup W] [--config batched] [--policy paths]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tree GDN head-node updates/sec + % of HBM/VALU roofline, 1 MI355X"
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, published
+PEAK_VALU_F32_TFS = 157.3      # MI355X fp32 vector, published (256 CU x 2.4 GHz)
+
+WORKLOAD_TEXT = {
+    "tiny": "Fig. 1 tree, 1 request, 1 head, d=16, fp32 operands",
+    "layer1": "1 request x 1 GDN layer x 32 value heads (16 key heads), d_k=d_v=128, one 64-node tree (depth<=8, branching 1-4), bf16 operands, fp32 state",
+    "batched": "8 requests x 48 GDN layers x 32 value heads (16 key heads), d_k=d_v=128, per-request 64-node trees (depth<=8, branching 1-4), bf16 operands, fp32 state, commit of accepted paths of length 1-8, conv C=8192",
+    "widedeep": "32 requests x 1 layer x 32 value heads, d=128, 256-node trees (depth<=16, root-skewed branching 1-6), bf16 operands",
+    "chainmix": "64 requests x 1 layer x 32 value heads, d=128: 32 chains of 16 + 32 trees of 128 nodes, bf16 operands, accepted lengths 0-16",
+    "paper28": "1 request x 1 layer x 32 value heads, d=128, the 28-node draft geometry padded to 32 rows",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def alg_bytes_flops(wl):
+    """Algorithmic HBM bytes and flops of verify, commit and conv for one step."""
+    opb = 4 if wl.op_dtype == 0 else 2
+    grp = wl.h_v // wl.h_k
+    hn = wl.head_node_updates
+    mat = wl.d_k * wl.d_v * 4
+    inst = wl.n_req * wl.n_layers * wl.h_v
+    per_hn = (2 * wl.d_k * opb) / grp + wl.d_v * opb + 8 + wl.d_v * opb  # q,k shared; v; g,beta; o
+    v_bytes = hn * per_hn + inst * mat
+    v_flops = hn * 6 * wl.d_k * wl.d_v
+    plen = sum(min(int(oracle_depth(p, a)), wl.max_path) for p, a in zip(wl.parents, wl.accepted))
+    c_upd = plen * wl.n_layers * wl.h_v
+    active = sum(1 for p, a in zip(wl.parents, wl.accepted) if a >= 0)
+    c_bytes = active * wl.n_layers * wl.h_v * 2 * mat + c_upd * ((wl.d_k * opb) / grp + wl.d_v * opb + 8)
+    c_flops = c_upd * 4 * wl.d_k * wl.d_v
+    conv_bytes = wl.total_nodes * wl.n_layers * wl.channels * opb * 2 + wl.n_layers * wl.channels * 16
+    return dict(verify_bytes=v_bytes, verify_flops=v_flops, commit_bytes=c_bytes,
+                commit_flops=c_flops, conv_bytes=conv_bytes, commit_updates=c_upd)
+
+
+def oracle_depth(parent, a):
+    if a < 0:
+        return 0
+    d, x = 0, int(a)
+    while x != -1:
+        d += 1
+        x = int(parent[x])
+    return d
+
+
+def cpu_baseline(wl, budget_s=12.0):
+    """fp64 oracle (conv + verify + commit) on the first k layers of the workload, k chosen
+    so that the run takes about budget_s seconds; scaled to head-node updates/s."""
+    import numpy as np
+
+    import oracle
+    from lumo_synth import configs
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+
+    def sub(k):
+        a = wl.arrays
+        arr = {"q": a["q"][:k], "k": a["k"][:k], "v": a["v"][:k], "g": a["g"][:k],
+               "beta": a["beta"][:k], "state0": np.ascontiguousarray(a["state0"][:, :k]),
+               "x": a["x"][:k], "hist": np.ascontiguousarray(a["hist"][:, :k]), "w": a["w"][:k]}
+        return configs.Workload(**{**wl.__dict__, "n_layers": k, "arrays": arr})
+
+    def run(k):
+        w = sub(k)
+        t0 = time.perf_counter()
+        oracle.conv_all(w)
+        oracle.verify_all(w, n_threads=threads)
+        oracle.commit(w, n_threads=threads)
+        return time.perf_counter() - t0, w.head_node_updates
+
+    t1, hn1 = run(1)
+    k = 1
+    if t1 < budget_s and wl.n_layers > 1:
+        k = int(min(wl.n_layers, max(1, budget_s // max(t1, 1e-3))))
+        t1, hn1 = run(k) if k > 1 else (t1, hn1)
+    return {"value": hn1 / t1, "unit": "head-node updates/s", "cores": threads, "kind": "oracle",
+            "sample": f"conv + verify + commit of {k} of {wl.n_layers} layers "
+                      f"({hn1} head-node updates), all requests and heads, {t1:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="batched")
+    ap.add_argument("--policy", default="paths")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the step shards "
+              "by request with no cross-GPU exchange; see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_23900_amd as L
+    from paper_2609_23900_amd.step import GdnTreeStep
+    from lumo_synth import configs
+
+    policy = L.POLICIES[args.policy]
+    log(f"[bench] generating {args.config}")
+    wl = configs.build(args.config)
+    log(f"[bench] uploading; policy {args.policy}")
+    st = GdnTreeStep.from_workload(wl, policy=policy, keep_state0=False)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        st.conv(stream)
+        if ev is not None:
+            ev[1].record(stream)
+        st.verify(stream)
+        if ev is not None:
+            ev[2].record(stream)
+        st.commit(stream)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done; timing {args.steps} steps")
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    conv_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    ver_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+    com_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
+    ms_step = total_ms / args.steps
+    log(f"[bench] step {ms_step:.3f} ms (conv {conv_ms:.3f}, verify {ver_ms:.3f}, commit {com_ms:.3f})")
+    assert torch.isfinite(st.state).all().item(), "non-finite state"
+
+    ab = alg_bytes_flops(wl)
+    hn = wl.head_node_updates
+    if policy == L.LUMO_POLICY_WY:
+        ach = ab["verify_bytes"] / (ver_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
+    else:
+        ach = ab["verify_flops"] / (ver_ms * 1e-3) / 1e12
+        roof = {"bound": "alu", "achieved": round(ach, 2), "peak": PEAK_VALU_F32_TFS,
+                "unit": "TFLOP/s", "frac": round(ach / PEAK_VALU_F32_TFS, 4), "traffic": None}
+    roof["kernel"] = "verify"
+    roof["per_launch"] = (f"{ab['verify_flops'] / 1e9:.2f} GFLOP, {ab['verify_bytes'] / 1e6:.1f} MB "
+                          f"algorithmic per verify call")
+    kernels = {
+        "conv_gather_ms": round(conv_ms, 4),
+        "conv_hbm_frac": round(ab["conv_bytes"] / (conv_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "verify_ms": round(ver_ms, 4),
+        "commit_ms": round(com_ms, 4),
+        "commit_hbm_frac": round(ab["commit_bytes"] / (com_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+    }
+    out = {
+        "metric": METRIC, "value": round(hn / (ms_step * 1e-3), 1), "unit": "head-node updates/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded trees and operands shaped like the paper's workloads)",
+        "config": {"workload": f"{args.config}: {WORKLOAD_TEXT[args.config]}",
+                   "policy": args.policy, "head_node_updates_per_step": hn,
+                   "operands": "bf16" if wl.op_dtype == 1 else "f32"},
+        "roofline": roof, "kernels": kernels,
+    }
+    if not args.no_cpu:
+        log("[bench] CPU oracle leg")
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,254 @@
+/*
+ * lumo_tree.h - C ABI of the MI355X (gfx950) tree-verification library for the
+ * Gated DeltaNet recurrence (LumoTree, arXiv 2609.23900).
+ *
+ * One speculative-decoding step of a hybrid model's GDN layers, for a batch of
+ * requests, each carrying its own candidate tree:
+ *   lumo_tree_plan         host: validate parents, derive the tree descriptor
+ *   lumo_tree_conv_gather  device: causal conv over each node's ancestry window
+ *   lumo_tree_gdn_verify   device: every node's recurrent output from its ancestry
+ *   lumo_gdn_commit        device: derive the accepted path, replay it into the
+ *                          native state, publish the convolution history
+ * plus a captured-graph form of the commit.
+ *
+ * Conventions shared by every entry point
+ *   - Device pointers are HIP device (or managed) memory owned by the caller.
+ *     The library never allocates or frees device memory on these paths except
+ *     the graph object of lumo_gdn_commit_graph_create.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream). All
+ *     device work is enqueued on it asynchronously, with no host synchronisation,
+ *     so every device entry point can be captured into a graph.
+ *   - Arguments are validated on the host before anything is enqueued; a non-OK
+ *     status means nothing was launched. lumo_last_error() then returns a
+ *     description (thread-local, valid until the next call on that thread).
+ *   - Calls are stateless and thread-safe.
+ *
+ * Tensor layouts (rows are physical rows; requests are concatenated, request r
+ * owns rows [row_off[r], row_off[r+1]); node i of request r lives at row
+ * row_off[r] + slot[i]; rows beyond a request's nodes are padding and are never
+ * read or written):
+ *   q, k        [n_layers][total_rows][h_k][d_k]            op_dtype
+ *   v           [n_layers][total_rows][h_v][d_v]            op_dtype
+ *   g, beta     [n_layers][total_rows][h_v]                 float32; alpha = exp(g)
+ *   state       [n_req][n_layers][h_v][d_k][d_v]            float32, key-major:
+ *                                                           entry (i, j) is R[j][i]
+ *   o           [n_layers][total_rows][h_v][d_v]            op_dtype
+ *   x, y        [n_layers][total_rows][channels]            op_dtype
+ *   conv_hist   [n_req][n_layers][3][channels]              op_dtype, oldest first
+ *   w           [n_layers][channels][4]                     float32, tap 3 = newest
+ *   bias        [n_layers][channels]                        float32
+ * Value head h reads key head h / (h_v / h_k).
+ */
+#ifndef LUMO_TREE_H
+#define LUMO_TREE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    LUMO_OK = 0,
+    LUMO_EINVAL = 1,       /* null / misaligned pointer, bad scalar argument      */
+    LUMO_EDESC = 2,        /* malformed tree (parents, rows) or plan mismatch     */
+    LUMO_ESHAPE = 3,       /* dims inconsistent with each other or with the plan  */
+    LUMO_EUNSUPPORTED = 4, /* head size / dtype / option not built                */
+    LUMO_EHIP = 5,         /* a HIP call or kernel launch failed                  */
+    LUMO_ESPACE = 6        /* caller buffer (plan words, workspace) too small     */
+} lumo_status;
+
+typedef enum { LUMO_F32 = 0, LUMO_BF16 = 1 } lumo_dtype;
+
+/* Verification schedules (Sec. IV-A, IV-C). All produce the same outputs. */
+typedef enum {
+    /* Dependent path groups: the tree is cut into disjoint first-child chains; a
+     * chain starts from the pre-tree state (the spine) or from the exported cut
+     * state of its parent; chains are launched level by level (one launch per
+     * dependency level), each node is updated once. Needs a workspace. */
+    LUMO_POLICY_PATHS = 0,
+    /* The paper's two launches: the spine exports the cut states of its branch
+     * nodes; every other root-to-leaf path then runs from its spine cut state,
+     * recomputing off-spine prefixes it shares with other paths. Needs a workspace. */
+    LUMO_POLICY_TWO_LEVEL = 1,
+    /* Every root-to-leaf path from the pre-tree state in one launch; no cut
+     * states, shared prefixes recomputed. No workspace. */
+    LUMO_POLICY_RECOMPUTE = 2,
+    /* Tree WY form: R_t = gamma_t R0 + sum over ancestors of decayed rank-1
+     * terms; the R0 [K | Q] products run on MFMA (bf16 split in three), the
+     * ancestor-masked triangular system on the vector units. One launch, no
+     * workspace, no state dump. bf16 operands only. */
+    LUMO_POLICY_WY = 3
+} lumo_policy;
+
+typedef struct {
+    int32_t n_req;    /* requests in the batch                                  */
+    int32_t n_layers; /* stacked GDN layers (independent instances)            */
+    int32_t h_k;      /* query/key heads                                        */
+    int32_t h_v;      /* value heads; h_v % h_k == 0                            */
+    int32_t d_k;      /* key dim: 16, 32, 64 or 128                             */
+    int32_t d_v;      /* value dim: 16, 32, 64 or 128                           */
+    int32_t op_dtype; /* lumo_dtype of q, k, v, o, x, y, conv_hist              */
+} lumo_gdn_dims;
+
+/* Host summary of a plan: counts and the word offsets of every section of the
+ * int32 plan blob. Filled by lumo_tree_plan; read-only for the caller. */
+typedef struct {
+    int32_t n_req, total_nodes, total_rows;
+    int32_t max_nodes; /* most nodes in one request                           */
+    int32_t max_depth; /* most nodes on one root-to-leaf path                 */
+    int32_t policy;
+    int32_t n_paths;   /* leaves over all requests                            */
+    int32_t n_spine;   /* spine nodes over all requests                       */
+    int32_t n_seg, n_seg_nodes, n_levels, n_cuts, max_level_seg, max_seg_len;
+    int32_t n_words;   /* blob size in int32 words                            */
+    /* section offsets (int32 words) inside the blob */
+    int32_t o_node_off, o_row_off, o_req, o_parent, o_depth, o_slot, o_row, o_conv_src;
+    int32_t o_path_off, o_path_leaf, o_spine_off, o_spine, o_level_off, o_seg, o_seg_nodes;
+} lumo_plan;
+
+/* A plan whose blob has been copied to device memory. */
+typedef struct {
+    const int32_t* blob;      /* device copy of the lumo_tree_plan words              */
+    const int32_t* host_blob; /* host copy of the same words; read only during a call
+                                 (level boundaries of the schedule), never by kernels  */
+    lumo_plan plan;           /* the host summary returned with those words           */
+} lumo_tree_desc;
+
+/*
+ * lumo_tree_plan - validate candidate trees and derive the shared tree descriptor
+ * (Sec. III-C; spine-first slots Sec. V-B; path groups Sec. IV-A, Alg. 2; cut
+ * states Sec. IV-C, Eq. (4); conv gather sources Sec. V-C).
+ *
+ *   n_req        requests (>= 0)
+ *   node_off     host [n_req+1]: request r owns flat nodes [node_off[r], node_off[r+1])
+ *   parent       host [node_off[n_req]]: request-local parent ids; node 0 of a
+ *                non-empty request is its root (-1); otherwise 0 <= parent[i] < i
+ *   n_rows       host [n_req]: physical rows of request r (>= its node count)
+ *   policy       lumo_policy whose schedule the plan carries
+ *   blob         host int32 words receiving the plan, or NULL to query the size
+ *   blob_words   capacity of blob in words
+ *   out          host summary (always filled on LUMO_OK / LUMO_ESPACE)
+ *
+ * Derived per request (bit-exact, fully determined):
+ *   depth (root 0); leaves in increasing id; root-to-leaf paths; spine = the
+ *   first-child chain from the root (children ordered by id); slot = physical
+ *   order spine first, then the remaining nodes in increasing id; per node the
+ *   four conv window sources oldest first (absolute row, or -1-h for committed
+ *   history entry h); the verify schedule of `policy`.
+ * Blob sections (words; see the o_* offsets):
+ *   node_off[n_req+1], row_off[n_req+1], req[N], parent[N], depth[N], slot[N],
+ *   row[N] (absolute), conv_src[N][4], path_off[n_req+1], path_leaf[n_paths],
+ *   spine_off[n_req+1], spine[n_spine], level_off[n_levels+1],
+ *   seg[n_seg][4] = {request, source cut (-1 = pre-tree state), first entry, length},
+ *   seg_nodes[n_seg_nodes][3] = {absolute row, writes output (0/1), cut to export (-1 none)}.
+ * Returns LUMO_EDESC for malformed trees, LUMO_ESPACE (with out->n_words set)
+ * when blob is NULL or too small, LUMO_EINVAL for bad arguments.
+ */
+lumo_status lumo_tree_plan(int32_t n_req, const int32_t* node_off, const int32_t* parent,
+                           const int32_t* n_rows, int32_t policy, int32_t* blob,
+                           int64_t blob_words, lumo_plan* out);
+
+/*
+ * lumo_tree_gdn_workspace_bytes - device workspace needed by lumo_tree_gdn_verify
+ * for this plan: one fp32 d_k x d_v matrix per (exported cut, layer, value head)
+ * (the cut-state payload of Eq. (4), Sec. IV-C). 0 for RECOMPUTE and WY.
+ */
+size_t lumo_tree_gdn_workspace_bytes(const lumo_gdn_dims* dims, const lumo_plan* plan);
+
+/*
+ * lumo_tree_conv_gather - tree causal convolution (Sec. V-C, Tab. II row 3).
+ * For node i at depth j of request r, layer l, channel c, the window is the last
+ * four entries of (conv_hist[r][l][0..2], x along the root-to-i ancestry):
+ *   y[l][row(i)][c] = act(bias[l][c] + sum_{t=0..3} w[l][c][t] * window[t][c])
+ * accumulated in fp32 in tap order 0..3 starting from the bias, then the
+ * activation, then one round-to-nearest-even cast to op_dtype.
+ *   channels  multiple of 8; x, y, conv_hist 16-byte aligned
+ *   bias      nullable (zero); act 0 = identity, 1 = SiLU
+ * Pad rows of y are not written.
+ */
+lumo_status lumo_tree_conv_gather(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                  int32_t channels, const void* x, const void* conv_hist,
+                                  const float* w, const float* bias, int32_t act, void* y,
+                                  void* stream);
+
+/*
+ * lumo_tree_gdn_verify - recurrent output of every tree node (Sec. III-B,
+ * Eq. (2)-(3); path-parallel scan Sec. IV-A, Alg. 2). For each request r, layer l,
+ * value head h and node i, with R_pi the state after the root-to-parent path
+ * (R = pre-tree state state0[r][l][h] for the root's parent):
+ *   R'_i = alpha_i R_pi;  delta_i = beta_i (v_i - R'_i k_i);
+ *   R_i = R'_i + delta_i k_i^T;  o_i = R_i q_i     (alpha_i = exp(g_i))
+ * computed with fp32 state and fp32 arithmetic; o is cast once (RNE) to op_dtype.
+ *   state0        pre-tree state; never written
+ *   o             written at every node row; pad rows untouched
+ *   node_states   nullable debug dump [n_layers][total_rows][h_v][d_k][d_v] fp32:
+ *                 the state R_i of every node (key-major) at its row. Bitwise equal
+ *                 to what lumo_gdn_commit publishes for a path ending at that node.
+ *                 Not available with LUMO_POLICY_WY (LUMO_EUNSUPPORTED).
+ *   workspace     >= lumo_tree_gdn_workspace_bytes() bytes (nullable when 0)
+ *   flags         reserved, must be 0
+ * The schedule is the policy the plan was built for.
+ */
+lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                 const void* q, const void* k, const void* v, const float* g,
+                                 const float* beta, const float* state0, void* o,
+                                 float* node_states, void* workspace, size_t workspace_bytes,
+                                 int32_t flags, void* stream);
+
+/*
+ * lumo_gdn_commit - publish the accepted path (Alg. 1 publication; Alg. 2 replay;
+ * device-selected path Sec. V-A; conv history Sec. V-C).
+ *   accepted_node  device [n_req]: request-local accepted node, -1 = none
+ *   max_path       fixed path capacity (1..4096); the work shape depends only on it
+ *   path_out       device [n_req][max_path]: root-first accepted path, padded -1
+ *   path_len       device [n_req]: its length; -1 when accepted_node[r] is not in
+ *                  [-1, nodes of r) or the path is longer than max_path (then the
+ *                  state and history of request r are left unchanged)
+ *   k, v, g, beta  the operands recorded for verification (q is not needed)
+ *   state          in/out: the pre-tree state, replaced in place by the state after
+ *                  replaying the path with the update of lumo_tree_gdn_verify
+ *                  (bitwise the same arithmetic); untouched for an empty path
+ *   x, conv_hist   nullable pair: when given, conv_hist[r][l] becomes the last
+ *                  three entries of (conv_hist[r][l], x rows of the path), in place
+ */
+lumo_status lumo_gdn_commit(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                            int32_t max_path, const int32_t* accepted_node, int32_t* path_out,
+                            int32_t* path_len, const void* k, const void* v, const float* g,
+                            const float* beta, float* state, int32_t channels, const void* x,
+                            void* conv_hist, void* stream);
+
+/* Opaque captured commit (Sec. V-A: one fixed-shape committer graph). */
+typedef struct lumo_commit_graph lumo_commit_graph;
+
+/*
+ * lumo_gdn_commit_graph_create - capture the launches of lumo_gdn_commit with
+ * these exact arguments into an instantiated HIP graph. Device buffers are bound
+ * by address: replays read the current contents of accepted_node (and every
+ * operand) at launch time. The caller keeps all buffers alive until destroy.
+ */
+lumo_status lumo_gdn_commit_graph_create(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                         int32_t max_path, const int32_t* accepted_node,
+                                         int32_t* path_out, int32_t* path_len, const void* k,
+                                         const void* v, const float* g, const float* beta,
+                                         float* state, int32_t channels, const void* x,
+                                         void* conv_hist, lumo_commit_graph** out);
+
+/* Replay the captured commit on `stream`. */
+lumo_status lumo_gdn_commit_graph_launch(lumo_commit_graph* graph, void* stream);
+
+/* Release the graph (NULL is ignored). */
+void lumo_gdn_commit_graph_destroy(lumo_commit_graph* graph);
+
+/* Description of the last non-OK status returned on this thread ("" if none). */
+const char* lumo_last_error(void);
+
+/* Library version string. */
+const char* lumo_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LUMO_TREE_H */

@@ -1,0 +1,235 @@
+"""Python binding of liblumo_tree.so (tree verification of the Gated DeltaNet recurrence
+on MI355X / gfx950). Argument marshalling only: every step runs in the library's HIP
+kernels; torch tensors only provide device memory and the current HIP stream.
+
+The functions keep the names of the C ABI (include/lumo_tree.h):
+  lumo_tree_plan, lumo_tree_gdn_workspace_bytes, lumo_tree_conv_gather,
+  lumo_tree_gdn_verify, lumo_gdn_commit, lumo_gdn_commit_graph_create,
+  lumo_gdn_commit_graph_launch, lumo_gdn_commit_graph_destroy, lumo_last_error,
+  lumo_version.
+Device arguments are torch tensors on the GPU (or None where the ABI allows NULL);
+host arguments are numpy int32 arrays. A non-OK status raises LumoError.
+
+Importing this module loads the library and fails if it has not been built
+(python -m paper_2609_23900_amd.build); there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch  # loads the process's HIP runtime before the library binds to it
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "liblumo_tree.so")
+
+LUMO_OK, LUMO_EINVAL, LUMO_EDESC, LUMO_ESHAPE, LUMO_EUNSUPPORTED, LUMO_EHIP, LUMO_ESPACE = range(7)
+LUMO_F32, LUMO_BF16 = 0, 1
+LUMO_POLICY_PATHS, LUMO_POLICY_TWO_LEVEL, LUMO_POLICY_RECOMPUTE, LUMO_POLICY_WY = range(4)
+POLICIES = {"paths": 0, "two_level": 1, "recompute": 2, "wy": 3}
+STATUS_NAMES = ("LUMO_OK", "LUMO_EINVAL", "LUMO_EDESC", "LUMO_ESHAPE", "LUMO_EUNSUPPORTED",
+                "LUMO_EHIP", "LUMO_ESPACE")
+
+
+class LumoError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES[status] if 0 <= status < 7 else status}: {msg}")
+        self.status = status
+
+
+class lumo_gdn_dims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("n_req", "n_layers", "h_k", "h_v", "d_k", "d_v", "op_dtype")]
+
+
+_PLAN_FIELDS = ("n_req", "total_nodes", "total_rows", "max_nodes", "max_depth", "policy",
+                "n_paths", "n_spine", "n_seg", "n_seg_nodes", "n_levels", "n_cuts",
+                "max_level_seg", "max_seg_len", "n_words", "o_node_off", "o_row_off", "o_req",
+                "o_parent", "o_depth", "o_slot", "o_row", "o_conv_src", "o_path_off",
+                "o_path_leaf", "o_spine_off", "o_spine", "o_level_off", "o_seg", "o_seg_nodes")
+
+
+class lumo_plan(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in _PLAN_FIELDS]
+
+
+class lumo_tree_desc(ctypes.Structure):
+    _fields_ = [("blob", ctypes.c_void_p), ("host_blob", ctypes.c_void_p), ("plan", lumo_plan)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2609_23900_amd.build` "
+                          "(hipcc, gfx950); there is no fallback implementation")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    PD = ctypes.POINTER(lumo_gdn_dims)
+    PT = ctypes.POINTER(lumo_tree_desc)
+    L.lumo_tree_plan.argtypes = [I32, P, P, P, I32, P, I64, ctypes.POINTER(lumo_plan)]
+    L.lumo_tree_gdn_workspace_bytes.argtypes = [PD, ctypes.POINTER(lumo_plan)]
+    L.lumo_tree_gdn_workspace_bytes.restype = SZ
+    L.lumo_tree_conv_gather.argtypes = [PD, PT, I32, P, P, P, P, I32, P, P]
+    L.lumo_tree_gdn_verify.argtypes = [PD, PT, P, P, P, P, P, P, P, P, P, SZ, I32, P]
+    L.lumo_gdn_commit.argtypes = [PD, PT, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
+    L.lumo_gdn_commit_graph_create.argtypes = [PD, PT, I32, P, P, P, P, P, P, P, P, I32, P, P,
+                                               ctypes.POINTER(ctypes.c_void_p)]
+    L.lumo_gdn_commit_graph_launch.argtypes = [P, P]
+    L.lumo_gdn_commit_graph_destroy.argtypes = [P]
+    L.lumo_gdn_commit_graph_destroy.restype = None
+    L.lumo_last_error.restype = ctypes.c_char_p
+    L.lumo_version.restype = ctypes.c_char_p
+    for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_gdn_verify",
+              "lumo_gdn_commit", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
+        getattr(L, f).restype = ctypes.c_int
+    return L
+
+
+_lib = _load()
+
+
+def lumo_last_error() -> str:
+    return _lib.lumo_last_error().decode()
+
+
+def lumo_version() -> str:
+    return _lib.lumo_version().decode()
+
+
+def _check(st: int):
+    if st != LUMO_OK:
+        raise LumoError(st, lumo_last_error())
+
+
+def _dptr(t):
+    """Device pointer of a tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("device arguments must be torch tensors")
+    if not t.is_cuda:
+        raise ValueError("device argument is not on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("device argument must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _hptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def dims(n_req, n_layers, h_k, h_v, d_k, d_v, op_dtype) -> lumo_gdn_dims:
+    return lumo_gdn_dims(n_req, n_layers, h_k, h_v, d_k, d_v, op_dtype)
+
+
+def lumo_tree_plan(node_off, parent, n_rows, policy=LUMO_POLICY_PATHS):
+    """Host planner. Returns (plan summary, int32 numpy blob)."""
+    node_off = np.ascontiguousarray(node_off, dtype=np.int32)
+    parent = np.ascontiguousarray(parent, dtype=np.int32)
+    n_rows = np.ascontiguousarray(n_rows, dtype=np.int32)
+    n_req = int(node_off.shape[0]) - 1
+    plan = lumo_plan()
+    st = _lib.lumo_tree_plan(n_req, _hptr(node_off), _hptr(parent) if parent.size else None,
+                             _hptr(n_rows) if n_rows.size else None, int(policy), None, 0,
+                             ctypes.byref(plan))
+    if st != LUMO_ESPACE:
+        _check(st)
+    blob = np.zeros(max(plan.n_words, 1), dtype=np.int32)
+    _check(_lib.lumo_tree_plan(n_req, _hptr(node_off), _hptr(parent) if parent.size else None,
+                               _hptr(n_rows) if n_rows.size else None, int(policy), _hptr(blob),
+                               blob.shape[0], ctypes.byref(plan)))
+    return plan, blob
+
+
+class TreeDesc:
+    """A plan plus its device copy (keeps both buffers alive)."""
+
+    def __init__(self, plan: lumo_plan, blob: np.ndarray, device="cuda"):
+        self.plan = plan
+        self.host = np.ascontiguousarray(blob, dtype=np.int32)
+        self.dev = torch.from_numpy(self.host).to(device)
+        self.desc = lumo_tree_desc(ctypes.c_void_p(self.dev.data_ptr()), _hptr(self.host), plan)
+
+    @classmethod
+    def build(cls, node_off, parent, n_rows, policy=LUMO_POLICY_PATHS, device="cuda"):
+        plan, blob = lumo_tree_plan(node_off, parent, n_rows, policy)
+        return cls(plan, blob, device)
+
+    def section(self, name, count):
+        off = getattr(self.plan, "o_" + name)
+        return self.host[off:off + count]
+
+
+def lumo_tree_gdn_workspace_bytes(d: lumo_gdn_dims, plan: lumo_plan) -> int:
+    return int(_lib.lumo_tree_gdn_workspace_bytes(ctypes.byref(d), ctypes.byref(plan)))
+
+
+def lumo_tree_conv_gather(d, desc: TreeDesc, channels, x, conv_hist, w, bias, act, y, stream=None):
+    _check(_lib.lumo_tree_conv_gather(ctypes.byref(d), ctypes.byref(desc.desc), int(channels),
+                                      _dptr(x), _dptr(conv_hist), _dptr(w), _dptr(bias), int(act),
+                                      _dptr(y), _stream(stream)))
+
+
+def lumo_tree_gdn_verify(d, desc: TreeDesc, q, k, v, g, beta, state0, o, node_states=None,
+                         workspace=None, flags=0, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib.lumo_tree_gdn_verify(ctypes.byref(d), ctypes.byref(desc.desc), _dptr(q), _dptr(k),
+                                     _dptr(v), _dptr(g), _dptr(beta), _dptr(state0), _dptr(o),
+                                     _dptr(node_states), _dptr(workspace), ws_bytes, int(flags),
+                                     _stream(stream)))
+
+
+def lumo_gdn_commit(d, desc: TreeDesc, max_path, accepted_node, path_out, path_len, k, v, g, beta,
+                    state, channels=0, x=None, conv_hist=None, stream=None):
+    _check(_lib.lumo_gdn_commit(ctypes.byref(d), ctypes.byref(desc.desc), int(max_path),
+                                _dptr(accepted_node), _dptr(path_out), _dptr(path_len), _dptr(k),
+                                _dptr(v), _dptr(g), _dptr(beta), _dptr(state), int(channels),
+                                _dptr(x), _dptr(conv_hist), _stream(stream)))
+
+
+class CommitGraph:
+    """Captured fixed-shape commit (lumo_gdn_commit_graph_*)."""
+
+    def __init__(self, handle, keep):
+        self.handle = handle
+        self._keep = keep
+
+    def launch(self, stream=None):
+        lumo_gdn_commit_graph_launch(self, stream)
+
+    def close(self):
+        if self.handle:
+            lumo_gdn_commit_graph_destroy(self)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def lumo_gdn_commit_graph_create(d, desc: TreeDesc, max_path, accepted_node, path_out, path_len,
+                                 k, v, g, beta, state, channels=0, x=None, conv_hist=None):
+    h = ctypes.c_void_p()
+    _check(_lib.lumo_gdn_commit_graph_create(ctypes.byref(d), ctypes.byref(desc.desc),
+                                             int(max_path), _dptr(accepted_node), _dptr(path_out),
+                                             _dptr(path_len), _dptr(k), _dptr(v), _dptr(g),
+                                             _dptr(beta), _dptr(state), int(channels), _dptr(x),
+                                             _dptr(conv_hist), ctypes.byref(h)))
+    return CommitGraph(h, (desc, accepted_node, path_out, path_len, k, v, g, beta, state, x,
+                           conv_hist))
+
+
+def lumo_gdn_commit_graph_launch(graph: CommitGraph, stream=None):
+    _check(_lib.lumo_gdn_commit_graph_launch(graph.handle, _stream(stream)))
+
+
+def lumo_gdn_commit_graph_destroy(graph: CommitGraph):
+    _lib.lumo_gdn_commit_graph_destroy(graph.handle)
+    graph.handle = None

@@ -1,0 +1,252 @@
+// C ABI of the library: host-side validation, dispatch to the kernel launchers,
+// captured commit graphs, and error reporting. No exception crosses this boundary.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "internal.h"
+#include "launch.h"
+
+namespace lumo {
+
+namespace {
+thread_local std::string g_err;
+}
+
+lumo_status fail(lumo_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+void clear_error() { g_err.clear(); }
+
+namespace {
+
+bool pow2_head(int d) { return d == 16 || d == 32 || d == 64 || d == 128; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+lumo_status check_ptr(const void* p, const char* fn, const char* name, bool nullable = false) {
+    if (!p) return nullable ? LUMO_OK : fail(LUMO_EINVAL, "%s: %s is NULL", fn, name);
+    if (!aligned16(p)) return fail(LUMO_EINVAL, "%s: %s is not 16-byte aligned", fn, name);
+    return LUMO_OK;
+}
+
+#define LUMO_TRY(expr)                      \
+    do {                                    \
+        lumo_status st_ = (expr);           \
+        if (st_ != LUMO_OK) return st_;     \
+    } while (0)
+
+lumo_status check_dims(const lumo_gdn_dims* d, const char* fn) {
+    if (!d) return fail(LUMO_EINVAL, "%s: dims is NULL", fn);
+    if (d->n_req < 0 || d->n_layers < 1 || d->h_k < 1 || d->h_v < 1)
+        return fail(LUMO_ESHAPE, "%s: need n_req >= 0 and n_layers, h_k, h_v >= 1", fn);
+    if (d->h_v % d->h_k) return fail(LUMO_ESHAPE, "%s: h_v (%d) is not a multiple of h_k (%d)", fn, d->h_v, d->h_k);
+    if (!pow2_head(d->d_k) || !pow2_head(d->d_v))
+        return fail(LUMO_EUNSUPPORTED, "%s: d_k=%d d_v=%d (supported: 16, 32, 64, 128)", fn, d->d_k, d->d_v);
+    if (d->op_dtype != LUMO_F32 && d->op_dtype != LUMO_BF16)
+        return fail(LUMO_EUNSUPPORTED, "%s: op_dtype %d", fn, d->op_dtype);
+    return LUMO_OK;
+}
+
+lumo_status check_desc(const lumo_gdn_dims* d, const lumo_tree_desc* desc, const char* fn) {
+    if (!desc) return fail(LUMO_EINVAL, "%s: desc is NULL", fn);
+    const lumo_plan& p = desc->plan;
+    if (p.n_req != d->n_req)
+        return fail(LUMO_EDESC, "%s: plan has %d requests, dims %d", fn, p.n_req, d->n_req);
+    if (p.n_words <= 0 || p.total_nodes < 0 || p.total_rows < p.total_nodes)
+        return fail(LUMO_EDESC, "%s: malformed plan summary", fn);
+    if (!desc->blob || !desc->host_blob) return fail(LUMO_EINVAL, "%s: desc blob pointers are NULL", fn);
+    if (p.o_seg_nodes + kSegNodeWords * (int64_t)p.n_seg_nodes > p.n_words)
+        return fail(LUMO_EDESC, "%s: plan offsets exceed its size", fn);
+    return LUMO_OK;
+}
+
+}  // namespace
+}  // namespace lumo
+
+using namespace lumo;
+
+extern "C" const char* lumo_last_error(void) { return g_err.c_str(); }
+
+extern "C" const char* lumo_version(void) { return "lumo_tree 0.1 gfx950"; }
+
+extern "C" size_t lumo_tree_gdn_workspace_bytes(const lumo_gdn_dims* d, const lumo_plan* p) {
+    if (!d || !p) return 0;
+    if (p->policy != LUMO_POLICY_PATHS && p->policy != LUMO_POLICY_TWO_LEVEL) return 0;
+    return (size_t)p->n_cuts * d->n_layers * d->h_v * d->d_k * d->d_v * sizeof(float);
+}
+
+extern "C" lumo_status lumo_tree_conv_gather(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                             int32_t channels, const void* x, const void* conv_hist,
+                                             const float* w, const float* bias, int32_t act, void* y,
+                                             void* stream) {
+    static const char* fn = "lumo_tree_conv_gather";
+    clear_error();
+    LUMO_TRY(check_dims(dims, fn));
+    LUMO_TRY(check_desc(dims, desc, fn));
+    if (channels <= 0 || channels % 8) return fail(LUMO_ESHAPE, "%s: channels %d must be a positive multiple of 8", fn, channels);
+    if (act != 0 && act != 1) return fail(LUMO_EINVAL, "%s: act %d (0 identity, 1 SiLU)", fn, act);
+    if (desc->plan.total_nodes == 0) return LUMO_OK;
+    LUMO_TRY(check_ptr(x, fn, "x"));
+    LUMO_TRY(check_ptr(conv_hist, fn, "conv_hist"));
+    LUMO_TRY(check_ptr(w, fn, "w"));
+    LUMO_TRY(check_ptr(bias, fn, "bias", true));
+    LUMO_TRY(check_ptr(y, fn, "y"));
+    ConvArgs a{channels, x, conv_hist, w, bias, act, y};
+    hipError_t e = launch_conv(*dims, *desc, a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
+extern "C" lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lumo_tree_desc* desc, const void* q,
+                                            const void* k, const void* v, const float* g, const float* beta,
+                                            const float* state0, void* o, float* node_states, void* workspace,
+                                            size_t workspace_bytes, int32_t flags, void* stream) {
+    static const char* fn = "lumo_tree_gdn_verify";
+    clear_error();
+    LUMO_TRY(check_dims(dims, fn));
+    LUMO_TRY(check_desc(dims, desc, fn));
+    if (flags != 0) return fail(LUMO_EINVAL, "%s: flags must be 0", fn);
+    const int policy = desc->plan.policy;
+    if (policy < LUMO_POLICY_PATHS || policy > LUMO_POLICY_WY) return fail(LUMO_EDESC, "%s: plan policy %d", fn, policy);
+    if (desc->plan.total_nodes == 0) return LUMO_OK;
+    LUMO_TRY(check_ptr(q, fn, "q"));
+    LUMO_TRY(check_ptr(k, fn, "k"));
+    LUMO_TRY(check_ptr(v, fn, "v"));
+    LUMO_TRY(check_ptr(g, fn, "g"));
+    LUMO_TRY(check_ptr(beta, fn, "beta"));
+    LUMO_TRY(check_ptr(state0, fn, "state0"));
+    LUMO_TRY(check_ptr(o, fn, "o"));
+    LUMO_TRY(check_ptr(node_states, fn, "node_states", true));
+    const size_t need = lumo_tree_gdn_workspace_bytes(dims, &desc->plan);
+    if (need) {
+        LUMO_TRY(check_ptr(workspace, fn, "workspace"));
+        if (workspace_bytes < need)
+            return fail(LUMO_ESPACE, "%s: workspace needs %zu bytes, got %zu", fn, need, workspace_bytes);
+    }
+    GdnArgs a{q, k, v, g, beta, state0, o, node_states, static_cast<float*>(workspace)};
+    hipError_t e;
+    if (policy == LUMO_POLICY_WY) {
+        if (node_states) return fail(LUMO_EUNSUPPORTED, "%s: the WY policy keeps no per-node states", fn);
+        if (dims->op_dtype != LUMO_BF16 || dims->d_k != 128 || dims->d_v != 128)
+            return fail(LUMO_EUNSUPPORTED, "%s: the WY policy is built for bf16 operands with d_k = d_v = 128", fn);
+        e = launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream));
+    } else {
+        e = launch_scan(*dims, *desc, a, static_cast<hipStream_t>(stream));
+    }
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: policy %d not available in this build", fn, policy);
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
+namespace {
+
+lumo_status check_commit(const lumo_gdn_dims* dims, const lumo_tree_desc* desc, int32_t max_path,
+                         const int32_t* accepted, int32_t* path_out, int32_t* path_len, const void* k,
+                         const void* v, const float* g, const float* beta, float* state, int32_t channels,
+                         const void* x, void* conv_hist, const char* fn) {
+    LUMO_TRY(check_dims(dims, fn));
+    LUMO_TRY(check_desc(dims, desc, fn));
+    if (max_path < 1 || max_path > 4096) return fail(LUMO_EINVAL, "%s: max_path %d (1..4096)", fn, max_path);
+    if (dims->n_req == 0) return LUMO_OK;
+    LUMO_TRY(check_ptr(accepted, fn, "accepted_node"));
+    LUMO_TRY(check_ptr(path_out, fn, "path_out"));
+    LUMO_TRY(check_ptr(path_len, fn, "path_len"));
+    LUMO_TRY(check_ptr(k, fn, "k"));
+    LUMO_TRY(check_ptr(v, fn, "v"));
+    LUMO_TRY(check_ptr(g, fn, "g"));
+    LUMO_TRY(check_ptr(beta, fn, "beta"));
+    LUMO_TRY(check_ptr(state, fn, "state"));
+    if ((x == nullptr) != (conv_hist == nullptr))
+        return fail(LUMO_EINVAL, "%s: x and conv_hist must both be given or both be NULL", fn);
+    if (x) {
+        LUMO_TRY(check_ptr(x, fn, "x"));
+        LUMO_TRY(check_ptr(conv_hist, fn, "conv_hist"));
+        if (channels <= 0 || channels % 8)
+            return fail(LUMO_ESHAPE, "%s: channels %d must be a positive multiple of 8", fn, channels);
+    }
+    return LUMO_OK;
+}
+
+}  // namespace
+
+extern "C" lumo_status lumo_gdn_commit(const lumo_gdn_dims* dims, const lumo_tree_desc* desc, int32_t max_path,
+                                       const int32_t* accepted_node, int32_t* path_out, int32_t* path_len,
+                                       const void* k, const void* v, const float* g, const float* beta, float* state,
+                                       int32_t channels, const void* x, void* conv_hist, void* stream) {
+    static const char* fn = "lumo_gdn_commit";
+    clear_error();
+    LUMO_TRY(check_commit(dims, desc, max_path, accepted_node, path_out, path_len, k, v, g, beta, state, channels, x,
+                          conv_hist, fn));
+    if (dims->n_req == 0) return LUMO_OK;
+    CommitArgs a{max_path, accepted_node, path_out, path_len, k, v, g, beta, state, channels, x, conv_hist};
+    hipError_t e = launch_commit(*dims, *desc, a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
+struct lumo_commit_graph {
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+};
+
+extern "C" lumo_status lumo_gdn_commit_graph_create(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                                    int32_t max_path, const int32_t* accepted_node, int32_t* path_out,
+                                                    int32_t* path_len, const void* k, const void* v, const float* g,
+                                                    const float* beta, float* state, int32_t channels, const void* x,
+                                                    void* conv_hist, lumo_commit_graph** out) {
+    static const char* fn = "lumo_gdn_commit_graph_create";
+    clear_error();
+    if (!out) return fail(LUMO_EINVAL, "%s: out is NULL", fn);
+    *out = nullptr;
+    LUMO_TRY(check_commit(dims, desc, max_path, accepted_node, path_out, path_len, k, v, g, beta, state, channels, x,
+                          conv_hist, fn));
+    lumo_commit_graph* cg = new (std::nothrow) lumo_commit_graph();
+    if (!cg) return fail(LUMO_EHIP, "%s: out of host memory", fn);
+    hipStream_t s = nullptr;
+    hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal);
+    if (e == hipSuccess) {
+        hipError_t le = hipSuccess;
+        if (dims->n_req > 0) {
+            CommitArgs a{max_path, accepted_node, path_out, path_len, k, v, g, beta, state, channels, x, conv_hist};
+            le = launch_commit(*dims, *desc, a, s);
+        }
+        e = hipStreamEndCapture(s, &cg->graph);
+        if (e == hipSuccess) e = le;
+    }
+    if (e == hipSuccess) e = hipGraphInstantiate(&cg->exec, cg->graph, nullptr, nullptr, 0);
+    if (s) (void)hipStreamDestroy(s);
+    if (e != hipSuccess) {
+        if (cg->exec) (void)hipGraphExecDestroy(cg->exec);
+        if (cg->graph) (void)hipGraphDestroy(cg->graph);
+        delete cg;
+        return fail(LUMO_EHIP, "%s: capture failed: %s", fn, hipGetErrorString(e));
+    }
+    *out = cg;
+    return LUMO_OK;
+}
+
+extern "C" lumo_status lumo_gdn_commit_graph_launch(lumo_commit_graph* graph, void* stream) {
+    clear_error();
+    if (!graph || !graph->exec) return fail(LUMO_EINVAL, "lumo_gdn_commit_graph_launch: graph is NULL");
+    hipError_t e = hipGraphLaunch(graph->exec, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(LUMO_EHIP, "lumo_gdn_commit_graph_launch: %s", hipGetErrorString(e));
+    return LUMO_OK;
+}
+
+extern "C" void lumo_gdn_commit_graph_destroy(lumo_commit_graph* graph) {
+    if (!graph) return;
+    if (graph->exec) (void)hipGraphExecDestroy(graph->exec);
+    if (graph->graph) (void)hipGraphDestroy(graph->graph);
+    delete graph;
+}

@@ -1,0 +1,135 @@
+// Tree causal convolution (LumoTree Sec. V-C, Tab. II row 3).
+//
+// The planner turns the topology into static gather sources: for every node, the
+// four rows of its window (oldest first), each either an x row along the ancestry
+// or a committed-history entry. The kernel gathers those rows and applies the four
+// taps in order with fp32 accumulation starting from the bias, then the activation,
+// then one cast. One thread handles 8 contiguous channels of one (layer, node);
+// loads and stores are 16-byte vectors, every x row is read by at most four nodes
+// (itself and three descendants), and the taps of a channel block stay in cache
+// across the nodes of a layer. HBM-bound.
+#include "device_common.h"
+#include "internal.h"
+#include "launch.h"
+
+namespace lumo {
+namespace {
+
+struct ConvParams {
+    const int32_t* blob;
+    int32_t o_req, o_row, o_conv_src;
+    int32_t total_nodes, total_rows, n_layers, channels, n_cchunks, act;
+    const void* x;
+    const void* hist;
+    const float* w;
+    const float* bias;
+    void* y;
+};
+
+template <int OPT> struct Vec8;
+template <> struct Vec8<0> {
+    static __device__ __forceinline__ void ld(const float* p, float (&v)[8]) {
+        const float4 a = reinterpret_cast<const float4*>(p)[0];
+        const float4 b = reinterpret_cast<const float4*>(p)[1];
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    }
+    static __device__ __forceinline__ void st(float* p, const float (&v)[8]) {
+        reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+        reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+    }
+};
+template <> struct Vec8<1> {
+    static __device__ __forceinline__ void ld(const uint16_t* p, float (&v)[8]) {
+        const uint4 a = reinterpret_cast<const uint4*>(p)[0];
+        v[0] = bf16_lo(a.x); v[1] = bf16_hi(a.x); v[2] = bf16_lo(a.y); v[3] = bf16_hi(a.y);
+        v[4] = bf16_lo(a.z); v[5] = bf16_hi(a.z); v[6] = bf16_lo(a.w); v[7] = bf16_hi(a.w);
+    }
+    static __device__ __forceinline__ void st(uint16_t* p, const float (&v)[8]) {
+        uint4 a;
+        a.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+        a.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+        a.z = (uint32_t)f32_to_bf16(v[4]) | ((uint32_t)f32_to_bf16(v[5]) << 16);
+        a.w = (uint32_t)f32_to_bf16(v[6]) | ((uint32_t)f32_to_bf16(v[7]) << 16);
+        reinterpret_cast<uint4*>(p)[0] = a;
+    }
+};
+
+template <int OPT>
+__global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
+    using T = typename Op<OPT>::T;
+    int t = xcd_remap(blockIdx.x, gridDim.x);
+    const int cc = t % p.n_cchunks;
+    t /= p.n_cchunks;
+    const int n = t % p.total_nodes;  // nodes of a layer are adjacent: ancestors in cache
+    const int l = t / p.total_nodes;
+    const int c = (cc * 256 + (int)threadIdx.x) * 8;
+    if (c >= p.channels) return;
+    const int r = p.blob[p.o_req + n];
+    const int row = p.blob[p.o_row + n];
+    const int32_t* src = p.blob + p.o_conv_src + 4 * n;
+    const T* x = static_cast<const T*>(p.x);
+    const T* hist = static_cast<const T*>(p.hist);
+    float acc[8];
+    if (p.bias) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = p.bias[(long)l * p.channels + c + e];
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+    }
+    // taps of 8 channels: 32 consecutive floats [c][t]
+    float wt[32];
+    const float4* wp = reinterpret_cast<const float4*>(p.w + ((long)l * p.channels + c) * 4);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float4 q = wp[e];
+        wt[4 * e] = q.x; wt[4 * e + 1] = q.y; wt[4 * e + 2] = q.z; wt[4 * e + 3] = q.w;
+    }
+#pragma unroll
+    for (int tap = 0; tap < 4; ++tap) {
+        const int s = src[tap];
+        const T* rp = s >= 0 ? x + ((long)l * p.total_rows + s) * p.channels + c
+                             : hist + (((long)r * p.n_layers + l) * 3 + (-1 - s)) * p.channels + c;
+        float xv[8];
+        Vec8<OPT>::ld(rp, xv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = __builtin_fmaf(wt[4 * e + tap], xv[e], acc[e]);
+    }
+    if (p.act == 1) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = acc[e] / (1.f + __expf(-acc[e]));
+    }
+    Vec8<OPT>::st(static_cast<T*>(p.y) + ((long)l * p.total_rows + row) * p.channels + c, acc);
+}
+
+}  // namespace
+
+hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const ConvArgs& a, hipStream_t s) {
+    const lumo_plan& pl = desc.plan;
+    if (pl.total_nodes == 0) return hipSuccess;
+    ConvParams p;
+    p.blob = desc.blob;
+    p.o_req = pl.o_req;
+    p.o_row = pl.o_row;
+    p.o_conv_src = pl.o_conv_src;
+    p.total_nodes = pl.total_nodes;
+    p.total_rows = pl.total_rows;
+    p.n_layers = d.n_layers;
+    p.channels = a.channels;
+    p.n_cchunks = (a.channels + 2047) / 2048;
+    p.act = a.act;
+    p.x = a.x;
+    p.hist = a.hist;
+    p.w = a.w;
+    p.bias = a.bias;
+    p.y = a.y;
+    const long blocks = (long)d.n_layers * pl.total_nodes * p.n_cchunks;
+    if (d.op_dtype == LUMO_BF16)
+        hipLaunchKernelGGL(conv_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, s, p);
+    else
+        hipLaunchKernelGGL(conv_kernel<0>, dim3((unsigned)blocks), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace lumo

@@ -1,0 +1,111 @@
+// Device helpers shared by the gfx950 kernels: operand decoding, the single
+// per-value-row gated delta-rule update used by both verification and commit, and
+// the XCD-aware block remap.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lumo {
+
+// ---------------------------------------------------------------- bf16 / fp32 operands
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;  // NaN stays NaN
+    u += 0x7fffu + ((u >> 16) & 1u);                     // round to nearest even
+    return (uint16_t)(u >> 16);
+}
+
+template <int OPT> struct Op;
+template <> struct Op<0> {
+    using T = float;
+    static __device__ __forceinline__ float ld(const T* p, long i) { return p[i]; }
+    static __device__ __forceinline__ void st(T* p, long i, float x) { p[i] = x; }
+    // N consecutive values starting at p (N even, p 8-byte aligned)
+    template <int N>
+    static __device__ __forceinline__ void ld_row(const T* __restrict__ p, float (&out)[N]) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) out[i] = p[i];
+    }
+};
+template <> struct Op<1> {
+    using T = uint16_t;
+    static __device__ __forceinline__ float ld(const T* p, long i) { return __uint_as_float(((uint32_t)p[i]) << 16); }
+    static __device__ __forceinline__ void st(T* p, long i, float x) { p[i] = f32_to_bf16(x); }
+    template <int N>
+    static __device__ __forceinline__ void ld_row(const T* __restrict__ p, float (&out)[N]) {
+        const uint32_t* w = reinterpret_cast<const uint32_t*>(p);
+#pragma unroll
+        for (int i = 0; i < N / 2; ++i) {
+            const uint32_t x = w[i];
+            out[2 * i] = bf16_lo(x);
+            out[2 * i + 1] = bf16_hi(x);
+        }
+    }
+};
+
+// ---------------------------------------------------------------- the recurrence
+// Elements of k per uniform operand chunk (16 dwords of bf16: one scalar load).
+constexpr int kChunk = 32;
+
+// One gated delta-rule node update (Eq. (2)-(3)) for one value row j of the head
+// matrix, S[i] = R[j][i]. `kp` is the node's key row (wave-uniform address).
+//   u = (R_pi k)_j;  delta = beta (v_j - alpha u);  R_j <- alpha R_j + delta k
+// alpha is applied to the dot product instead of the matrix (same value in exact
+// arithmetic). The operation order is fixed (explicit fma, contraction off), so
+// verification and commit produce bitwise identical states.
+template <int DK, int OPT>
+__device__ __forceinline__ void gdn_row_update(float (&S)[DK], const typename Op<OPT>::T* __restrict__ kp,
+                                               float vj, float alpha, float beta) {
+    float u = 0.f;
+#pragma unroll
+    for (int c = 0; c < DK; c += kChunk) {
+        asm volatile("" ::: "memory");  // one chunk of the row live at a time
+        float kf[kChunk < DK ? kChunk : DK];
+        Op<OPT>::template ld_row<(kChunk < DK ? kChunk : DK)>(kp + c, kf);
+#pragma unroll
+        for (int i = 0; i < (kChunk < DK ? kChunk : DK); ++i) u = __builtin_fmaf(S[c + i], kf[i], u);
+    }
+    const float delta = beta * __builtin_fmaf(-alpha, u, vj);
+    // The key row is re-read chunk by chunk in the second pass instead of being kept
+    // live: a wave holds about 100 scalar registers, fewer than a 128-wide fp32 row.
+#pragma unroll
+    for (int c = 0; c < DK; c += kChunk) {
+        asm volatile("" ::: "memory");
+        float kf[kChunk < DK ? kChunk : DK];
+        Op<OPT>::template ld_row<(kChunk < DK ? kChunk : DK)>(kp + c, kf);
+#pragma unroll
+        for (int i = 0; i < (kChunk < DK ? kChunk : DK); ++i) S[c + i] = __builtin_fmaf(delta, kf[i], alpha * S[c + i]);
+    }
+}
+
+// o_j = R_j . q
+template <int DK, int OPT>
+__device__ __forceinline__ float gdn_row_output(const float (&S)[DK], const typename Op<OPT>::T* __restrict__ qp) {
+    float o = 0.f;
+#pragma unroll
+    for (int c = 0; c < DK; c += kChunk) {
+        asm volatile("" ::: "memory");
+        float qf[kChunk < DK ? kChunk : DK];
+        Op<OPT>::template ld_row<(kChunk < DK ? kChunk : DK)>(qp + c, qf);
+#pragma unroll
+        for (int i = 0; i < (kChunk < DK ? kChunk : DK); ++i) o = __builtin_fmaf(S[c + i], qf[i], o);
+    }
+    return o;
+}
+
+// ---------------------------------------------------------------- launch geometry
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).
+// Remap so that consecutive logical block ids run on the same XCD: blocks that
+// share operands (same segment and layer, neighbouring heads) then share an L2.
+__device__ __forceinline__ int xcd_remap(int p, int nb) {
+    constexpr int X = 8;
+    const int xcd = p % X, local = p / X;
+    const int base = nb / X, extra = nb % X;
+    return (xcd < extra ? xcd * (base + 1) : extra * (base + 1) + (xcd - extra) * base) + local;
+}
+
+}  // namespace lumo

@@ -1,0 +1,58 @@
+// Host launchers of the gfx950 kernels (arguments already validated by the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "lumo_tree.h"
+
+namespace lumo {
+
+struct GdnArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    const float* g;
+    const float* beta;
+    const float* state0;
+    void* o;
+    float* node_states;
+    float* ws;
+};
+
+// Sequential path scans (PATHS / TWO_LEVEL / RECOMPUTE): one launch per dependency level.
+hipError_t launch_scan(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s);
+
+// Tree WY form on MFMA (one launch).
+hipError_t launch_wy(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s);
+
+struct CommitArgs {
+    int32_t max_path;
+    const int32_t* accepted;
+    int32_t* path_out;
+    int32_t* path_len;
+    const void* k;
+    const void* v;
+    const float* g;
+    const float* beta;
+    float* state;
+    int32_t channels;
+    const void* x;
+    void* conv_hist;
+};
+
+hipError_t launch_commit(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const CommitArgs& a, hipStream_t s);
+
+struct ConvArgs {
+    int32_t channels;
+    const void* x;
+    const void* hist;
+    const float* w;
+    const float* bias;
+    int32_t act;
+    void* y;
+};
+
+hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const ConvArgs& a, hipStream_t s);
+
+}  // namespace lumo

@@ -1,0 +1,165 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/lumo_tree.h declares, and rejects bad arguments on the host (documented
+status codes) before anything would be launched. No compute call is made here."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import paper_2609_23900_amd as L
+from lumo_synth import trees
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lumo_tree.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lumo_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_gdn_verify", "lumo_gdn_commit",
+              "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch",
+              "lumo_gdn_commit_graph_destroy", "lumo_tree_gdn_workspace_bytes", "lumo_last_error"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol():
+    out = subprocess.run(["nm", "-D", "--defined-only", L.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (lumo_\w+)", out))
+    missing = [f for f in declared_functions() if f not in exported]
+    assert not missing, missing
+    for f in declared_functions():
+        assert hasattr(L._lib, f)
+
+
+def test_binding_names_match_abi():
+    for f in declared_functions():
+        assert callable(getattr(L, f)), f
+
+
+def test_version():
+    assert "gfx950" in L.lumo_version()
+
+
+# ---------------------------------------------------------------- host-side rejection
+FAKE = 0x10000  # an aligned address that is never dereferenced (validation fails first)
+
+
+def _desc(n_req=1, policy=0):
+    par = trees.FIG1_PARENT
+    plan, blob = L.lumo_tree_plan(np.array([0, 7] if n_req == 1 else [0, 7, 14], np.int32),
+                                  np.concatenate([par] * n_req),
+                                  np.array([7] * n_req, np.int32), policy)
+    d = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
+    return d, blob
+
+
+def _verify(d, desc, ptrs=None, ws=0, flags=0):
+    p = [ctypes.c_void_p(FAKE)] * 7 if ptrs is None else ptrs
+    return L._lib.lumo_tree_gdn_verify(ctypes.byref(d), ctypes.byref(desc), *p, None,
+                                       ctypes.c_void_p(FAKE), ws, flags, None)
+
+
+def _dims(**kw):
+    base = dict(n_req=1, n_layers=1, h_k=1, h_v=1, d_k=16, d_v=16, op_dtype=0)
+    base.update(kw)
+    return L.lumo_gdn_dims(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(d_k=48), L.LUMO_EUNSUPPORTED), (dict(d_v=256), L.LUMO_EUNSUPPORTED),
+    (dict(h_k=2, h_v=3), L.LUMO_ESHAPE), (dict(n_layers=0), L.LUMO_ESHAPE),
+    (dict(op_dtype=7), L.LUMO_EUNSUPPORTED), (dict(n_req=2), L.LUMO_EDESC)])
+def test_verify_rejects_bad_dims(kw, status):
+    desc, _blob = _desc()
+    assert _verify(_dims(**kw), desc) == status
+    assert L.lumo_last_error()
+
+
+def test_verify_rejects_null_and_misaligned():
+    desc, _blob = _desc()
+    ptrs = [ctypes.c_void_p(FAKE)] * 7
+    ptrs[2] = None
+    assert _verify(_dims(), desc, ptrs) == L.LUMO_EINVAL
+    ptrs = [ctypes.c_void_p(FAKE)] * 7
+    ptrs[0] = ctypes.c_void_p(FAKE + 4)
+    assert _verify(_dims(), desc, ptrs) == L.LUMO_EINVAL
+    assert "aligned" in L.lumo_last_error()
+
+
+def test_verify_rejects_flags_and_small_workspace():
+    desc, _blob = _desc()
+    assert _verify(_dims(), desc, flags=1) == L.LUMO_EINVAL
+    need = L.lumo_tree_gdn_workspace_bytes(_dims(), desc.plan)
+    assert need == 2 * 16 * 16 * 4
+    assert _verify(_dims(), desc, ws=need - 4) == L.LUMO_ESPACE
+
+
+def test_verify_rejects_null_desc_blob():
+    desc, _blob = _desc()
+    desc.blob = None
+    assert _verify(_dims(), desc) == L.LUMO_EINVAL
+
+
+def test_wy_requires_bf16_d128():
+    desc, _blob = _desc(policy=L.LUMO_POLICY_WY)
+    assert _verify(_dims(), desc) == L.LUMO_EUNSUPPORTED
+
+
+def _commit(d, desc, max_path=4, x=True, hist=True, channels=8, accepted=FAKE):
+    P = ctypes.c_void_p
+    return L._lib.lumo_gdn_commit(ctypes.byref(d), ctypes.byref(desc), max_path,
+                                  P(accepted) if accepted else None, P(FAKE), P(FAKE), P(FAKE),
+                                  P(FAKE), P(FAKE), P(FAKE), P(FAKE), channels,
+                                  P(FAKE) if x else None, P(FAKE) if hist else None, None)
+
+
+def test_commit_rejects_bad_arguments():
+    desc, _blob = _desc()
+    assert _commit(_dims(), desc, max_path=0) == L.LUMO_EINVAL
+    assert _commit(_dims(), desc, max_path=5000) == L.LUMO_EINVAL
+    assert _commit(_dims(), desc, x=True, hist=False) == L.LUMO_EINVAL
+    assert _commit(_dims(), desc, channels=12) == L.LUMO_ESHAPE
+    assert _commit(_dims(), desc, accepted=0) == L.LUMO_EINVAL
+    assert _commit(_dims(d_k=24), desc) == L.LUMO_EUNSUPPORTED
+
+
+def test_conv_rejects_bad_arguments():
+    desc, _blob = _desc()
+    P = ctypes.c_void_p
+    f = L._lib.lumo_tree_conv_gather
+    assert f(ctypes.byref(_dims()), ctypes.byref(desc), 12, P(FAKE), P(FAKE), P(FAKE), None, 1,
+             P(FAKE), None) == L.LUMO_ESHAPE
+    assert f(ctypes.byref(_dims()), ctypes.byref(desc), 16, P(FAKE), P(FAKE), P(FAKE), None, 3,
+             P(FAKE), None) == L.LUMO_EINVAL
+    assert f(ctypes.byref(_dims()), ctypes.byref(desc), 16, P(FAKE), None, P(FAKE), None, 1,
+             P(FAKE), None) == L.LUMO_EINVAL
+
+
+def test_graph_create_rejects_and_null_launch():
+    desc, _blob = _desc()
+    h = ctypes.c_void_p()
+    P = ctypes.c_void_p
+    st = L._lib.lumo_gdn_commit_graph_create(ctypes.byref(_dims()), ctypes.byref(desc), 0, P(FAKE),
+                                             P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+                                             P(FAKE), 0, None, None, ctypes.byref(h))
+    assert st == L.LUMO_EINVAL and not h.value
+    assert L._lib.lumo_gdn_commit_graph_launch(None, None) == L.LUMO_EINVAL
+    L._lib.lumo_gdn_commit_graph_destroy(None)
+
+
+def test_empty_batch_is_a_no_op():
+    plan, blob = L.lumo_tree_plan(np.array([0], np.int32), np.zeros(0, np.int32),
+                                  np.zeros(0, np.int32), 0)
+    desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
+    d = _dims(n_req=0)
+    assert _verify(d, desc, [None] * 7) == L.LUMO_OK
+    assert _commit(d, desc, accepted=0) == L.LUMO_OK

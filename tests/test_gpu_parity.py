@@ -1,0 +1,323 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Small configs are compared in full; the full-size configs on sampled instances
+(request, layer, value head), every node of each. Descriptor products (path_out,
+path_len) are compared bit for bit. Invariants that hold bitwise on the GPU (policy
+equivalence, commit == dumped node state, identity update, identical subtrees,
+repeatability) are checked as such.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - collected on CPU, skipped there
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import oracle  # noqa: E402
+import paper_2609_23900_amd as L  # noqa: E402
+from paper_2609_23900_amd.step import GdnTreeStep  # noqa: E402
+from lumo_synth import configs, trees  # noqa: E402
+from lumo_synth import operands as ops  # noqa: E402
+import gpu_util as gu  # noqa: E402
+import pins  # noqa: E402
+
+SEQ_POLICIES = [L.LUMO_POLICY_PATHS, L.LUMO_POLICY_TWO_LEVEL, L.LUMO_POLICY_RECOMPUTE]
+
+_WL = {}
+
+
+def workload(name):
+    if name not in _WL:
+        _WL[name] = configs.build(name)
+    return _WL[name]
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run(wl, policy, *, with_conv=True, node_states=False, commit=True, arrays=None):
+    say(f"[gpu] {wl.name} policy={policy} conv={with_conv} dump={node_states}")
+    a = wl.arrays if arrays is None else arrays
+    st = GdnTreeStep(n_req=wl.n_req, n_layers=wl.n_layers, h_k=wl.h_k, h_v=wl.h_v, d_k=wl.d_k,
+                     d_v=wl.d_v, op_dtype=wl.op_dtype, node_off=wl.node_off,
+                     parent=wl.parent_flat, n_rows=wl.n_rows,
+                     arrays={k: v for k, v in a.items() if with_conv or k not in ("x", "hist", "w")},
+                     policy=policy, max_path=wl.max_path, accepted=wl.accepted,
+                     channels=wl.channels if with_conv else 0, with_node_states=node_states)
+    if with_conv:
+        st.conv()
+    st.verify()
+    if commit:
+        st.commit()
+    torch.cuda.synchronize()
+    return st
+
+
+# ---------------------------------------------------------------- small configs, full parity
+
+@pytest.mark.parametrize("policy", SEQ_POLICIES)
+@pytest.mark.parametrize("name", ["tiny", "layer1", "paper28"])
+def test_small_config_parity(name, policy):
+    wl = workload(name)
+    st = run(wl, policy, node_states=(name != "layer1"))
+    o = gu.to_np(st.o)
+    inst = [(r, l, h) for r in range(wl.n_req) for l in range(wl.n_layers) for h in range(wl.h_v)]
+    gu.check_outputs(wl, o, inst)
+    ref_state, po, pl = oracle.commit(wl)
+    assert np.array_equal(st.path_out.cpu().numpy(), po)
+    assert np.array_equal(st.path_len.cpu().numpy(), pl)
+    gu.check_states(wl, st.state.cpu().numpy(), ref_state, inst)
+    # conv and conv-history publication
+    y = gu.to_np(st.y)
+    yref = oracle.conv_all(wl)
+    rows = oracle.plan.flat_rows(wl.parents, wl.row_off)
+    assert gu.max_rel(y[:, rows], yref[:, rows]) <= gu.out_tol(wl)
+    href = oracle.conv_hist_publish(wl, po, pl)
+    assert np.array_equal(gu.to_np(st.hist).astype(np.float64), href)
+
+
+@pytest.mark.parametrize("name", ["tiny", "paper28"])
+def test_commit_equals_dumped_node_state(name):
+    """Publishing the path to node i reproduces the verified state of i bit for bit."""
+    wl = workload(name)
+    st = run(wl, L.LUMO_POLICY_PATHS, with_conv=False, node_states=True, commit=False)
+    ns = st.node_states.cpu().numpy()
+    rows = gu.node_rows(wl, 0)
+    for node in range(len(wl.parents[0])):
+        st.reset_state()
+        st.accepted.fill_(node)
+        st.commit()
+        torch.cuda.synchronize()
+        s = st.state.cpu().numpy()
+        for l in range(wl.n_layers):
+            for h in range(wl.h_v):
+                assert np.array_equal(s[0, l, h], ns[l, rows[node], h]), (node, l, h)
+
+
+def test_policies_bitwise_identical():
+    wl = workload("paper28")
+    outs = [gu.to_np(run(wl, p, with_conv=False, commit=False).o) for p in SEQ_POLICIES]
+    rows = oracle.plan.flat_rows(wl.parents, wl.row_off)
+    for o in outs[1:]:
+        assert np.array_equal(o[:, rows], outs[0][:, rows])
+
+
+# ---------------------------------------------------------------- full-size configs, sampled
+
+@pytest.mark.parametrize("name,policy,n_inst", [
+    ("batched", L.LUMO_POLICY_PATHS, 24),
+    ("widedeep", L.LUMO_POLICY_PATHS, 12),
+    ("widedeep", L.LUMO_POLICY_TWO_LEVEL, 6),
+    ("chainmix", L.LUMO_POLICY_RECOMPUTE, 16),
+    ("chainmix", L.LUMO_POLICY_PATHS, 8),
+])
+def test_full_size_sampled_parity(name, policy, n_inst):
+    wl = workload(name)
+    st = run(wl, policy)
+    o = gu.to_np(st.o)
+    inst = gu.sample_instances(wl, n_inst, seed=7)
+    worst = gu.check_outputs(wl, o, inst)
+    say(f"  outputs worst max-rel {worst:.3e}")
+    ref_state, po, pl = oracle.commit(wl)
+    assert np.array_equal(st.path_out.cpu().numpy(), po)
+    assert np.array_equal(st.path_len.cpu().numpy(), pl)
+    ws = gu.check_states(wl, st.state.cpu().numpy(), ref_state, inst)
+    say(f"  states worst max-rel {ws:.3e}")
+    # conv on two sampled layers, history on all
+    y = gu.to_np(st.y)
+    rows = oracle.plan.flat_rows(wl.parents, wl.row_off)
+    for l in sorted({0, wl.n_layers - 1}):
+        sub = {"x": wl.arrays["x"][l:l + 1], "hist": wl.arrays["hist"][:, l:l + 1],
+               "w": wl.arrays["w"][l:l + 1]}
+        one = configs.Workload(**{**wl.__dict__, "n_layers": 1, "arrays": sub})
+        yref = oracle.conv_all(one)
+        assert gu.max_rel(y[l][rows], yref[0][rows]) <= gu.out_tol(wl)
+    href = oracle.conv_hist_publish(wl, po, pl)
+    assert np.array_equal(gu.to_np(st.hist).astype(np.float64), href)
+
+
+# ---------------------------------------------------------------- invariants and edge cases
+
+def test_identity_update_keeps_state_bitwise():
+    wl = configs.build("paper28", with_conv=False)
+    a = dict(wl.arrays)
+    a["beta"] = np.zeros_like(a["beta"])
+    a["g"] = np.zeros_like(a["g"])  # alpha = exp(0) = 1
+    st = run(wl, L.LUMO_POLICY_PATHS, with_conv=False, arrays=a)
+    assert np.array_equal(st.state.cpu().numpy(), a["state0"])
+
+
+def test_identical_sibling_subtrees_bitwise():
+    par = np.array([-1, 0, 0, 1, 2, 3, 4, 1, 2], np.int32)
+    wl = pins.make_wl([par], d_k=128, d_v=128, h_k=2, h_v=4, op_dtype=ops.BF16, max_path=4)
+    wl.arrays = ops.make_gdn_operands(3, n_req=1, n_layers=1, total_rows=9, h_k=2, h_v=4,
+                                      d_k=128, d_v=128, op_dtype=ops.BF16)
+    rows = gu.node_rows(wl, 0)
+    for x, y in ((1, 2), (3, 4), (5, 6), (7, 8)):
+        for key in ("q", "k", "v", "g", "beta"):
+            wl.arrays[key][:, rows[y]] = wl.arrays[key][:, rows[x]]
+    for policy in SEQ_POLICIES:
+        o = run(wl, policy, with_conv=False, commit=False).o.cpu()
+        for x, y in ((1, 2), (3, 4), (5, 6), (7, 8)):
+            assert torch.equal(o[:, rows[x]], o[:, rows[y]])
+
+
+def test_pad_rows_never_read_or_written():
+    wl = configs.build("paper28")
+    a = {k: v.copy() for k, v in wl.arrays.items()}
+    rows = set(oracle.plan.flat_rows(wl.parents, wl.row_off).tolist())
+    pad = [r for r in range(wl.total_rows) if r not in rows]
+    assert pad
+    nan_bf16 = np.uint16(0x7FC0)
+    for key in ("q", "k", "v", "x"):
+        a[key][:, pad] = nan_bf16
+    for key in ("g", "beta"):
+        a[key][:, pad] = np.nan
+    st = run(wl, L.LUMO_POLICY_TWO_LEVEL, arrays=a)
+    o = gu.to_np(st.o)
+    assert np.all(o[:, pad] == 0)           # untouched zero fill
+    assert np.all(np.isfinite(o[:, sorted(rows)]))
+    assert np.all(np.isfinite(st.state.cpu().numpy()))
+    y = gu.to_np(st.y)
+    assert np.all(y[:, pad] == 0) and np.all(np.isfinite(y[:, sorted(rows)]))
+    gu.check_outputs(wl, o, [(0, 0, 0), (0, 0, 31)])
+
+
+def test_accepted_edge_cases():
+    wl = configs.build("paper28", with_conv=True)
+    cases = [(-1, 0), (0, 1), (27, None), (28, -1), (-2, -1), (99, -1)]
+    for acc, want_len in cases:
+        st = run(wl, L.LUMO_POLICY_RECOMPUTE, with_conv=True, commit=False)
+        st.accepted.fill_(acc)
+        st.max_path = 12
+        hist0 = st.hist.clone()
+        st.commit()
+        torch.cuda.synchronize()
+        pl = int(st.path_len.cpu()[0])
+        po = st.path_out.cpu().numpy()[0]
+        if want_len is None:
+            path, L_ = oracle.plan.accepted_path(wl.parents[0], acc, 12)
+            assert pl == L_ and list(po) == path
+        else:
+            assert pl == want_len
+        if pl <= 0:
+            assert np.all(po == -1)
+            assert torch.equal(st.state, st.state0)
+            assert torch.equal(st.hist, hist0)
+    # a path longer than max_path is refused without touching the state
+    st = run(wl, L.LUMO_POLICY_RECOMPUTE, with_conv=False, commit=False)
+    deep = int(np.argmax(trees.depths(wl.parents[0])))
+    st.accepted.fill_(deep)
+    st.max_path = 4
+    st.path_out = torch.full((1, 4), -7, dtype=torch.int32, device="cuda")
+    st.commit()
+    torch.cuda.synchronize()
+    assert int(st.path_len.cpu()[0]) == -1 and torch.equal(st.state, st.state0)
+
+
+def test_empty_batch_and_root_only_requests():
+    parents = [np.array([-1], np.int32), np.array([-1, 0], np.int32), np.array([-1], np.int32)]
+    wl = pins.make_wl(parents, d_k=64, d_v=32, h_k=1, h_v=2, op_dtype=ops.BF16, n_rows=[1, 3, 2],
+                      max_path=2, n_layers=2)
+    wl.arrays = ops.make_gdn_operands(5, n_req=3, n_layers=2, total_rows=6, h_k=1, h_v=2,
+                                      d_k=64, d_v=32, op_dtype=ops.BF16)
+    wl.accepted = np.array([0, 1, -1], np.int32)
+    st = run(wl, L.LUMO_POLICY_PATHS, with_conv=False)
+    inst = [(r, l, h) for r in range(3) for l in range(2) for h in range(2)]
+    gu.check_outputs(wl, gu.to_np(st.o), inst)
+    ref, po, pl = oracle.commit(wl)
+    assert np.array_equal(st.path_len.cpu().numpy(), pl)
+    gu.check_states(wl, st.state.cpu().numpy(), ref, inst)
+    # n_req = 0: every entry point is a no-op
+    d = L.dims(0, 1, 1, 1, 16, 16, 0)
+    desc = L.TreeDesc.build(np.array([0], np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32))
+    e = torch.zeros(16, device="cuda")
+    L.lumo_tree_gdn_verify(d, desc, e, e, e, e, e, e, e)
+    L.lumo_gdn_commit(d, desc, 1, e.int(), e.int(), e.int(), e, e, e, e, e)
+    torch.cuda.synchronize()
+
+
+def test_repeatability_bitwise():
+    wl = workload("layer1")
+    o1 = run(wl, L.LUMO_POLICY_PATHS).o.cpu()
+    o2 = run(wl, L.LUMO_POLICY_PATHS).o.cpu()
+    assert torch.equal(o1, o2)
+
+
+def test_multi_cycle_continuation():
+    """verify -> commit -> verify on the next tree from the published state."""
+    wl1 = configs.build("layer1", with_conv=False)
+    st = run(wl1, L.LUMO_POLICY_PATHS, with_conv=False)
+    wl2 = configs.build("layer1", seed=101, with_conv=False)
+    ref_state, _, _ = oracle.commit(wl1)
+    a2 = dict(wl2.arrays)
+    a2["state0"] = ref_state.astype(np.float32)          # oracle-published state, rounded
+    st2 = GdnTreeStep.from_workload(wl2, policy=L.LUMO_POLICY_PATHS, with_conv=False)
+    st2.verify(state0=st.state)                          # GPU-published state
+    torch.cuda.synchronize()
+    gu.check_outputs(wl2, gu.to_np(st2.o), gu.sample_instances(wl2, 8), arrays=a2)
+
+
+# ---------------------------------------------------------------- captured commit graph
+
+def test_commit_graph_replays():
+    wl = workload("chainmix")
+    st = run(wl, L.LUMO_POLICY_RECOMPUTE, with_conv=True, commit=False)
+    hist0 = st.hist.clone()
+    g = st.commit_graph(with_conv=True)
+    rng = np.random.default_rng(5)
+    inst = gu.sample_instances(wl, 6, seed=3)
+    for rep in range(24):
+        lens = rng.integers(0, 17, size=wl.n_req)
+        acc = np.array([configs._pick_accepted(rng, p, int(L_), int(L_)) if L_ > 0 else -1
+                        for p, L_ in zip(wl.parents, lens)], np.int32)
+        st.state.copy_(st.state0)
+        st.hist.copy_(hist0)
+        st.accepted.copy_(torch.from_numpy(acc))
+        torch.cuda.synchronize()
+        g.launch()
+        torch.cuda.synchronize()
+        ref, po, pl = oracle.commit(wl, accepted=acc)
+        assert np.array_equal(st.path_out.cpu().numpy(), po), rep
+        assert np.array_equal(st.path_len.cpu().numpy(), pl), rep
+        gu.check_states(wl, st.state.cpu().numpy(), ref, inst)
+        href = oracle.conv_hist_publish(wl, po, pl)
+        assert np.array_equal(gu.to_np(st.hist).astype(np.float64), href), rep
+    g.close()
+
+
+# ---------------------------------------------------------------- negative controls
+
+def test_negative_control_sibling_swap_detected():
+    """Swapping two siblings' operand rows must break parity (the test has teeth)."""
+    wl = configs.build("paper28", with_conv=False)
+    a = {k: v.copy() for k, v in wl.arrays.items()}
+    par = wl.parents[0]
+    ch = oracle.plan.children(par)
+    p = next(i for i in range(len(par)) if len(ch[i]) >= 2)
+    x, y = ch[p][0], ch[p][1]
+    rows = gu.node_rows(wl, 0)
+    for key in ("k", "v", "g", "beta"):
+        a[key][:, [rows[x], rows[y]]] = a[key][:, [rows[y], rows[x]]]
+    o = gu.to_np(run(wl, L.LUMO_POLICY_PATHS, with_conv=False, commit=False, arrays=a).o)
+    with pytest.raises(AssertionError):
+        gu.check_outputs(wl, o, [(0, 0, h) for h in range(wl.h_v)])
+
+
+def test_negative_control_zero_replay_detected():
+    wl = configs.build("paper28", with_conv=False)
+    st = run(wl, L.LUMO_POLICY_PATHS, with_conv=False, commit=False)
+    st.accepted.fill_(-1)
+    st.commit()
+    torch.cuda.synchronize()
+    ref, _, _ = oracle.commit(wl)
+    with pytest.raises(AssertionError):
+        gu.check_states(wl, st.state.cpu().numpy(), ref, [(0, 0, 0)])

@@ -1,8 +1,9 @@
 """Plant plausible mistakes in copies of the oracle and check that a pin trips.
 
 Each mutation edits one expression of oracle/lumo_oracle.c (a dropped term, a wrong
-sign, a wrong index, a transposed operand, a reversed tap order, a skipped node),
-compiles the copy with gcc into a temporary directory and runs every pin against it.
+sign, a wrong index, a transposed operand, a reversed tap order, a skipped node);
+every mutant stays within the bounds of its arrays. The copy is
+compiled with gcc into a temporary directory and runs every pin against it.
 The real oracle is never modified.
 """
 import os
@@ -37,7 +38,8 @@ MUTATIONS = {
                             "gdn_output(d, s.R, l, row[s.path[len > 1 ? len - 2 : 0]], h,"),
     "reversed_taps": ("acc += (double)w[((long)l * channels + c) * 4 + t] * xv;",
                       "acc += (double)w[((long)l * channels + c) * 4 + (3 - t)] * xv;"),
-    "window_off_by_one": ("const int pos = 3 + len - 4 + t;", "const int pos = 3 + len - 3 + t;"),
+    "history_reversed": ("xv = ld_op(hist, (((long)r * n_layers + l) * 3 + pos) * channels + c, op_dtype);",
+                         "xv = ld_op(hist, (((long)r * n_layers + l) * 3 + (2 - pos)) * channels + c, op_dtype);"),
     "hist_publish_shift": ("const int pos = L + e;", "const int pos = L + e - 1 < 0 ? 0 : L + e - 1;"),
     "commit_skips_last": ("for (int p = 0; p < path_len[r]; ++p)", "for (int p = 0; p + 1 < path_len[r]; ++p)"),
 }
