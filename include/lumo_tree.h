@@ -106,6 +106,7 @@ typedef struct {
     /* section offsets (int32 words) inside the blob */
     int32_t o_node_off, o_row_off, o_req, o_parent, o_depth, o_slot, o_row, o_conv_src;
     int32_t o_path_off, o_path_leaf, o_spine_off, o_spine, o_level_off, o_seg, o_seg_nodes;
+    int32_t o_dfs, o_dfs_pos;
 } lumo_plan;
 
 /* A plan whose blob has been copied to device memory. */
@@ -142,7 +143,9 @@ typedef struct {
  *   row[N] (absolute), conv_src[N][4], path_off[n_req+1], path_leaf[n_paths],
  *   spine_off[n_req+1], spine[n_spine], level_off[n_levels+1],
  *   seg[n_seg][4] = {request, source cut (-1 = pre-tree state), first entry, length},
- *   seg_nodes[n_seg_nodes][3] = {absolute row, writes output (0/1), cut to export (-1 none)}.
+ *   seg_nodes[n_seg_nodes][3] = {absolute row, writes output (0/1), cut to export (-1 none)},
+ *   dfs[N] (per request: node ids in depth-first preorder, children by increasing id),
+ *   dfs_pos[N] (position of each node in that order).
  * Returns LUMO_EDESC for malformed trees, LUMO_ESPACE (with out->n_words set)
  * when blob is NULL or too small, LUMO_EINVAL for bad arguments.
  */

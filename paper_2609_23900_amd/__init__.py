@@ -47,7 +47,8 @@ _PLAN_FIELDS = ("n_req", "total_nodes", "total_rows", "max_nodes", "max_depth", 
                 "n_paths", "n_spine", "n_seg", "n_seg_nodes", "n_levels", "n_cuts",
                 "max_level_seg", "max_seg_len", "n_words", "o_node_off", "o_row_off", "o_req",
                 "o_parent", "o_depth", "o_slot", "o_row", "o_conv_src", "o_path_off",
-                "o_path_leaf", "o_spine_off", "o_spine", "o_level_off", "o_seg", "o_seg_nodes")
+                "o_path_leaf", "o_spine_off", "o_spine", "o_level_off", "o_seg", "o_seg_nodes",
+                "o_dfs", "o_dfs_pos")
 
 
 class lumo_plan(ctypes.Structure):

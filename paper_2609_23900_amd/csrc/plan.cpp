@@ -29,6 +29,7 @@ struct ReqTree {
     std::vector<int> leaves, spine, slot;
     std::vector<char> on_spine;
     std::vector<int> owner;  // smallest leaf id whose path contains the node
+    std::vector<int> dfs, dfs_pos;  // preorder (children by increasing id) and its inverse
 
     int n_children(int x) const { return child_off[x + 1] - child_off[x]; }
     int first_child(int x) const { return n_children(x) ? child[child_off[x]] : -1; }
@@ -77,6 +78,16 @@ lumo_status build_tree(int r, int n, const int32_t* parent, ReqTree& t) {
         }
         t.owner[i] = best;
     }
+    t.dfs.reserve(n);
+    std::vector<int> stack{0};
+    while (!stack.empty()) {
+        const int x = stack.back();
+        stack.pop_back();
+        t.dfs.push_back(x);
+        for (int e = t.child_off[x + 1] - 1; e >= t.child_off[x]; --e) stack.push_back(t.child[e]);
+    }
+    t.dfs_pos.assign(n, 0);
+    for (int p = 0; p < n; ++p) t.dfs_pos[t.dfs[p]] = p;
     return LUMO_OK;
 }
 
@@ -257,6 +268,8 @@ extern "C" lumo_status lumo_tree_plan(int32_t n_req, const int32_t* node_off, co
     p.o_level_off = take(p.n_levels + 1);
     p.o_seg = take((int64_t)lumo::kSegWords * p.n_seg);
     p.o_seg_nodes = take((int64_t)lumo::kSegNodeWords * p.n_seg_nodes);
+    p.o_dfs = take(N);
+    p.o_dfs_pos = take(N);
     if (w > (int64_t(1) << 30)) return lumo::fail(LUMO_ESHAPE, "lumo_tree_plan: plan too large");
     p.n_words = (int32_t)w;
     *out = p;
@@ -279,6 +292,8 @@ extern "C" lumo_status lumo_tree_plan(int32_t n_req, const int32_t* node_off, co
             b[p.o_depth + base + i] = t.depth[i];
             b[p.o_slot + base + i] = t.slot[i];
             b[p.o_row + base + i] = row_base[r] + t.slot[i];
+            b[p.o_dfs + base + i] = t.dfs[i];
+            b[p.o_dfs_pos + base + i] = t.dfs_pos[i];
             // window = last four of (hist0, hist1, hist2, ancestry root..i), oldest first
             int anc[4] = {-1, -1, -1, -1};  // anc[3] = i, anc[2] = parent, ...
             int x = i;

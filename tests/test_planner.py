@@ -56,6 +56,22 @@ def _check_against_oracle(parents, n_rows, node_off, policy):
         assert sec("conv_src", 4 * N).reshape(-1, 4)[b:b + n].tolist() == oplan.conv_sources(par, rows)
         leaves += oplan.leaves(par)
         spines += oplan.spine(par)
+        # depth-first preorder: a permutation where every subtree is contiguous
+        dfs = list(sec("dfs", N)[b:b + n])
+        pos = list(sec("dfs_pos", N)[b:b + n])
+        assert sorted(dfs) == list(range(n)) and all(pos[dfs[k]] == k for k in range(n))
+        if n:
+            assert dfs[0] == 0
+            size = [1] * n
+            for i in range(n - 1, 0, -1):
+                size[par[i]] += size[i]
+            for i in range(n):
+                sub = set(dfs[pos[i]:pos[i] + size[i]])
+                assert all(i in oplan.ancestry(par, x) for x in sub)
+            ch = oplan.children(par)
+            for i in range(n):   # children visited in increasing id
+                cp = [pos[c] for c in ch[i]]
+                assert cp == sorted(cp)
     assert list(sec("path_leaf", plan.n_paths)) == leaves
     assert list(sec("spine", plan.n_spine)) == spines
     assert plan.max_depth == max(max(oplan.depth(p)) + 1 for p in parents)
