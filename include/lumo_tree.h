@@ -76,9 +76,11 @@ typedef enum {
      * states, shared prefixes recomputed. No workspace. */
     LUMO_POLICY_RECOMPUTE = 2,
     /* Tree WY form: R_t = gamma_t R0 + sum over ancestors of decayed rank-1
-     * terms; the R0 [K | Q] products run on MFMA (bf16 split in three), the
-     * ancestor-masked triangular system on the vector units. One launch, no
-     * workspace, no state dump. bf16 operands only. */
+     * terms; the R0 [K | Q] products run on MFMA (R0 as bf16 hi + lo), the
+     * ancestor-masked triangular system on the vector units. Two launches; the
+     * workspace holds per-node coefficient records; no state dump. bf16 operands,
+     * d_k = d_v = 128, paths of at most 17 nodes. Outputs agree with the
+     * sequential schedules to rounding, not bitwise. */
     LUMO_POLICY_WY = 3
 } lumo_policy;
 
@@ -155,8 +157,10 @@ lumo_status lumo_tree_plan(int32_t n_req, const int32_t* node_off, const int32_t
 
 /*
  * lumo_tree_gdn_workspace_bytes - device workspace needed by lumo_tree_gdn_verify
- * for this plan: one fp32 d_k x d_v matrix per (exported cut, layer, value head)
- * (the cut-state payload of Eq. (4), Sec. IV-C). 0 for RECOMPUTE and WY.
+ * for this plan: PATHS / TWO_LEVEL one fp32 d_k x d_v matrix per (exported cut,
+ * layer, value head) (the cut-state payload of Eq. (4), Sec. IV-C); WY one
+ * coefficient record of 8 + 2 D floats per (node, layer, value head), D = 8 when
+ * paths have at most 9 nodes, else 16; RECOMPUTE 0.
  */
 size_t lumo_tree_gdn_workspace_bytes(const lumo_gdn_dims* dims, const lumo_plan* plan);
 

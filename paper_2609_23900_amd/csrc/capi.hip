@@ -81,6 +81,7 @@ extern "C" const char* lumo_version(void) { return "lumo_tree 0.1 gfx950"; }
 
 extern "C" size_t lumo_tree_gdn_workspace_bytes(const lumo_gdn_dims* d, const lumo_plan* p) {
     if (!d || !p) return 0;
+    if (p->policy == LUMO_POLICY_WY) return wy_workspace_bytes(*d, *p);
     if (p->policy != LUMO_POLICY_PATHS && p->policy != LUMO_POLICY_TWO_LEVEL) return 0;
     return (size_t)p->n_cuts * d->n_layers * d->h_v * d->d_k * d->d_v * sizeof(float);
 }
@@ -127,6 +128,14 @@ extern "C" lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lum
     LUMO_TRY(check_ptr(state0, fn, "state0"));
     LUMO_TRY(check_ptr(o, fn, "o"));
     LUMO_TRY(check_ptr(node_states, fn, "node_states", true));
+    if (policy == LUMO_POLICY_WY) {
+        if (node_states) return fail(LUMO_EUNSUPPORTED, "%s: the WY policy keeps no per-node states", fn);
+        if (dims->op_dtype != LUMO_BF16 || dims->d_k != 128 || dims->d_v != 128)
+            return fail(LUMO_EUNSUPPORTED, "%s: the WY policy is built for bf16 operands with d_k = d_v = 128", fn);
+        if (desc->plan.max_depth > kWyMaxDepth)
+            return fail(LUMO_EUNSUPPORTED, "%s: the WY policy handles paths of at most %d nodes (plan has %d)", fn,
+                        kWyMaxDepth, desc->plan.max_depth);
+    }
     const size_t need = lumo_tree_gdn_workspace_bytes(dims, &desc->plan);
     if (need) {
         LUMO_TRY(check_ptr(workspace, fn, "workspace"));
@@ -136,9 +145,6 @@ extern "C" lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lum
     GdnArgs a{q, k, v, g, beta, state0, o, node_states, static_cast<float*>(workspace)};
     hipError_t e;
     if (policy == LUMO_POLICY_WY) {
-        if (node_states) return fail(LUMO_EUNSUPPORTED, "%s: the WY policy keeps no per-node states", fn);
-        if (dims->op_dtype != LUMO_BF16 || dims->d_k != 128 || dims->d_v != 128)
-            return fail(LUMO_EUNSUPPORTED, "%s: the WY policy is built for bf16 operands with d_k = d_v = 128", fn);
         e = launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream));
     } else {
         e = launch_scan(*dims, *desc, a, static_cast<hipStream_t>(stream));

@@ -163,3 +163,21 @@ def test_empty_batch_is_a_no_op():
     d = _dims(n_req=0)
     assert _verify(d, desc, [None] * 7) == L.LUMO_OK
     assert _commit(d, desc, accepted=0) == L.LUMO_OK
+
+
+def test_wy_rejects_paths_longer_than_17():
+    par = trees.chain(18)
+    plan, blob = L.lumo_tree_plan(np.array([0, 18], np.int32), par, np.array([18], np.int32),
+                                  L.LUMO_POLICY_WY)
+    desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
+    d = _dims(h_k=1, h_v=1, d_k=128, d_v=128, op_dtype=1)
+    assert _verify(d, desc, ws=L.lumo_tree_gdn_workspace_bytes(d, plan)) == L.LUMO_EUNSUPPORTED
+    assert "17" in L.lumo_last_error()
+
+
+def test_wy_workspace_size():
+    par = trees.FIG1_PARENT
+    plan, blob = L.lumo_tree_plan(np.array([0, 7], np.int32), par, np.array([7], np.int32),
+                                  L.LUMO_POLICY_WY)
+    d = _dims(h_k=2, h_v=4, d_k=128, d_v=128, op_dtype=1, n_layers=3)
+    assert L.lumo_tree_gdn_workspace_bytes(d, plan) == 7 * 3 * 4 * (8 + 2 * 8) * 4

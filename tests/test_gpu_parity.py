@@ -321,3 +321,62 @@ def test_negative_control_zero_replay_detected():
     ref, _, _ = oracle.commit(wl)
     with pytest.raises(AssertionError):
         gu.check_states(wl, st.state.cpu().numpy(), ref, [(0, 0, 0)])
+
+
+# ---------------------------------------------------------------- WY form on MFMA
+
+@pytest.mark.parametrize("name,n_inst", [("layer1", 32), ("paper28", 32), ("batched", 24),
+                                          ("widedeep", 12), ("chainmix", 16)])
+def test_wy_parity(name, n_inst):
+    wl = workload(name)
+    st = run(wl, L.LUMO_POLICY_WY)
+    o = gu.to_np(st.o)
+    worst = gu.check_outputs(wl, o, gu.sample_instances(wl, n_inst, seed=11))
+    say(f"  wy outputs worst max-rel {worst:.3e}")
+    rows = set(oracle.plan.flat_rows(wl.parents, wl.row_off).tolist())
+    pad = [r for r in range(wl.total_rows) if r not in rows]
+    if pad:
+        assert np.all(o[:, pad] == 0)
+    ref_state, po, pl = oracle.commit(wl)
+    assert np.array_equal(st.path_len.cpu().numpy(), pl)
+    gu.check_states(wl, st.state.cpu().numpy(), ref_state, gu.sample_instances(wl, n_inst, seed=12))
+
+
+def test_wy_agrees_with_sequential_scan():
+    """WY and the sequential scan compute the same recurrence: outputs within bf16 rounding."""
+    wl = workload("layer1")
+    o_seq = gu.to_np(run(wl, L.LUMO_POLICY_PATHS, with_conv=False, commit=False).o)
+    o_wy = gu.to_np(run(wl, L.LUMO_POLICY_WY, with_conv=False, commit=False).o)
+    rows = oracle.plan.flat_rows(wl.parents, wl.row_off)
+    for h in range(wl.h_v):
+        a, b = o_seq[0, rows, h], o_wy[0, rows, h]
+        assert gu.max_rel(b, a) <= 2 ** -7, h
+
+
+def test_wy_identical_sibling_subtrees():
+    par = np.array([-1, 0, 0, 1, 2, 3, 4, 1, 2], np.int32)
+    wl = pins.make_wl([par], d_k=128, d_v=128, h_k=2, h_v=4, op_dtype=ops.BF16, max_path=4)
+    wl.arrays = ops.make_gdn_operands(3, n_req=1, n_layers=1, total_rows=9, h_k=2, h_v=4,
+                                      d_k=128, d_v=128, op_dtype=ops.BF16)
+    rows = gu.node_rows(wl, 0)
+    for x, y in ((1, 2), (3, 4), (5, 6), (7, 8)):
+        for key in ("q", "k", "v", "g", "beta"):
+            wl.arrays[key][:, rows[y]] = wl.arrays[key][:, rows[x]]
+    o = run(wl, L.LUMO_POLICY_WY, with_conv=False, commit=False).o.cpu()
+    for x, y in ((1, 2), (3, 4), (5, 6), (7, 8)):
+        assert torch.equal(o[:, rows[x]], o[:, rows[y]])
+    gu.check_outputs(wl, gu.to_np(o.cuda()), [(0, 0, h) for h in range(4)])
+
+
+def test_wy_deep_chain_and_ragged_requests():
+    """Chains of 17 nodes (the WY depth limit), 1-node and 40-node requests, padding."""
+    rng = np.random.default_rng(9)
+    parents = [trees.chain(17), np.array([-1], np.int32),
+               trees.random_tree(rng, 40, 9, trees.bmax_uniform(3)), trees.chain(5)]
+    wl = pins.make_wl(parents, d_k=128, d_v=128, h_k=4, h_v=8, op_dtype=ops.BF16,
+                      n_rows=[17, 3, 41, 5], n_layers=2, max_path=17)
+    wl.arrays = ops.make_gdn_operands(21, n_req=4, n_layers=2, total_rows=66, h_k=4, h_v=8,
+                                      d_k=128, d_v=128, op_dtype=ops.BF16)
+    st = run(wl, L.LUMO_POLICY_WY, with_conv=False, commit=False)
+    inst = [(r, l, h) for r in range(4) for l in range(2) for h in (0, 3, 7)]
+    gu.check_outputs(wl, gu.to_np(st.o), inst)
