@@ -4,7 +4,9 @@
 //   1. path kernel    accepted node -> root-first path and its length (bit-exact)
 //   2. replay kernel  one wavefront per (request, layer, value head, value tile):
 //                     load the pre-tree state tile, apply the recorded updates of the
-//                     path with the same row update the verifier uses, store in place
+//                     path with the same row update the verifier uses, store in place;
+//                     the path's rows and value entries are fetched before the loop,
+//                     the wave-uniform key rows are read with scalar loads
 //   3. history kernel conv history <- last three of (history, x rows of the path)
 // Empty or invalid paths leave the state and the history untouched.
 #include "device_common.h"
@@ -51,19 +53,28 @@ __global__ __launch_bounds__(256) void path_kernel(PathParams p) {
 struct ReplayParams {
     const int32_t* blob;
     int32_t o_node_off, o_row;
-    const void* k;
-    const void* v;
-    const float* g;
-    const float* beta;
-    float* state;
-    const int32_t* path_out;
-    const int32_t* path_len;
     int32_t max_path, n_layers, total_rows, h_k, h_v, d_v, group, n_vtiles;
 };
 
+// Path entries whose row and value are prefetched before the update loop.
+constexpr int kPrefetch = 16;
+
+// One replayed update (the verifier's row update) for path entry e.
 template <int DK, int OPT>
-__global__ __launch_bounds__(64) void replay_kernel(ReplayParams p) {
-    using T = typename Op<OPT>::T;
+__device__ __forceinline__ void replay_step(float (&S)[DK], const typename Op<OPT>::T* __restrict__ k,
+                                            const float* __restrict__ g, const float* __restrict__ beta,
+                                            const ReplayParams& p, int l, int h, int hk, int row, float vj) {
+    const long gi = ((long)l * p.total_rows + row) * p.h_v + h;
+    const long ki = (((long)l * p.total_rows + row) * p.h_k + hk) * DK;
+    gdn_row_update<DK, OPT>(S, k + ki, vj, __expf(g[gi]), beta[gi]);
+}
+
+template <int DK, int OPT>
+__global__ __launch_bounds__(64) void replay_kernel(ReplayParams p, const typename Op<OPT>::T* __restrict__ k,
+                                                   const typename Op<OPT>::T* __restrict__ v,
+                                                   const float* __restrict__ g, const float* __restrict__ beta,
+                                                   float* __restrict__ state, const int32_t* __restrict__ path_out,
+                                                   const int32_t* __restrict__ path_len) {
     int t = xcd_remap(blockIdx.x, gridDim.x);
     const int vt = t % p.n_vtiles;
     t /= p.n_vtiles;
@@ -71,29 +82,35 @@ __global__ __launch_bounds__(64) void replay_kernel(ReplayParams p) {
     t /= p.h_v;
     const int l = t % p.n_layers;
     const int r = t / p.n_layers;
-    const int len = p.path_len[r];
+    const int len = path_len[r];
     if (len <= 0) return;
-    const int j = vt * 64 + (int)threadIdx.x;
+    const int lane = (int)threadIdx.x;
+    const int j = vt * 64 + lane;
     const bool act = j < p.d_v;
     const int jc = act ? j : p.d_v - 1;
     const int hk = h / p.group;
     const int base = p.blob[p.o_node_off + r];
     const long mat = (long)DK * p.d_v;
-    float* st = p.state + (((long)r * p.n_layers + l) * p.h_v + h) * mat;
+    float* st = state + (((long)r * p.n_layers + l) * p.h_v + h) * mat;
+    const int32_t* path = path_out + (long)r * p.max_path;
+    // row of path entry `lane` (lanes past the path read the root's row)
+    const int prow = p.blob[p.o_row + base + path[lane < len ? lane : 0]];
+    float vpre[kPrefetch];
+#pragma unroll
+    for (int e = 0; e < kPrefetch; ++e) {
+        const int re = __builtin_amdgcn_readlane(prow, e);  // wave-uniform row
+        vpre[e] = Op<OPT>::ld(v, (((long)l * p.total_rows + re) * p.h_v + h) * p.d_v + jc);
+    }
     float S[DK];
 #pragma unroll
     for (int i = 0; i < DK; ++i) S[i] = st[(long)i * p.d_v + jc];
-    const T* __restrict__ k = static_cast<const T*>(p.k);
-    const T* __restrict__ v = static_cast<const T*>(p.v);
-    const int32_t* path = p.path_out + (long)r * p.max_path;
     for (int e = 0; e < len; ++e) {
-        const int row = p.blob[p.o_row + base + path[e]];
-        const long gi = ((long)l * p.total_rows + row) * p.h_v + h;
-        const long ki = (((long)l * p.total_rows + row) * p.h_k + hk) * DK;
-        const float alpha = __expf(p.g[gi]);
-        const float beta = p.beta[gi];
-        const float vj = Op<OPT>::ld(v, gi * p.d_v + jc);
-        gdn_row_update<DK, OPT>(S, k + ki, vj, alpha, beta);
+        const int re = e < 64 ? __builtin_amdgcn_readlane(prow, e) : p.blob[p.o_row + base + path[e]];
+        const float vj = e < kPrefetch ? vpre[0]
+                                       : Op<OPT>::ld(v, (((long)l * p.total_rows + re) * p.h_v + h) * p.d_v + jc);
+        replay_step<DK, OPT>(S, k, g, beta, p, l, h, hk, re, vj);
+#pragma unroll
+        for (int i = 0; i + 1 < kPrefetch; ++i) vpre[i] = vpre[i + 1];  // next entry's value to slot 0
     }
     if (act) {
 #pragma unroll
@@ -146,13 +163,20 @@ __global__ __launch_bounds__(256) void hist_kernel(HistParams p) {
         for (int w = 0; w < W; ++w) reinterpret_cast<uint4*>(hist + (long)e * p.channels + c)[w] = val[e][w];
 }
 
+template <int DK, int OPT>
+void launch_replay_dk(dim3 grid, hipStream_t s, const ReplayParams& p, const CommitArgs& a) {
+    using T = typename Op<OPT>::T;
+    hipLaunchKernelGGL((replay_kernel<DK, OPT>), grid, dim3(64), 0, s, p, static_cast<const T*>(a.k),
+                       static_cast<const T*>(a.v), a.g, a.beta, a.state, a.path_out, a.path_len);
+}
+
 template <int OPT>
-hipError_t launch_replay(int dk, dim3 grid, hipStream_t s, const ReplayParams& p) {
+hipError_t launch_replay(int dk, dim3 grid, hipStream_t s, const ReplayParams& p, const CommitArgs& a) {
     switch (dk) {
-        case 16: hipLaunchKernelGGL((replay_kernel<16, OPT>), grid, dim3(64), 0, s, p); break;
-        case 32: hipLaunchKernelGGL((replay_kernel<32, OPT>), grid, dim3(64), 0, s, p); break;
-        case 64: hipLaunchKernelGGL((replay_kernel<64, OPT>), grid, dim3(64), 0, s, p); break;
-        default: hipLaunchKernelGGL((replay_kernel<128, OPT>), grid, dim3(64), 0, s, p); break;
+        case 16: launch_replay_dk<16, OPT>(grid, s, p, a); break;
+        case 32: launch_replay_dk<32, OPT>(grid, s, p, a); break;
+        case 64: launch_replay_dk<64, OPT>(grid, s, p, a); break;
+        default: launch_replay_dk<128, OPT>(grid, s, p, a); break;
     }
     return hipGetLastError();
 }
@@ -172,13 +196,6 @@ hipError_t launch_commit(const lumo_gdn_dims& d, const lumo_tree_desc& desc, con
     rp.blob = desc.blob;
     rp.o_node_off = pl.o_node_off;
     rp.o_row = pl.o_row;
-    rp.k = a.k;
-    rp.v = a.v;
-    rp.g = a.g;
-    rp.beta = a.beta;
-    rp.state = a.state;
-    rp.path_out = a.path_out;
-    rp.path_len = a.path_len;
     rp.max_path = a.max_path;
     rp.n_layers = d.n_layers;
     rp.total_rows = pl.total_rows;
@@ -188,8 +205,8 @@ hipError_t launch_commit(const lumo_gdn_dims& d, const lumo_tree_desc& desc, con
     rp.group = d.h_v / d.h_k;
     rp.n_vtiles = (d.d_v + 63) / 64;
     const long blocks = (long)d.n_req * d.n_layers * d.h_v * rp.n_vtiles;
-    e = d.op_dtype == LUMO_BF16 ? launch_replay<1>(d.d_k, dim3((unsigned)blocks), s, rp)
-                                : launch_replay<0>(d.d_k, dim3((unsigned)blocks), s, rp);
+    e = d.op_dtype == LUMO_BF16 ? launch_replay<1>(d.d_k, dim3((unsigned)blocks), s, rp, a)
+                                : launch_replay<0>(d.d_k, dim3((unsigned)blocks), s, rp, a);
     if (e != hipSuccess) return e;
 
     if (a.x && a.conv_hist) {

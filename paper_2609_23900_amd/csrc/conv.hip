@@ -4,10 +4,10 @@
 // four rows of its window (oldest first), each either an x row along the ancestry
 // or a committed-history entry. The kernel gathers those rows and applies the four
 // taps in order with fp32 accumulation starting from the bias, then the activation,
-// then one cast. One thread handles 8 contiguous channels of one (layer, node);
-// loads and stores are 16-byte vectors, every x row is read by at most four nodes
-// (itself and three descendants), and the taps of a channel block stay in cache
-// across the nodes of a layer. HBM-bound.
+// then one cast. One thread handles 8 contiguous channels of one layer for a run of
+// nodes; loads and stores are 16-byte vectors, the thread's taps stay in registers,
+// and every x row is read by at most four nodes (itself and three descendants, which
+// follow it closely in node order, so the re-reads hit L2). HBM-bound.
 #include "device_common.h"
 #include "internal.h"
 #include "launch.h"
@@ -55,30 +55,25 @@ template <> struct Vec8<1> {
     }
 };
 
+// One block: one layer, 2048 channels (8 per thread), a run of kNodesPerBlock nodes.
+// The taps and bias of the thread's channels stay in registers across the run; the
+// window rows of consecutive nodes (parents, grandparents) are mostly L2 hits.
+constexpr int kNodesPerBlock = 32;
+
 template <int OPT>
 __global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
     using T = typename Op<OPT>::T;
     int t = xcd_remap(blockIdx.x, gridDim.x);
+    const int ng = (p.total_nodes + kNodesPerBlock - 1) / kNodesPerBlock;
+    const int grp = t % ng;
+    t /= ng;
     const int cc = t % p.n_cchunks;
-    t /= p.n_cchunks;
-    const int n = t % p.total_nodes;  // nodes of a layer are adjacent: ancestors in cache
-    const int l = t / p.total_nodes;
+    const int l = t / p.n_cchunks;
     const int c = (cc * 256 + (int)threadIdx.x) * 8;
     if (c >= p.channels) return;
-    const int r = p.blob[p.o_req + n];
-    const int row = p.blob[p.o_row + n];
-    const int32_t* src = p.blob + p.o_conv_src + 4 * n;
     const T* x = static_cast<const T*>(p.x);
     const T* hist = static_cast<const T*>(p.hist);
-    float acc[8];
-    if (p.bias) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = p.bias[(long)l * p.channels + c + e];
-    } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-    }
-    // taps of 8 channels: 32 consecutive floats [c][t]
+    T* y = static_cast<T*>(p.y);
     float wt[32];
     const float4* wp = reinterpret_cast<const float4*>(p.w + ((long)l * p.channels + c) * 4);
 #pragma unroll
@@ -86,21 +81,37 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
         const float4 q = wp[e];
         wt[4 * e] = q.x; wt[4 * e + 1] = q.y; wt[4 * e + 2] = q.z; wt[4 * e + 3] = q.w;
     }
+    float b0[8];
 #pragma unroll
-    for (int tap = 0; tap < 4; ++tap) {
-        const int s = src[tap];
-        const T* rp = s >= 0 ? x + ((long)l * p.total_rows + s) * p.channels + c
-                             : hist + (((long)r * p.n_layers + l) * 3 + (-1 - s)) * p.channels + c;
-        float xv[8];
-        Vec8<OPT>::ld(rp, xv);
+    for (int e = 0; e < 8; ++e) b0[e] = p.bias ? p.bias[(long)l * p.channels + c + e] : 0.f;
+    const int n0 = grp * kNodesPerBlock;
+    const int n1 = min(p.total_nodes, n0 + kNodesPerBlock);
+#pragma unroll 2
+    for (int n = n0; n < n1; ++n) {
+        const int r = p.blob[p.o_req + n];
+        const int row = p.blob[p.o_row + n];
+        const int32_t* src = p.blob + p.o_conv_src + 4 * n;
+        float acc[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = __builtin_fmaf(wt[4 * e + tap], xv[e], acc[e]);
+        for (int e = 0; e < 8; ++e) acc[e] = b0[e];
+        float xv[4][8];
+#pragma unroll
+        for (int tap = 0; tap < 4; ++tap) {
+            const int s = src[tap];
+            const T* rp = s >= 0 ? x + ((long)l * p.total_rows + s) * p.channels + c
+                                 : hist + (((long)r * p.n_layers + l) * 3 + (-1 - s)) * p.channels + c;
+            Vec8<OPT>::ld(rp, xv[tap]);
+        }
+#pragma unroll
+        for (int tap = 0; tap < 4; ++tap)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] = __builtin_fmaf(wt[4 * e + tap], xv[tap][e], acc[e]);
+        if (p.act == 1) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] = acc[e] / (1.f + __expf(-acc[e]));
+        }
+        Vec8<OPT>::st(y + ((long)l * p.total_rows + row) * p.channels + c, acc);
     }
-    if (p.act == 1) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = acc[e] / (1.f + __expf(-acc[e]));
-    }
-    Vec8<OPT>::st(static_cast<T*>(p.y) + ((long)l * p.total_rows + row) * p.channels + c, acc);
 }
 
 }  // namespace
@@ -124,7 +135,7 @@ hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.w = a.w;
     p.bias = a.bias;
     p.y = a.y;
-    const long blocks = (long)d.n_layers * pl.total_nodes * p.n_cchunks;
+    const long blocks = (long)d.n_layers * p.n_cchunks * ((pl.total_nodes + kNodesPerBlock - 1) / kNodesPerBlock);
     if (d.op_dtype == LUMO_BF16)
         hipLaunchKernelGGL(conv_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, s, p);
     else

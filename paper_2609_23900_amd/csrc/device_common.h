@@ -51,8 +51,18 @@ template <> struct Op<1> {
 // Elements of k per uniform operand chunk (16 dwords of bf16: one scalar load).
 constexpr int kChunk = 32;
 
+// A wave-uniform offset hidden from the optimiser: every chunk of a key or query row
+// is then loaded (scalar load) right where it is used instead of the whole row being
+// hoisted and kept live; a wave holds about 100 scalar registers, fewer than one
+// 128-wide fp32 row.
+__device__ __forceinline__ int opaque(int x) {
+    asm volatile("" : "+s"(x));
+    return x;
+}
+
 // One gated delta-rule node update (Eq. (2)-(3)) for one value row j of the head
-// matrix, S[i] = R[j][i]. `kp` is the node's key row (wave-uniform address).
+// matrix, S[i] = R[j][i]. `kp` is the node's key row (wave-uniform address, scalar
+// loads chunk by chunk).
 //   u = (R_pi k)_j;  delta = beta (v_j - alpha u);  R_j <- alpha R_j + delta k
 // alpha is applied to the dot product instead of the matrix (same value in exact
 // arithmetic). The operation order is fixed (explicit fma, contraction off), so
@@ -60,39 +70,36 @@ constexpr int kChunk = 32;
 template <int DK, int OPT>
 __device__ __forceinline__ void gdn_row_update(float (&S)[DK], const typename Op<OPT>::T* __restrict__ kp,
                                                float vj, float alpha, float beta) {
+    constexpr int C = kChunk < DK ? kChunk : DK;
     float u = 0.f;
 #pragma unroll
-    for (int c = 0; c < DK; c += kChunk) {
-        asm volatile("" ::: "memory");  // one chunk of the row live at a time
-        float kf[kChunk < DK ? kChunk : DK];
-        Op<OPT>::template ld_row<(kChunk < DK ? kChunk : DK)>(kp + c, kf);
+    for (int c = 0; c < DK; c += C) {
+        float kf[C];
+        Op<OPT>::template ld_row<C>(kp + opaque(c), kf);
 #pragma unroll
-        for (int i = 0; i < (kChunk < DK ? kChunk : DK); ++i) u = __builtin_fmaf(S[c + i], kf[i], u);
+        for (int i = 0; i < C; ++i) u = __builtin_fmaf(S[c + i], kf[i], u);
     }
     const float delta = beta * __builtin_fmaf(-alpha, u, vj);
-    // The key row is re-read chunk by chunk in the second pass instead of being kept
-    // live: a wave holds about 100 scalar registers, fewer than a 128-wide fp32 row.
 #pragma unroll
-    for (int c = 0; c < DK; c += kChunk) {
-        asm volatile("" ::: "memory");
-        float kf[kChunk < DK ? kChunk : DK];
-        Op<OPT>::template ld_row<(kChunk < DK ? kChunk : DK)>(kp + c, kf);
+    for (int c = 0; c < DK; c += C) {
+        float kf[C];
+        Op<OPT>::template ld_row<C>(kp + opaque(c), kf);
 #pragma unroll
-        for (int i = 0; i < (kChunk < DK ? kChunk : DK); ++i) S[c + i] = __builtin_fmaf(delta, kf[i], alpha * S[c + i]);
+        for (int i = 0; i < C; ++i) S[c + i] = __builtin_fmaf(delta, kf[i], alpha * S[c + i]);
     }
 }
 
 // o_j = R_j . q
 template <int DK, int OPT>
 __device__ __forceinline__ float gdn_row_output(const float (&S)[DK], const typename Op<OPT>::T* __restrict__ qp) {
+    constexpr int C = kChunk < DK ? kChunk : DK;
     float o = 0.f;
 #pragma unroll
-    for (int c = 0; c < DK; c += kChunk) {
-        asm volatile("" ::: "memory");
-        float qf[kChunk < DK ? kChunk : DK];
-        Op<OPT>::template ld_row<(kChunk < DK ? kChunk : DK)>(qp + c, qf);
+    for (int c = 0; c < DK; c += C) {
+        float qf[C];
+        Op<OPT>::template ld_row<C>(qp + opaque(c), qf);
 #pragma unroll
-        for (int i = 0; i < (kChunk < DK ? kChunk : DK); ++i) o = __builtin_fmaf(S[c + i], qf[i], o);
+        for (int i = 0; i < C; ++i) o = __builtin_fmaf(S[c + i], qf[i], o);
     }
     return o;
 }
