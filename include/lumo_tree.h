@@ -109,6 +109,10 @@ typedef struct {
     int32_t o_node_off, o_row_off, o_req, o_parent, o_depth, o_slot, o_row, o_conv_src;
     int32_t o_path_off, o_path_leaf, o_spine_off, o_spine, o_level_off, o_seg, o_seg_nodes;
     int32_t o_dfs, o_dfs_pos;
+    /* preorder tables (chunks of 32 preorder positions per request) */
+    int32_t n_anc;       /* ancestor slots per position: max(1, max_depth - 1)  */
+    int32_t n_chunks;    /* chunks over all requests                            */
+    int32_t o_pre_row, o_pre_depth, o_pre_anc, o_chunk_off, o_chunk_stack;
 } lumo_plan;
 
 /* A plan whose blob has been copied to device memory. */
@@ -147,7 +151,13 @@ typedef struct {
  *   seg[n_seg][4] = {request, source cut (-1 = pre-tree state), first entry, length},
  *   seg_nodes[n_seg_nodes][3] = {absolute row, writes output (0/1), cut to export (-1 none)},
  *   dfs[N] (per request: node ids in depth-first preorder, children by increasing id),
- *   dfs_pos[N] (position of each node in that order).
+ *   dfs_pos[N] (position of each node in that order),
+ *   pre_row[N], pre_depth[N] (absolute row and depth of the node at each preorder
+ *   position), pre_anc[N][n_anc][2] ({candidate slot, absolute row} of the ancestor at
+ *   depth m of that node; the slot is m when the ancestor precedes the position's
+ *   chunk of 32, else 16 + its offset in the chunk), chunk_off[n_req+1],
+ *   chunk_stack[n_chunks][16] (rows of the ancestors of each chunk's first node by
+ *   depth, -1 beyond its depth).
  * Returns LUMO_EDESC for malformed trees, LUMO_ESPACE (with out->n_words set)
  * when blob is NULL or too small, LUMO_EINVAL for bad arguments.
  */

@@ -28,11 +28,15 @@ struct ConvParams {
 
 template <int OPT> struct Vec8;
 template <> struct Vec8<0> {
-    static __device__ __forceinline__ void ld(const float* p, float (&v)[8]) {
-        const float4 a = reinterpret_cast<const float4*>(p)[0];
-        const float4 b = reinterpret_cast<const float4*>(p)[1];
-        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    struct Raw {
+        float4 a, b;
+    };
+    static __device__ __forceinline__ Raw ld_raw(const float* p) {
+        return Raw{reinterpret_cast<const float4*>(p)[0], reinterpret_cast<const float4*>(p)[1]};
+    }
+    static __device__ __forceinline__ void unpack(const Raw& w, float (&v)[8]) {
+        v[0] = w.a.x; v[1] = w.a.y; v[2] = w.a.z; v[3] = w.a.w;
+        v[4] = w.b.x; v[5] = w.b.y; v[6] = w.b.z; v[7] = w.b.w;
     }
     static __device__ __forceinline__ void st(float* p, const float (&v)[8]) {
         reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
@@ -40,8 +44,9 @@ template <> struct Vec8<0> {
     }
 };
 template <> struct Vec8<1> {
-    static __device__ __forceinline__ void ld(const uint16_t* p, float (&v)[8]) {
-        const uint4 a = reinterpret_cast<const uint4*>(p)[0];
+    using Raw = uint4;
+    static __device__ __forceinline__ Raw ld_raw(const uint16_t* p) { return reinterpret_cast<const uint4*>(p)[0]; }
+    static __device__ __forceinline__ void unpack(const Raw& a, float (&v)[8]) {
         v[0] = bf16_lo(a.x); v[1] = bf16_hi(a.x); v[2] = bf16_lo(a.y); v[3] = bf16_hi(a.y);
         v[4] = bf16_lo(a.z); v[5] = bf16_hi(a.z); v[6] = bf16_lo(a.w); v[7] = bf16_hi(a.w);
     }
@@ -69,8 +74,10 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
     t /= ng;
     const int cc = t % p.n_cchunks;
     const int l = t / p.n_cchunks;
-    const int c = (cc * 256 + (int)threadIdx.x) * 8;
-    if (c >= p.channels) return;
+    // channel-less threads stay alive: their lanes still carry node info for readlane
+    const int c0ch = (cc * 256 + (int)threadIdx.x) * 8;
+    const bool has_c = c0ch < p.channels;
+    const int c = has_c ? c0ch : p.channels - 8;
     const T* x = static_cast<const T*>(p.x);
     const T* hist = static_cast<const T*>(p.hist);
     T* y = static_cast<T*>(p.y);
@@ -85,32 +92,52 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) b0[e] = p.bias ? p.bias[(long)l * p.channels + c + e] : 0.f;
     const int n0 = grp * kNodesPerBlock;
-    const int n1 = min(p.total_nodes, n0 + kNodesPerBlock);
-#pragma unroll 2
-    for (int n = n0; n < n1; ++n) {
-        const int r = p.blob[p.o_req + n];
-        const int row = p.blob[p.o_row + n];
-        const int32_t* src = p.blob + p.o_conv_src + 4 * n;
-        float acc[8];
+    const int nn = min(p.total_nodes, n0 + kNodesPerBlock) - n0;
+    // node info of the run, one node per lane (lanes 0..31 of every wave), broadcast
+    // per node with readlane so the window loads depend on nothing but registers
+    const int li = (int)threadIdx.x & (kNodesPerBlock - 1);
+    const int mine = n0 + (li < nn ? li : 0);
+    const int i_req = p.blob[p.o_req + mine];
+    const int i_row = p.blob[p.o_row + mine];
+    int i_src[4];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = b0[e];
-        float xv[4][8];
+    for (int tap = 0; tap < 4; ++tap) i_src[tap] = p.blob[p.o_conv_src + 4 * mine + tap];
+    // kBatch nodes per step: all their window loads are issued before any is used
+    constexpr int kBatch = 4;
+    for (int i0 = 0; i0 < nn; i0 += kBatch) {
+        typename Vec8<OPT>::Raw raw[kBatch][4];
 #pragma unroll
-        for (int tap = 0; tap < 4; ++tap) {
-            const int s = src[tap];
-            const T* rp = s >= 0 ? x + ((long)l * p.total_rows + s) * p.channels + c
-                                 : hist + (((long)r * p.n_layers + l) * 3 + (-1 - s)) * p.channels + c;
-            Vec8<OPT>::ld(rp, xv[tap]);
+        for (int bi = 0; bi < kBatch; ++bi) {
+            const int i = min(i0 + bi, nn - 1);  // past the run: reload the last node, not stored
+            const int r = __builtin_amdgcn_readlane(i_req, i);
+#pragma unroll
+            for (int tap = 0; tap < 4; ++tap) {
+                const int s = __builtin_amdgcn_readlane(i_src[tap], i);
+                const T* rp = s >= 0 ? x + ((long)l * p.total_rows + s) * p.channels + c
+                                     : hist + (((long)r * p.n_layers + l) * 3 + (-1 - s)) * p.channels + c;
+                raw[bi][tap] = Vec8<OPT>::ld_raw(rp);
+            }
         }
 #pragma unroll
-        for (int tap = 0; tap < 4; ++tap)
+        for (int bi = 0; bi < kBatch; ++bi) {
+            if (i0 + bi >= nn) break;
+            const int row = __builtin_amdgcn_readlane(i_row, i0 + bi);
+            float acc[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[e] = __builtin_fmaf(wt[4 * e + tap], xv[tap][e], acc[e]);
-        if (p.act == 1) {
+            for (int e = 0; e < 8; ++e) acc[e] = b0[e];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[e] = acc[e] / (1.f + __expf(-acc[e]));
+            for (int tap = 0; tap < 4; ++tap) {
+                float xv[8];
+                Vec8<OPT>::unpack(raw[bi][tap], xv);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[e] = __builtin_fmaf(wt[4 * e + tap], xv[e], acc[e]);
+            }
+            if (p.act == 1) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[e] = acc[e] / (1.f + __expf(-acc[e]));
+            }
+            if (has_c) Vec8<OPT>::st(y + ((long)l * p.total_rows + row) * p.channels + c, acc);
         }
-        Vec8<OPT>::st(y + ((long)l * p.total_rows + row) * p.channels + c, acc);
     }
 }
 

@@ -14,5 +14,7 @@ void clear_error();
 // Seg record and seg_nodes entry widths of the plan blob.
 constexpr int kSegWords = 4;      // {request, source cut, first entry, length}
 constexpr int kSegNodeWords = 3;  // {absolute row, writes output, cut to export}
+constexpr int kPreChunk = 32;     // preorder positions per chunk
+constexpr int kPreStack = 16;     // path-stack candidate slots per chunk
 
 }  // namespace lumo

@@ -50,7 +50,7 @@ template <int D> struct Rec {
 
 struct WyParams {
     const int32_t* blob;
-    int32_t o_node_off, o_parent, o_depth, o_row, o_dfs, o_dfs_pos;
+    int32_t o_node_off, o_pre_row, o_pre_depth, o_pre_anc, o_chunk_off, o_chunk_stack, n_anc;
     int32_t n_layers, total_rows, total_nodes, h_k, h_v, group;
 };
 
@@ -78,36 +78,29 @@ __global__ __launch_bounds__(64) void wy_coef_kernel(WyParams p, const uint16_t*
     const int lane = threadIdx.x;
     const int base = p.blob[p.o_node_off + r];
     const int N = p.blob[p.o_node_off + r + 1] - base;
-    const int32_t* par = p.blob + p.o_parent + base;
-    const int32_t* dep = p.blob + p.o_depth + base;
-    const int32_t* row = p.blob + p.o_row + base;
-    const int32_t* dfs = p.blob + p.o_dfs + base;
-    const int32_t* dpos = p.blob + p.o_dfs_pos + base;
+    const int32_t* prow = p.blob + p.o_pre_row + base;
+    const int32_t* pdep = p.blob + p.o_pre_depth + base;
+    const int32_t* panc = p.blob + p.o_pre_anc + 2L * base * p.n_anc;
+    const int32_t* stack = p.blob + p.o_chunk_stack + (long)kStack * p.blob[p.o_chunk_off + r];
     const long krow0 = (long)l * p.total_rows;
 
-    for (int c0 = 0; c0 < N; c0 += kTile) {
-        const int f = dfs[c0];
-        const int df = dep[f];
-        // candidate rows of this lane in the two candidate tiles
+    for (int c0 = 0; c0 < N; c0 += kTile, stack += kStack) {
+        // Gram candidates: slots 0..15 the chunk's path stack, 16..47 the chunk itself
         int cand[2];
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt) {
             const int ci = mt * kTile + lane % kTile;
-            int node = -1;
+            int rw = -1;
             if (ci < kStack) {
-                if (ci < df) {
-                    int x = f;
-                    for (int s = df; s > ci; --s) x = par[x];
-                    node = x;
-                }
+                rw = stack[ci];
             } else if (ci < kStack + kTile) {
                 const int pos = c0 + ci - kStack;
-                if (pos < N) node = dfs[pos];
+                if (pos < N) rw = prow[pos];
             }
-            cand[mt] = node >= 0 ? row[node] : -1;
+            cand[mt] = rw;
         }
         const int tpos = c0 + lane % kTile;
-        const int trow = tpos < N ? row[dfs[tpos]] : -1;
+        const int trow = tpos < N ? prow[tpos] : -1;
         f32x16 acc[2][2];
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt)
@@ -143,26 +136,29 @@ __global__ __launch_bounds__(64) void wy_coef_kernel(WyParams p, const uint16_t*
         const int t = lane % kTile;
         const int pos = c0 + t;
         if (pos < N) {
-            const int n = dfs[pos];
-            const int d = dep[n];
-            const int rn = row[n];
+            const int d = pdep[pos];
+            const int rn = prow[pos];
+            int ci[D], arow[D];
+#pragma unroll
+            for (int m = 0; m < D; ++m) {
+                ci[m] = m < d ? panc[2 * ((long)pos * p.n_anc + m)] : 0;
+                arow[m] = m < d ? panc[2 * ((long)pos * p.n_anc + m) + 1] : rn;
+            }
             for (int hv = hk * p.group + lane / kTile; hv < (hk + 1) * p.group; hv += 2) {
                 float* out = coef + (((long)l * p.h_v + hv) * p.total_nodes + base + pos) * W;
                 const long gi = (krow0 + rn) * p.h_v + hv;
                 const float bn = beta[gi];
-                float gam = __expf(g[gi]);  // running product of alpha from node n upward
-                int x = n;
-                for (int m = d - 1; m >= 0; --m) {
-                    x = par[x];  // ancestor at depth m
-                    const int px = dpos[x];
-                    const int ci = px >= c0 ? kStack + (px - c0) : m;
-                    out[8 + m] = bn * gam * G[ci][t];
-                    out[8 + D + m] = gam * G[ci][kTile + t];
-                    gam *= __expf(g[(krow0 + row[x]) * p.h_v + hv]);
-                }
-                for (int m = d; m < D; ++m) {
-                    out[8 + m] = 0.f;
-                    out[8 + D + m] = 0.f;
+                float al[D];
+#pragma unroll
+                for (int m = 0; m < D; ++m) al[m] = __expf(g[(krow0 + arow[m]) * p.h_v + hv]);
+                // Gamma(a_m -> n) = product of alpha over the ancestors deeper than m and n
+                float gam = __expf(g[gi]);
+#pragma unroll
+                for (int m = D - 1; m >= 0; --m) {
+                    const bool live = m < d;
+                    out[8 + m] = live ? bn * gam * G[ci[m]][t] : 0.f;
+                    out[8 + D + m] = live ? gam * G[ci[m]][kTile + t] : 0.f;
+                    if (live) gam *= al[m];
                 }
                 out[0] = __int_as_float(rn);
                 out[1] = __int_as_float(d);
@@ -217,65 +213,135 @@ __device__ __forceinline__ void stage_issue(Stage<D>& st, const float* __restric
     }
 }
 
+// Key and query rows of a chunk, staged once per block and shared by its waves:
+// [key | query][32 nodes][16 slots of 8 bf16]; key block kb of node n sits in slot
+// kb ^ (n & 15), so the fragment reads of a half-wave (32 nodes, one key block)
+// spread over all banks.
+struct KQTile {
+    uint4 slot[2 * kTile * 16];
+};
+
+constexpr int kMaxWaves = 4;  // 2 value heads x 2 column halves per block
+
 template <int D>
-__global__ __launch_bounds__(64, 2) void wy_main_kernel(WyParams p, const uint16_t* __restrict__ kmat,
-                                                        const uint16_t* __restrict__ qmat,
-                                                        const uint16_t* __restrict__ vmat,
-                                                        const float* __restrict__ state0,
-                                                        const float* __restrict__ coef, uint16_t* __restrict__ out) {
+constexpr size_t wy_lds_bytes() {
+    return sizeof(KQTile) + kMaxWaves * 2 * sizeof(Stage<D>);
+}
+
+template <int D, int NVH>
+__global__ __launch_bounds__(256, 2) void wy_main_kernel(WyParams p, const uint16_t* __restrict__ kmat,
+                                                         const uint16_t* __restrict__ qmat,
+                                                         const uint16_t* __restrict__ vmat,
+                                                         const float* __restrict__ state0,
+                                                         const float* __restrict__ coef, uint16_t* __restrict__ out) {
     constexpr int W = Rec<D>::kWords;
-    __shared__ Stage<D> stage[2];
+    extern __shared__ uint4 lds[];
+    KQTile& tile = *reinterpret_cast<KQTile*>(lds);
+    constexpr int nthr = 128 * NVH;           // NVH value heads x 2 column halves per block
+    const int tid = (int)threadIdx.x;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    Stage<D>* stage = reinterpret_cast<Stage<D>*>(lds + sizeof(KQTile) / 16) + 2 * wave;
+
     int b = xcd_remap(blockIdx.x, gridDim.x);
-    const int half = b & 1;
-    b >>= 1;
-    const int h = b % p.h_v;
-    b /= p.h_v;
+    const int pairs = p.group / NVH;
+    const int pp = b % pairs;
+    b /= pairs;
+    const int hk = b % p.h_k;
+    b /= p.h_k;
     const int l = b % p.n_layers;
     const int r = b / p.n_layers;
-    const int hk = h / p.group;
-    const int lane = threadIdx.x;
+    const int h = hk * p.group + pp * NVH + (wave >> 1);
+    const int half = wave & 1;
     const int j0 = 64 * half;
     const int base = p.blob[p.o_node_off + r];
     const int N = p.blob[p.o_node_off + r + 1] - base;
-    if (N <= 0) return;
-    const int32_t* row = p.blob + p.o_row + base;
-    const int32_t* dfs = p.blob + p.o_dfs + base;
+    if (N <= 0) return;  // uniform over the block
+    const int32_t* prow = p.blob + p.o_pre_row + base;
     const long krow0 = (long)l * p.total_rows;
     const float* cbase = coef + (((long)l * p.h_v + h) * p.total_nodes + base) * W;
 
-    // row of preorder node c0 + lane%32 (lanes past the request read node 0's row)
+    // rows feeding this thread's tile slots (slot g = round * nthr + tid) for chunk c0
+    constexpr int rounds = 2 * kTile * 16 / nthr;  // 4 or 8
+    auto tile_rows = [&](int c0, int (&rows)[rounds]) {
+#pragma unroll
+        for (int j = 0; j < rounds; ++j) {
+            const int n = ((j * nthr + tid) >> 4) & (kTile - 1);
+            const int pos = c0 + n;
+            rows[j] = prow[pos < N ? pos : 0];
+        }
+    };
+    auto tile_issue = [&](const int (&rows)[rounds]) {
+#pragma unroll
+        for (int j = 0; j < rounds; ++j) {
+            const int g = j * nthr + tid;
+            const int n = (g >> 4) & (kTile - 1);
+            const int kb = (g & 15) ^ (n & 15);
+            const uint16_t* src = (g >= kTile * 16 ? qmat : kmat) + ((krow0 + rows[j]) * p.h_k + hk) * kD + 8 * kb;
+            __builtin_amdgcn_global_load_lds(src, (lds_void*)&tile.slot[j * nthr + 64 * wave], 16, 0, 0);
+        }
+    };
     auto node_row = [&](int c0) {
         const int pos = c0 + lane % kTile;
-        return row[dfs[pos < N ? pos : 0]];
+        return prow[pos < N ? pos : 0];
     };
-    int trow = node_row(0);
-    stage_issue<D>(stage[0], cbase, vmat, 0, min(kTile, N), trow, krow0, p.h_v, h, j0, lane);
 
-    // R0 columns j0 + 32 ct + lane%32 as MFMA B fragments: keys 16 s + 8 (lane/32) + e,
-    // each fp32 value held as bf16 hi + bf16 lo (16 significant bits).
+    int trows[rounds];
+    tile_rows(0, trows);
+    tile_issue(trows);
+    int vrow = node_row(0);
+    stage_issue<D>(stage[0], cbase, vmat, 0, min(kTile, N), vrow, krow0, p.h_v, h, j0, lane);
+
+    // R0 columns j0 + 32 ct + lane%32 as MFMA B fragments: keys 16 s + 8 (lane/32) + e.
     const float* S = state0 + (((long)r * p.n_layers + l) * p.h_v + h) * (long)(kD * kD);
+    const float* Sl = S + (long)(8 * (lane / kTile)) * kD + j0 + lane % kTile;
     bf16x8 bhi[2][kD / 16], blo[2][kD / 16];
+    // Each fp32 value x is held as hi + lo: hi = x truncated to bf16, lo = the exact
+    // remainder x - hi rounded to bf16 (|x - hi - lo| <= 2^-15 |x|).
 #pragma unroll
     for (int ct = 0; ct < 2; ++ct)
 #pragma unroll
-        for (int s = 0; s < kD / 16; ++s)
+        for (int s = 0; s < kD / 16; ++s) {
+            uint32_t hw[4], lw[4];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float x = S[(long)(16 * s + 8 * (lane / kTile) + e) * kD + j0 + kTile * ct + lane % kTile];
-                const float hi = bf16_round(x);
-                bhi[ct][s][e] = (__bf16)hi;
-                blo[ct][s][e] = (__bf16)bf16_round(x - hi);
+            for (int e2 = 0; e2 < 4; ++e2) {
+                uint32_t h2[2], l2[2];
+#pragma unroll
+                for (int qq = 0; qq < 2; ++qq) {
+                    const uint32_t xb = __float_as_uint(Sl[(long)(16 * s + 2 * e2 + qq) * kD + kTile * ct]);
+                    const uint32_t hb = xb & 0xffff0000u;
+                    const uint32_t rb = __float_as_uint(__uint_as_float(xb) - __uint_as_float(hb));
+                    h2[qq] = hb;
+                    l2[qq] = rb + 0x7fffu + ((rb >> 16) & 1u);  // round to nearest even, upper half kept
+                }
+                hw[e2] = __builtin_amdgcn_perm(h2[1], h2[0], 0x07060302u);  // {hi(e+1), hi(e)} upper halves
+                lw[e2] = __builtin_amdgcn_perm(l2[1], l2[0], 0x07060302u);
             }
+            bhi[ct][s] = __builtin_bit_cast(bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
+            blo[ct][s] = __builtin_bit_cast(bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
+        }
 
     float dst[D];
 #pragma unroll
     for (int m = 0; m < D; ++m) dst[m] = 0.f;
     const long vcol = j0 + lane;
+    const int n_a = lane % kTile;               // node of this lane's A fragment rows
+    const int kb0 = lane / kTile;               // key block offset within a 16-key step
 
     for (int c0 = 0, buf = 0; c0 < N; c0 += kTile, buf ^= 1) {
         const int nv = min(kTile, N - c0);
-        const bool tvalid = lane % kTile < nv;
-        const int nrow = c0 + kTile < N ? node_row(c0 + kTile) : 0;  // rows of the next chunk
+        const bool more = c0 + kTile < N;
+        if (more) {  // rows of the next chunk, needed once this chunk's tile is consumed
+            tile_rows(c0 + kTile, trows);
+            vrow = node_row(c0 + kTile);
+        }
+        // this chunk's tile and staging have landed for every wave of the block
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        // the other staging buffer was last read by the previous chunk's recursion
+        if (more)
+            stage_issue<D>(stage[buf ^ 1], cbase, vmat, c0 + kTile, min(kTile, N - c0 - kTile), vrow, krow0,
+                           p.h_v, h, j0, lane);
         f32x16 ak[2], aq[2];
 #pragma unroll
         for (int ct = 0; ct < 2; ++ct)
@@ -286,10 +352,9 @@ __global__ __launch_bounds__(64, 2) void wy_main_kernel(WyParams p, const uint16
             }
 #pragma unroll
         for (int s = 0; s < kD / 16; ++s) {
-            const int kk = 16 * s + 8 * (lane / kTile);
-            const long ki = ((krow0 + trow) * p.h_k + hk) * kD + kk;
-            const bf16x8 fk = tvalid ? load_bf16x8(kmat + ki) : zero_bf16x8();
-            const bf16x8 fq = tvalid ? load_bf16x8(qmat + ki) : zero_bf16x8();
+            const int kb = 2 * s + kb0;
+            const bf16x8 fk = __builtin_bit_cast(bf16x8, tile.slot[n_a * 16 + (kb ^ (n_a & 15))]);
+            const bf16x8 fq = __builtin_bit_cast(bf16x8, tile.slot[(kTile + n_a) * 16 + (kb ^ (n_a & 15))]);
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) {
                 ak[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fk, bhi[ct][s], ak[ct], 0, 0, 0);
@@ -298,6 +363,8 @@ __global__ __launch_bounds__(64, 2) void wy_main_kernel(WyParams p, const uint16
                 aq[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fq, blo[ct][s], aq[ct], 0, 0, 0);
             }
         }
+        __syncthreads();  // every wave has read the tile: it may be refilled
+        if (more) tile_issue(trows);
         // Lane l holds column 32 ct + l%32 of tile ct for nodes 8(e/4) + 4(l/32) + e%4.
         // Swapping tile 0's upper half-wave with tile 1's lower half-wave leaves every
         // lane with one column (j0 + lane): [0][e] = node 8(e/4) + e%4, [1][e] = node 8(e/4) + 4 + e%4.
@@ -310,12 +377,6 @@ __global__ __launch_bounds__(64, 2) void wy_main_kernel(WyParams p, const uint16
             aq[0][e] = __uint_as_float(sq[0]);
             aq[1][e] = __uint_as_float(sq[1]);
         }
-        // this chunk's staging has landed; the other buffer is free for the next chunk
-        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-        __syncthreads();
-        if (c0 + kTile < N)
-            stage_issue<D>(stage[buf ^ 1], cbase, vmat, c0 + kTile, min(kTile, N - c0 - kTile), nrow, krow0, p.h_v,
-                           h, j0, lane);
         const float* rec = reinterpret_cast<const float*>(stage[buf].rec);
         const uint16_t* vs = reinterpret_cast<const uint16_t*>(stage[buf].v);
 #pragma clang loop unroll(full)
@@ -342,8 +403,23 @@ __global__ __launch_bounds__(64, 2) void wy_main_kernel(WyParams p, const uint16
             for (int m = 0; m < D; ++m) dst[m] = (m == d) ? delta : dst[m];
             out[((krow0 + rn) * p.h_v + h) * kD + vcol] = f32_to_bf16(ov);
         }
-        trow = nrow;
     }
+}
+
+template <int D, int NVH>
+hipError_t launch_wy_main(const lumo_gdn_dims& d, const WyParams& p, const uint16_t* k, const uint16_t* q,
+                          const uint16_t* v, const GdnArgs& a, hipStream_t s) {
+    const long mb = (long)d.n_req * d.n_layers * d.h_k * (p.group / NVH);
+    static bool attr_set = false;  // LDS above the 64 KB default (same value for every call)
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&wy_main_kernel<D, NVH>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)wy_lds_bytes<D>());
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    hipLaunchKernelGGL((wy_main_kernel<D, NVH>), dim3((unsigned)mb), dim3(128 * NVH), wy_lds_bytes<D>(), s, p, k, q,
+                       v, a.state0, a.ws, static_cast<uint16_t*>(a.o));
+    return hipGetLastError();
 }
 
 template <int D>
@@ -352,11 +428,12 @@ hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     WyParams p;
     p.blob = desc.blob;
     p.o_node_off = pl.o_node_off;
-    p.o_parent = pl.o_parent;
-    p.o_depth = pl.o_depth;
-    p.o_row = pl.o_row;
-    p.o_dfs = pl.o_dfs;
-    p.o_dfs_pos = pl.o_dfs_pos;
+    p.o_pre_row = pl.o_pre_row;
+    p.o_pre_depth = pl.o_pre_depth;
+    p.o_pre_anc = pl.o_pre_anc;
+    p.o_chunk_off = pl.o_chunk_off;
+    p.o_chunk_stack = pl.o_chunk_stack;
+    p.n_anc = pl.n_anc;
     p.n_layers = d.n_layers;
     p.total_rows = pl.total_rows;
     p.total_nodes = pl.total_nodes;
@@ -370,10 +447,11 @@ hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     hipLaunchKernelGGL(wy_coef_kernel<D>, dim3((unsigned)cb), dim3(64), 0, s, p, k, q, a.g, a.beta, a.ws);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const long mb = (long)d.n_req * d.n_layers * d.h_v * 2;
-    hipLaunchKernelGGL(wy_main_kernel<D>, dim3((unsigned)mb), dim3(64), 0, s, p, k, q, v, a.state0, a.ws,
-                       static_cast<uint16_t*>(a.o));
-    return hipGetLastError();
+    // one block per (request, layer, key head, pair of value heads): the pair's
+    // waves share the staged key and query rows
+    if (p.group % 2 == 0)
+        return launch_wy_main<D, 2>(d, p, k, q, v, a, s);
+    return launch_wy_main<D, 1>(d, p, k, q, v, a, s);
 }
 
 }  // namespace

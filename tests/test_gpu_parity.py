@@ -368,6 +368,20 @@ def test_wy_identical_sibling_subtrees():
     gu.check_outputs(wl, gu.to_np(o.cuda()), [(0, 0, h) for h in range(4)])
 
 
+@pytest.mark.parametrize("h_k,h_v", [(4, 4), (2, 8), (1, 2)])
+def test_wy_head_groupings(h_k, h_v):
+    """One, two and four value heads per key head (blocks of one or two value heads)."""
+    rng = np.random.default_rng(17)
+    parents = [trees.random_tree(rng, 45, 8, trees.bmax_uniform(4)), trees.FIG1_PARENT]
+    wl = pins.make_wl(parents, d_k=128, d_v=128, h_k=h_k, h_v=h_v, op_dtype=ops.BF16,
+                      n_rows=[48, 7], n_layers=2, max_path=8)
+    wl.arrays = ops.make_gdn_operands(23, n_req=2, n_layers=2, total_rows=55, h_k=h_k, h_v=h_v,
+                                      d_k=128, d_v=128, op_dtype=ops.BF16)
+    st = run(wl, L.LUMO_POLICY_WY, with_conv=False, commit=False)
+    inst = [(r, l, h) for r in range(2) for l in range(2) for h in range(h_v)]
+    gu.check_outputs(wl, gu.to_np(st.o), inst)
+
+
 def test_wy_deep_chain_and_ragged_requests():
     """Chains of 17 nodes (the WY depth limit), 1-node and 40-node requests, padding."""
     rng = np.random.default_rng(9)

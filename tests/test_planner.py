@@ -72,6 +72,34 @@ def _check_against_oracle(parents, n_rows, node_off, policy):
             for i in range(n):   # children visited in increasing id
                 cp = [pos[c] for c in ch[i]]
                 assert cp == sorted(cp)
+    # preorder tables used by the WY kernels (meaningful for paths of <= 17 nodes)
+    if plan.max_depth <= 17:
+        A = plan.n_anc
+        pre_anc = sec("pre_anc", 2 * N * A).reshape(N, A, 2)
+        chunk_off = sec("chunk_off", len(parents) + 1)
+        stacks = sec("chunk_stack", 16 * plan.n_chunks).reshape(-1, 16)
+        for r, par in enumerate(parents):
+            b = int(node_off[r])
+            rows = oplan.rows_of(par, int(row_off[r]))
+            dfs = list(sec("dfs", N)[b:b + len(par)])
+            dep = oplan.depth(par)
+            assert int(chunk_off[r + 1] - chunk_off[r]) == (len(par) + 31) // 32
+            for pos, x in enumerate(dfs):
+                assert sec("pre_row", N)[b + pos] == rows[x]
+                assert sec("pre_depth", N)[b + pos] == dep[x]
+                anc = oplan.ancestry(par, x)[:-1]
+                c0 = pos - pos % 32
+                for m in range(A):
+                    if m < len(anc):
+                        ap = dfs.index(anc[m])
+                        want = 16 + ap - c0 if ap >= c0 else m
+                        assert tuple(pre_anc[b + pos, m]) == (want, rows[anc[m]])
+                    else:
+                        assert tuple(pre_anc[b + pos, m]) == (-1, -1)
+                if pos == c0:
+                    st = stacks[chunk_off[r] + pos // 32]
+                    fanc = oplan.ancestry(par, x)[:-1]
+                    assert list(st) == [rows[fanc[m]] if m < len(fanc) else -1 for m in range(16)]
     assert list(sec("path_leaf", plan.n_paths)) == leaves
     assert list(sec("spine", plan.n_spine)) == spines
     assert plan.max_depth == max(max(oplan.depth(p)) + 1 for p in parents)
