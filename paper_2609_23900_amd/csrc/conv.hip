@@ -52,10 +52,10 @@ template <> struct Vec8<1> {
     }
     static __device__ __forceinline__ void st(uint16_t* p, const float (&v)[8]) {
         uint4 a;
-        a.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
-        a.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
-        a.z = (uint32_t)f32_to_bf16(v[4]) | ((uint32_t)f32_to_bf16(v[5]) << 16);
-        a.w = (uint32_t)f32_to_bf16(v[6]) | ((uint32_t)f32_to_bf16(v[7]) << 16);
+        a.x = f32x2_to_bf16x2(v[0], v[1]);
+        a.y = f32x2_to_bf16x2(v[2], v[3]);
+        a.z = f32x2_to_bf16x2(v[4], v[5]);
+        a.w = f32x2_to_bf16x2(v[6], v[7]);
         reinterpret_cast<uint4*>(p)[0] = a;
     }
 };

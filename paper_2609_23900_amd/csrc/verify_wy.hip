@@ -61,8 +61,6 @@ __device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t* p) {
 
 __device__ __forceinline__ bf16x8 zero_bf16x8() { return __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0)); }
 
-__device__ __forceinline__ float bf16_round(float x) { return __uint_as_float(((uint32_t)f32_to_bf16(x)) << 16); }
-
 // ------------------------------------------------------------------ coefficients
 template <int D>
 __global__ __launch_bounds__(64) void wy_coef_kernel(WyParams p, const uint16_t* __restrict__ kmat,
@@ -194,20 +192,24 @@ template <int D>
 __device__ __forceinline__ void stage_issue(Stage<D>& st, const float* __restrict__ cbase,
                                             const uint16_t* __restrict__ vmat, int c0, int nv, int myrow,
                                             long krow0, int h_v, int h, int j0, int lane) {
-    constexpr int W = Rec<D>::kWords;
-    // lane i of round k copies float4 (64 k + i) to LDS slot 64 k + i; slots past the
-    // chunk's records receive a copy of its last record and are never read.
-    const float4* src = reinterpret_cast<const float4*>(cbase + (long)c0 * W);
-    const int n4 = nv * W / 4;
+    constexpr int W4 = Rec<D>::kWords / 4;
+    // lane i of round k copies float4 (64 k + i) to LDS slot 64 k + i; the record slots
+    // of nodes past the chunk's end receive copies of its last record.
+    const float4* src = reinterpret_cast<const float4*>(cbase + (long)c0 * W4 * 4);
 #pragma unroll
-    for (int k = 0; k < Stage<D>::kRec4 / 64; ++k)
-        __builtin_amdgcn_global_load_lds(src + min(64 * k + lane, n4 - 1), (lds_void*)&st.rec[64 * k], 16, 0, 0);
-    // value rows: slot p = 64 k + lane holds node p / 8, columns j0 + 8 (p % 8) .. + 7
+    for (int k = 0; k < Stage<D>::kRec4 / 64; ++k) {
+        const int i = 64 * k + lane;
+        const int n = i / W4;
+        __builtin_amdgcn_global_load_lds(src + (n < nv ? i : (nv - 1) * W4 + i % W4), (lds_void*)&st.rec[64 * k], 16,
+                                         0, 0);
+    }
+    // value rows: slot p = 64 k + lane holds node p / 8, columns j0 + 8 (p % 8) .. + 7;
+    // myrow of lane n is the row of node n (the last node's row past the end)
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int pidx = 64 * k + lane;
         const int n = pidx >> 3;
-        const int rn = __shfl(myrow, n < nv ? n : 0);
+        const int rn = __shfl(myrow, n);
         const uint16_t* g = vmat + ((krow0 + rn) * h_v + h) * kD + j0 + 8 * (pidx & 7);
         __builtin_amdgcn_global_load_lds(g, (lds_void*)&st.v[64 * k], 16, 0, 0);
     }
@@ -239,7 +241,7 @@ __global__ __launch_bounds__(256, 2) void wy_main_kernel(WyParams p, const uint1
     KQTile& tile = *reinterpret_cast<KQTile*>(lds);
     constexpr int nthr = 128 * NVH;           // NVH value heads x 2 column halves per block
     const int tid = (int)threadIdx.x;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: head and half in SGPRs
     const int lane = tid & 63;
     Stage<D>* stage = reinterpret_cast<Stage<D>*>(lds + sizeof(KQTile) / 16) + 2 * wave;
 
@@ -268,7 +270,7 @@ __global__ __launch_bounds__(256, 2) void wy_main_kernel(WyParams p, const uint1
         for (int j = 0; j < rounds; ++j) {
             const int n = ((j * nthr + tid) >> 4) & (kTile - 1);
             const int pos = c0 + n;
-            rows[j] = prow[pos < N ? pos : 0];
+            rows[j] = prow[pos < N ? pos : N - 1];
         }
     };
     auto tile_issue = [&](const int (&rows)[rounds]) {
@@ -283,7 +285,7 @@ __global__ __launch_bounds__(256, 2) void wy_main_kernel(WyParams p, const uint1
     };
     auto node_row = [&](int c0) {
         const int pos = c0 + lane % kTile;
-        return prow[pos < N ? pos : 0];
+        return prow[pos < N ? pos : N - 1];
     };
 
     int trows[rounds];
@@ -297,7 +299,7 @@ __global__ __launch_bounds__(256, 2) void wy_main_kernel(WyParams p, const uint1
     const float* Sl = S + (long)(8 * (lane / kTile)) * kD + j0 + lane % kTile;
     bf16x8 bhi[2][kD / 16], blo[2][kD / 16];
     // Each fp32 value x is held as hi + lo: hi = x truncated to bf16, lo = the exact
-    // remainder x - hi rounded to bf16 (|x - hi - lo| <= 2^-15 |x|).
+    // remainder x - hi rounded to nearest bf16 (|x - hi - lo| <= 2^-15 |x|).
 #pragma unroll
     for (int ct = 0; ct < 2; ++ct)
 #pragma unroll
@@ -305,31 +307,26 @@ __global__ __launch_bounds__(256, 2) void wy_main_kernel(WyParams p, const uint1
             uint32_t hw[4], lw[4];
 #pragma unroll
             for (int e2 = 0; e2 < 4; ++e2) {
-                uint32_t h2[2], l2[2];
-#pragma unroll
-                for (int qq = 0; qq < 2; ++qq) {
-                    const uint32_t xb = __float_as_uint(Sl[(long)(16 * s + 2 * e2 + qq) * kD + kTile * ct]);
-                    const uint32_t hb = xb & 0xffff0000u;
-                    const uint32_t rb = __float_as_uint(__uint_as_float(xb) - __uint_as_float(hb));
-                    h2[qq] = hb;
-                    l2[qq] = rb + 0x7fffu + ((rb >> 16) & 1u);  // round to nearest even, upper half kept
-                }
-                hw[e2] = __builtin_amdgcn_perm(h2[1], h2[0], 0x07060302u);  // {hi(e+1), hi(e)} upper halves
-                lw[e2] = __builtin_amdgcn_perm(l2[1], l2[0], 0x07060302u);
+                const uint32_t x0 = __float_as_uint(Sl[(long)(16 * s + 2 * e2) * kD + kTile * ct]);
+                const uint32_t x1 = __float_as_uint(Sl[(long)(16 * s + 2 * e2 + 1) * kD + kTile * ct]);
+                hw[e2] = __builtin_amdgcn_perm(x1, x0, 0x07060302u);  // {hi(x1), hi(x0)}: upper halves
+                lw[e2] = f32x2_to_bf16x2(__uint_as_float(x0) - __uint_as_float(x0 & 0xffff0000u),
+                                         __uint_as_float(x1) - __uint_as_float(x1 & 0xffff0000u));
             }
             bhi[ct][s] = __builtin_bit_cast(bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
             blo[ct][s] = __builtin_bit_cast(bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
         }
 
-    float dst[D];
+    // delta of the current path by depth; slot D takes the writes of nodes at depth D,
+    // which have no descendants (their delta is never read)
+    float dst[D + 1];
 #pragma unroll
-    for (int m = 0; m < D; ++m) dst[m] = 0.f;
-    const long vcol = j0 + lane;
+    for (int m = 0; m <= D; ++m) dst[m] = 0.f;
+    const int vcol = j0 + lane;
     const int n_a = lane % kTile;               // node of this lane's A fragment rows
     const int kb0 = lane / kTile;               // key block offset within a 16-key step
 
     for (int c0 = 0, buf = 0; c0 < N; c0 += kTile, buf ^= 1) {
-        const int nv = min(kTile, N - c0);
         const bool more = c0 + kTile < N;
         if (more) {  // rows of the next chunk, needed once this chunk's tile is consumed
             tile_rows(c0 + kTile, trows);
@@ -379,15 +376,17 @@ __global__ __launch_bounds__(256, 2) void wy_main_kernel(WyParams p, const uint1
         }
         const float* rec = reinterpret_cast<const float*>(stage[buf].rec);
         const uint16_t* vs = reinterpret_cast<const uint16_t*>(stage[buf].v);
-#pragma clang loop unroll(full)
+        // Straight-line over all 32 slots: slots past the chunk's end hold exact copies of
+        // its last node (tile rows, value row, record), so they recompute that node's
+        // delta and output bit for bit and store the same value to the same place.
+#pragma unroll
         for (int n = 0; n < kTile; ++n) {
-            if (n >= nv) continue;  // full unroll keeps the register-indexed tiles static
             const int e = 4 * (n / 8) + n % 4;
             const float pk = ((n / 4) & 1) ? ak[1][e] : ak[0][e];
             const float pq = ((n / 4) & 1) ? aq[1][e] : aq[0][e];
             const float* cf = rec + n * W;
-            const int rn = __float_as_int(cf[0]);
-            const int d = __float_as_int(cf[1]);
+            const int rn = __builtin_amdgcn_readfirstlane(__float_as_int(cf[0]));  // uniform
+            const int d = __builtin_amdgcn_readfirstlane(__float_as_int(cf[1]));
             const float bn = cf[2], gm = cf[3], cn = cf[4];
             const float vj = __uint_as_float(((uint32_t)vs[n * 64 + lane]) << 16);
             float sa = 0.f, sb = 0.f;
@@ -399,9 +398,9 @@ __global__ __launch_bounds__(256, 2) void wy_main_kernel(WyParams p, const uint1
             const float u = __builtin_fmaf(-gm, pk, vj);           // v - gamma R0 k
             const float delta = __builtin_fmaf(bn, u, -sa);        // beta u - sum A delta
             const float ov = __builtin_fmaf(cn, delta, __builtin_fmaf(gm, pq, sb));
-#pragma unroll
-            for (int m = 0; m < D; ++m) dst[m] = (m == d) ? delta : dst[m];
-            out[((krow0 + rn) * p.h_v + h) * kD + vcol] = f32_to_bf16(ov);
+            dst[d < D ? d : D] = delta;  // uniform index: an indexed register write
+            uint16_t* orow = out + ((krow0 + rn) * p.h_v + h) * kD;
+            orow[vcol] = f32_to_bf16(ov);
         }
     }
 }
