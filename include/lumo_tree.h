@@ -77,10 +77,10 @@ typedef enum {
     LUMO_POLICY_RECOMPUTE = 2,
     /* Tree WY form: R_t = gamma_t R0 + sum over ancestors of decayed rank-1
      * terms; the R0 [K | Q] products run on MFMA (R0 as bf16 hi + lo), the
-     * ancestor-masked triangular system on the vector units. Two launches; the
-     * workspace holds per-node coefficient records; no state dump. bf16 operands,
-     * d_k = d_v = 128, paths of at most 17 nodes. Outputs agree with the
-     * sequential schedules to rounding, not bitwise. */
+     * ancestor-masked triangular system on the vector units. One launch, no
+     * workspace, no state dump. bf16 operands, d_k = d_v = 128, paths of at most
+     * 17 nodes. Outputs agree with the sequential schedules to rounding, not
+     * bitwise. */
     LUMO_POLICY_WY = 3
 } lumo_policy;
 
@@ -110,9 +110,8 @@ typedef struct {
     int32_t o_path_off, o_path_leaf, o_spine_off, o_spine, o_level_off, o_seg, o_seg_nodes;
     int32_t o_dfs, o_dfs_pos;
     /* preorder tables (chunks of 32 preorder positions per request) */
-    int32_t n_anc;       /* ancestor slots per position: max(1, max_depth - 1)  */
     int32_t n_chunks;    /* chunks over all requests                            */
-    int32_t o_pre_row, o_pre_depth, o_pre_anc, o_chunk_off, o_chunk_stack;
+    int32_t o_pre_row, o_pre_depth, o_pre_ci, o_chunk_off, o_chunk_stack;
 } lumo_plan;
 
 /* A plan whose blob has been copied to device memory. */
@@ -153,9 +152,10 @@ typedef struct {
  *   dfs[N] (per request: node ids in depth-first preorder, children by increasing id),
  *   dfs_pos[N] (position of each node in that order),
  *   pre_row[N], pre_depth[N] (absolute row and depth of the node at each preorder
- *   position), pre_anc[N][n_anc][2] ({candidate slot, absolute row} of the ancestor at
- *   depth m of that node; the slot is m when the ancestor precedes the position's
- *   chunk of 32, else 16 + its offset in the chunk), chunk_off[n_req+1],
+ *   position), pre_ci[N][4] (16 bytes, little-endian: byte m is the Gram candidate
+ *   slot of the node's ancestor at depth m: m when the ancestor precedes the position's
+ *   chunk of 32, else 16 + its offset in the chunk; 0xff past the node's depth),
+ *   chunk_off[n_req+1],
  *   chunk_stack[n_chunks][16] (rows of the ancestors of each chunk's first node by
  *   depth, -1 beyond its depth).
  * Returns LUMO_EDESC for malformed trees, LUMO_ESPACE (with out->n_words set)
@@ -168,9 +168,8 @@ lumo_status lumo_tree_plan(int32_t n_req, const int32_t* node_off, const int32_t
 /*
  * lumo_tree_gdn_workspace_bytes - device workspace needed by lumo_tree_gdn_verify
  * for this plan: PATHS / TWO_LEVEL one fp32 d_k x d_v matrix per (exported cut,
- * layer, value head) (the cut-state payload of Eq. (4), Sec. IV-C); WY one
- * coefficient record of 8 + 2 D floats per (node, layer, value head), D = 8 when
- * paths have at most 9 nodes, else 16; RECOMPUTE 0.
+ * layer, value head) (the cut-state payload of Eq. (4), Sec. IV-C); RECOMPUTE and
+ * WY 0.
  */
 size_t lumo_tree_gdn_workspace_bytes(const lumo_gdn_dims* dims, const lumo_plan* plan);
 

@@ -48,8 +48,8 @@ _PLAN_FIELDS = ("n_req", "total_nodes", "total_rows", "max_nodes", "max_depth", 
                 "max_level_seg", "max_seg_len", "n_words", "o_node_off", "o_row_off", "o_req",
                 "o_parent", "o_depth", "o_slot", "o_row", "o_conv_src", "o_path_off",
                 "o_path_leaf", "o_spine_off", "o_spine", "o_level_off", "o_seg", "o_seg_nodes",
-                "o_dfs", "o_dfs_pos", "n_anc", "n_chunks", "o_pre_row", "o_pre_depth",
-                "o_pre_anc", "o_chunk_off", "o_chunk_stack")
+                "o_dfs", "o_dfs_pos", "n_chunks", "o_pre_row", "o_pre_depth",
+                "o_pre_ci", "o_chunk_off", "o_chunk_stack")
 
 
 class lumo_plan(ctypes.Structure):
@@ -62,7 +62,7 @@ class lumo_tree_desc(ctypes.Structure):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2609_23900_amd.build` "
+        raise ImportError(f"{LIB_PATH} is not built: run `python paper_2609_23900_amd/build.py` "
                           "(hipcc, gfx950); there is no fallback implementation")
     L = ctypes.CDLL(LIB_PATH)
     P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t

@@ -81,7 +81,6 @@ extern "C" const char* lumo_version(void) { return "lumo_tree 0.1 gfx950"; }
 
 extern "C" size_t lumo_tree_gdn_workspace_bytes(const lumo_gdn_dims* d, const lumo_plan* p) {
     if (!d || !p) return 0;
-    if (p->policy == LUMO_POLICY_WY) return wy_workspace_bytes(*d, *p);
     if (p->policy != LUMO_POLICY_PATHS && p->policy != LUMO_POLICY_TWO_LEVEL) return 0;
     return (size_t)p->n_cuts * d->n_layers * d->h_v * d->d_k * d->d_v * sizeof(float);
 }

@@ -5,8 +5,9 @@
 //   2. replay kernel  one wavefront per (request, layer, value head, value tile):
 //                     load the pre-tree state tile, apply the recorded updates of the
 //                     path with the same row update the verifier uses, store in place;
-//                     the path's rows and value entries are fetched before the loop,
-//                     the wave-uniform key rows are read with scalar loads
+//                     before the loop the path's first key rows are copied to LDS
+//                     (direct global-to-LDS loads, in flight with the state load) and
+//                     its rows, decays, betas and value entries are fetched into lanes
 //   3. history kernel conv history <- last three of (history, x rows of the path)
 // Empty or invalid paths leave the state and the history untouched.
 #include "device_common.h"
@@ -56,21 +57,97 @@ struct ReplayParams {
     int32_t max_path, n_layers, total_rows, h_k, h_v, d_v, group, n_vtiles;
 };
 
-// Path entries whose row and value are prefetched before the update loop.
+// Path entries whose key row, row, decay, beta and value are fetched before the loop.
 constexpr int kPrefetch = 16;
 
-// One replayed update (the verifier's row update) for path entry e.
+template <int DK, int OPT> struct KeyRows {
+    using T = typename Op<OPT>::T;
+    static constexpr int kSeg = DK * (int)sizeof(T) / 16;                  // 16-byte segments per row
+    static constexpr int kSlots = (kPrefetch * kSeg + 63) / 64 * 64;      // whole wave copies
+};
+
+// One 16-byte segment of a key row as floats (4 fp32 or 8 bf16 values).
+template <int OPT> __device__ __forceinline__ void unpack_seg(const uint4 w, float (&f)[16 / (OPT ? 2 : 4)]);
+template <> __device__ __forceinline__ void unpack_seg<0>(const uint4 w, float (&f)[4]) {
+    f[0] = __uint_as_float(w.x); f[1] = __uint_as_float(w.y); f[2] = __uint_as_float(w.z); f[3] = __uint_as_float(w.w);
+}
+template <> __device__ __forceinline__ void unpack_seg<1>(const uint4 w, float (&f)[8]) {
+    f[0] = bf16_lo(w.x); f[1] = bf16_hi(w.x); f[2] = bf16_lo(w.y); f[3] = bf16_hi(w.y);
+    f[4] = bf16_lo(w.z); f[5] = bf16_hi(w.z); f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
+}
+
+// The verifier's row update (gdn_row_update: same operations in the same order, so
+// the result is bitwise identical) with the key row read from LDS, 32 elements at a
+// time (the compiler barrier keeps it from hoisting the whole row into registers).
 template <int DK, int OPT>
-__device__ __forceinline__ void replay_step(float (&S)[DK], const typename Op<OPT>::T* __restrict__ k,
-                                            const float* __restrict__ g, const float* __restrict__ beta,
-                                            const ReplayParams& p, int l, int h, int hk, int row, float vj) {
-    const long gi = ((long)l * p.total_rows + row) * p.h_v + h;
-    const long ki = (((long)l * p.total_rows + row) * p.h_k + hk) * DK;
-    gdn_row_update<DK, OPT>(S, k + ki, vj, __expf(g[gi]), beta[gi]);
+__device__ __forceinline__ void row_update_lds(float (&S)[DK], const uint4* kr, float vj, float alpha, float beta) {
+    constexpr int E = 16 / (int)sizeof(typename Op<OPT>::T);  // elements per 16-byte segment
+    constexpr int C = DK < 32 ? DK : 32;
+    float u = 0.f;
+#pragma unroll
+    for (int c0 = 0; c0 < DK; c0 += C) {
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int c = c0; c < c0 + C; c += E) {
+            float kf[E];
+            unpack_seg<OPT>(kr[c / E], kf);
+#pragma unroll
+            for (int i = 0; i < E; ++i) u = __builtin_fmaf(S[c + i], kf[i], u);
+        }
+    }
+    const float delta = beta * __builtin_fmaf(-alpha, u, vj);
+#pragma unroll
+    for (int c0 = 0; c0 < DK; c0 += C) {
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int c = c0; c < c0 + C; c += E) {
+            float kf[E];
+            unpack_seg<OPT>(kr[c / E], kf);
+#pragma unroll
+            for (int i = 0; i < E; ++i) S[c + i] = __builtin_fmaf(delta, kf[i], alpha * S[c + i]);
+        }
+    }
+}
+
+// Entries e0 .. e0 + kPrefetch - 1 of the path: lane e receives entry e0 + e's decay
+// and beta; its key row and the tile's 64 values go to LDS (direct global-to-LDS
+// copies). Lanes and slots past the path repeat its last entry.
+template <int DK, int OPT>
+__device__ __forceinline__ void replay_stage(const ReplayParams& p, const typename Op<OPT>::T* __restrict__ k,
+                                             const typename Op<OPT>::T* __restrict__ v, const float* __restrict__ g,
+                                             const float* __restrict__ beta, const int32_t* path, int base, int len,
+                                             int e0, int l, int h, int hk, int vt, int lane, uint4* krows,
+                                             uint4* vrows, float& apre, float& bpre) {
+    using T = typename Op<OPT>::T;
+    using KR = KeyRows<DK, OPT>;
+    constexpr int E = 16 / (int)sizeof(T);
+    constexpr int kVSeg = 64 / E;
+    const int ne = min(len - e0, kPrefetch);
+    const int prow = p.blob[p.o_row + base + path[e0 + min(lane, ne - 1)]];
+    const long gl = ((long)l * p.total_rows + prow) * p.h_v + h;
+    apre = __expf(g[gl]);
+    bpre = beta[gl];
+#pragma unroll
+    for (int i = 0; i < KR::kSlots / 64; ++i) {
+        const int sl = 64 * i + lane;
+        const int re = __shfl(prow, min(sl / KR::kSeg, ne - 1));
+        const T* kr = k + (((long)l * p.total_rows + re) * p.h_k + hk) * DK;
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint4*>(kr) + sl % KR::kSeg,
+                                         (__attribute__((address_space(3))) void*)&krows[64 * i], 16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < kPrefetch * kVSeg / 64; ++i) {
+        const int sl = 64 * i + lane;
+        const int re = __shfl(prow, min(sl / kVSeg, ne - 1));
+        const int c = min(vt * 64 + (sl % kVSeg) * E, p.d_v - E);  // columns past d_v: any valid segment
+        const T* vr = v + (((long)l * p.total_rows + re) * p.h_v + h) * p.d_v + c;
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint4*>(vr),
+                                         (__attribute__((address_space(3))) void*)&vrows[64 * i], 16, 0, 0);
+    }
 }
 
 template <int DK, int OPT>
-__global__ __launch_bounds__(64) void replay_kernel(ReplayParams p, const typename Op<OPT>::T* __restrict__ k,
+__global__ __launch_bounds__(64, 3) void replay_kernel(ReplayParams p, const typename Op<OPT>::T* __restrict__ k,
                                                    const typename Op<OPT>::T* __restrict__ v,
                                                    const float* __restrict__ g, const float* __restrict__ beta,
                                                    float* __restrict__ state, const int32_t* __restrict__ path_out,
@@ -82,6 +159,13 @@ __global__ __launch_bounds__(64) void replay_kernel(ReplayParams p, const typena
     t /= p.h_v;
     const int l = t % p.n_layers;
     const int r = t / p.n_layers;
+    using T = typename Op<OPT>::T;
+    using KR = KeyRows<DK, OPT>;
+    constexpr int E = 16 / (int)sizeof(T);          // elements per 16-byte segment
+    constexpr int kVSeg = 64 / E;                   // segments of one entry's 64 values
+    constexpr int kVSlots = kPrefetch * kVSeg;      // 128 or 256: whole wave copies
+    __shared__ uint4 krows[KR::kSlots];
+    __shared__ uint4 vrows[kVSlots];
     const int len = path_len[r];
     if (len <= 0) return;
     const int lane = (int)threadIdx.x;
@@ -93,28 +177,26 @@ __global__ __launch_bounds__(64) void replay_kernel(ReplayParams p, const typena
     const long mat = (long)DK * p.d_v;
     float* st = state + (((long)r * p.n_layers + l) * p.h_v + h) * mat;
     const int32_t* path = path_out + (long)r * p.max_path;
-    // row of path entry `lane` (lanes past the path read the root's row)
-    const int prow = p.blob[p.o_row + base + path[lane < len ? lane : 0]];
-    float vpre[kPrefetch];
-#pragma unroll
-    for (int e = 0; e < kPrefetch; ++e) {
-        const int re = __builtin_amdgcn_readlane(prow, e);  // wave-uniform row
-        vpre[e] = Op<OPT>::ld(v, (((long)l * p.total_rows + re) * p.h_v + h) * p.d_v + jc);
-    }
+    float apre, bpre;
+    replay_stage<DK, OPT>(p, k, v, g, beta, path, base, len, 0, l, h, hk, vt, lane, krows, vrows, apre, bpre);
     float S[DK];
 #pragma unroll
-    for (int i = 0; i < DK; ++i) S[i] = st[(long)i * p.d_v + jc];
-    for (int e = 0; e < len; ++e) {
-        const int re = e < 64 ? __builtin_amdgcn_readlane(prow, e) : p.blob[p.o_row + base + path[e]];
-        const float vj = e < kPrefetch ? vpre[0]
-                                       : Op<OPT>::ld(v, (((long)l * p.total_rows + re) * p.h_v + h) * p.d_v + jc);
-        replay_step<DK, OPT>(S, k, g, beta, p, l, h, hk, re, vj);
-#pragma unroll
-        for (int i = 0; i + 1 < kPrefetch; ++i) vpre[i] = vpre[i + 1];  // next entry's value to slot 0
+    for (int i = 0; i < DK; ++i) S[i] = (st + (long)i * p.d_v)[jc];  // uniform row base + lane offset
+    const T* vl = reinterpret_cast<const T*>(vrows);
+    for (int e0 = 0; e0 < len; e0 += kPrefetch) {
+        if (e0 > 0)  // paths longer than kPrefetch: the previous block has been consumed
+            replay_stage<DK, OPT>(p, k, v, g, beta, path, base, len, e0, l, h, hk, vt, lane, krows, vrows, apre, bpre);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the staged rows have landed in LDS
+        const int ne = min(len - e0, kPrefetch);
+        for (int e = 0; e < ne; ++e) {
+            const float ae = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(apre), e));
+            const float be = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bpre), e));
+            row_update_lds<DK, OPT>(S, krows + e * KR::kSeg, Op<OPT>::ld(vl, e * 64 + lane), ae, be);
+        }
     }
     if (act) {
 #pragma unroll
-        for (int i = 0; i < DK; ++i) st[(long)i * p.d_v + j] = S[i];
+        for (int i = 0; i < DK; ++i) (st + (long)i * p.d_v)[j] = S[i];
     }
 }
 

@@ -16,5 +16,6 @@ constexpr int kSegWords = 4;      // {request, source cut, first entry, length}
 constexpr int kSegNodeWords = 3;  // {absolute row, writes output, cut to export}
 constexpr int kPreChunk = 32;     // preorder positions per chunk
 constexpr int kPreStack = 16;     // path-stack candidate slots per chunk
+constexpr int kPreCiWords = 4;    // candidate-slot words per preorder position (16 bytes)
 
 }  // namespace lumo

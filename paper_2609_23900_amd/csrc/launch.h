@@ -23,10 +23,8 @@ struct GdnArgs {
 // Sequential path scans (PATHS / TWO_LEVEL / RECOMPUTE): one launch per dependency level.
 hipError_t launch_scan(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s);
 
-// Tree WY form on MFMA: coefficient kernel + main kernel. The workspace holds the
-// per-(instance, node) coefficient records.
+// Tree WY form on MFMA: one launch, no workspace.
 hipError_t launch_wy(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s);
-size_t wy_workspace_bytes(const lumo_gdn_dims& d, const lumo_plan& pl);
 constexpr int kWyMaxDepth = 17;  // nodes on a root-to-leaf path
 
 struct CommitArgs {

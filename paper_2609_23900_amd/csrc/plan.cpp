@@ -270,11 +270,10 @@ extern "C" lumo_status lumo_tree_plan(int32_t n_req, const int32_t* node_off, co
     p.o_seg_nodes = take((int64_t)lumo::kSegNodeWords * p.n_seg_nodes);
     p.o_dfs = take(N);
     p.o_dfs_pos = take(N);
-    p.n_anc = std::max(1, p.max_depth - 1);
     for (int r = 0; r < n_req; ++r) p.n_chunks += (tr[r].n + lumo::kPreChunk - 1) / lumo::kPreChunk;
     p.o_pre_row = take(N);
     p.o_pre_depth = take(N);
-    p.o_pre_anc = take(2 * N * (int64_t)p.n_anc);
+    p.o_pre_ci = take((int64_t)lumo::kPreCiWords * N);
     p.o_chunk_off = take(n_req + 1);
     p.o_chunk_stack = take((int64_t)lumo::kPreStack * p.n_chunks);
     if (w > (int64_t(1) << 30)) return lumo::fail(LUMO_ESHAPE, "lumo_tree_plan: plan too large");
@@ -322,8 +321,8 @@ extern "C" lumo_status lumo_tree_plan(int32_t n_req, const int32_t* node_off, co
     }
     b[p.o_path_off + n_req] = np;
     b[p.o_spine_off + n_req] = ns;
-    // preorder tables: per position the node's row and depth, and every ancestor's
-    // row with its Gram candidate slot in the position's chunk of kPreChunk
+    // preorder tables: per position the node's row and depth, and the Gram candidate
+    // slot of every ancestor in the position's chunk of kPreChunk (one byte per depth)
     int nc = 0;
     for (int r = 0; r < n_req; ++r) {
         const ReqTree& t = tr[r];
@@ -337,17 +336,16 @@ extern "C" lumo_status lumo_tree_plan(int32_t n_req, const int32_t* node_off, co
             b[p.o_pre_depth + base + pos] = t.depth[x];
             anc.assign(t.depth[x], 0);
             for (int y = t.parent[x], m = t.depth[x] - 1; y >= 0; y = t.parent[y], --m) anc[m] = y;
-            int32_t* pa = b + p.o_pre_anc + 2 * (int64_t)(base + pos) * p.n_anc;
-            for (int m = 0; m < p.n_anc; ++m) {
+            uint32_t ci[lumo::kPreCiWords] = {};
+            for (int m = 0; m < 4 * lumo::kPreCiWords; ++m) {
+                uint32_t slot = 0xffu;  // no ancestor at this depth (or deeper than the table)
                 if (m < t.depth[x]) {
                     const int ap = t.dfs_pos[anc[m]];
-                    pa[2 * m] = ap >= c0 ? lumo::kPreStack + (ap - c0) : m;
-                    pa[2 * m + 1] = row_base[r] + t.slot[anc[m]];
-                } else {
-                    pa[2 * m] = -1;
-                    pa[2 * m + 1] = -1;
+                    slot = ap >= c0 ? (uint32_t)(lumo::kPreStack + (ap - c0)) : (uint32_t)m;
                 }
+                ci[m / 4] |= slot << (8 * (m % 4));
             }
+            for (int w = 0; w < lumo::kPreCiWords; ++w) b[p.o_pre_ci + (int64_t)lumo::kPreCiWords * (base + pos) + w] = (int32_t)ci[w];
             if (pos == c0) {  // chunk start: the path stack is the first node's ancestry
                 int32_t* cs = b + p.o_chunk_stack + (int64_t)lumo::kPreStack * nc;
                 for (int m = 0; m < lumo::kPreStack; ++m)

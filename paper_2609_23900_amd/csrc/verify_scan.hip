@@ -34,7 +34,6 @@ __global__ __launch_bounds__(64) void scan_kernel(ScanParams p, const typename O
                                                   const float* __restrict__ state0,
                                                   typename Op<OPT>::T* __restrict__ o,
                                                   float* __restrict__ node_states, float* __restrict__ ws) {
-    using T = typename Op<OPT>::T;
     int t = xcd_remap(blockIdx.x, gridDim.x);
     const int vt = t % p.n_vtiles;
     t /= p.n_vtiles;

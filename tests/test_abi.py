@@ -175,9 +175,9 @@ def test_wy_rejects_paths_longer_than_17():
     assert "17" in L.lumo_last_error()
 
 
-def test_wy_workspace_size():
+def test_wy_needs_no_workspace():
     par = trees.FIG1_PARENT
     plan, blob = L.lumo_tree_plan(np.array([0, 7], np.int32), par, np.array([7], np.int32),
                                   L.LUMO_POLICY_WY)
     d = _dims(h_k=2, h_v=4, d_k=128, d_v=128, op_dtype=1, n_layers=3)
-    assert L.lumo_tree_gdn_workspace_bytes(d, plan) == 7 * 3 * 4 * (8 + 2 * 8) * 4
+    assert L.lumo_tree_gdn_workspace_bytes(d, plan) == 0

@@ -74,8 +74,7 @@ def _check_against_oracle(parents, n_rows, node_off, policy):
                 assert cp == sorted(cp)
     # preorder tables used by the WY kernels (meaningful for paths of <= 17 nodes)
     if plan.max_depth <= 17:
-        A = plan.n_anc
-        pre_anc = sec("pre_anc", 2 * N * A).reshape(N, A, 2)
+        pre_ci = sec("pre_ci", 4 * N).astype(np.uint32).view(np.uint8).reshape(N, 16)
         chunk_off = sec("chunk_off", len(parents) + 1)
         stacks = sec("chunk_stack", 16 * plan.n_chunks).reshape(-1, 16)
         for r, par in enumerate(parents):
@@ -89,13 +88,13 @@ def _check_against_oracle(parents, n_rows, node_off, policy):
                 assert sec("pre_depth", N)[b + pos] == dep[x]
                 anc = oplan.ancestry(par, x)[:-1]
                 c0 = pos - pos % 32
-                for m in range(A):
+                for m in range(16):
                     if m < len(anc):
                         ap = dfs.index(anc[m])
                         want = 16 + ap - c0 if ap >= c0 else m
-                        assert tuple(pre_anc[b + pos, m]) == (want, rows[anc[m]])
                     else:
-                        assert tuple(pre_anc[b + pos, m]) == (-1, -1)
+                        want = 0xFF
+                    assert pre_ci[b + pos, m] == want
                 if pos == c0:
                     st = stacks[chunk_off[r] + pos // 32]
                     fanc = oplan.ancestry(par, x)[:-1]
