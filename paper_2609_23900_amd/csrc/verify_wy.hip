@@ -41,6 +41,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kD = 128;                // d_k = d_v
@@ -144,13 +145,15 @@ __global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* 
 #pragma unroll
         for (int w = 0; w < D / 4; ++w) li.ci[w] = pci[(long)kPreCiWords * pos + w];
         li.g = gmat[(krow0 + row) * p.h_v + h];
-        li.b = bmat[(krow0 + prow[pos]) * p.h_v + h];
+        li.b = bmat[(krow0 + __shfl(row, t)) * p.h_v + h];  // node t's row sits on lane t
     };
     // block-shared tile rows of the chunk whose lane rows are `row`
     auto tile_issue = [&](int row) {
+        int tl = tid;
+        asm volatile("" : "+v"(tl));  // recomputed per call rather than kept live across the loop
 #pragma unroll
         for (int j = 0; j < kTileRows * 16 / nthr; ++j) {
-            const int gi = j * nthr + tid;
+            const int gi = j * nthr + tl;
             const int nr = gi >> 4;
             const int kb = (gi & 15) ^ (nr & 15);
             const int src = __shfl(row, nr < 2 * kTile ? nr % kTile : kTile + nr - 2 * kTile);
@@ -161,9 +164,11 @@ __global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* 
     };
     // the wave's value rows: slot q = 64 i + lane holds node q / 8, columns j0 + 8 (q % 8) .. + 7
     auto v_issue = [&](int row, uint4* dst) {
+        int ln = lane;
+        asm volatile("" : "+v"(ln));  // recomputed per call rather than kept live across the loop
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int q = 64 * i + lane;
+            const int q = 64 * i + ln;
             const int rn = __shfl(row, q >> 3);
             __builtin_amdgcn_global_load_lds(vmat + ((krow0 + rn) * p.h_v + h) * kD + j0 + 8 * (q & 7),
                                              (lds_void*)&dst[64 * i], 16, 0, 0);
@@ -177,27 +182,28 @@ __global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* 
     lane_info(0, rowC, info);
     int rowA = N > kTile ? lane_row(kTile) : rowC;  // next chunk
 
-    // R0 columns j0 + 32 ct + lane%32 as MFMA B fragments: keys 16 s + 8 (lane/32) + e.
+    // R0 columns j0 + 16 ct + lane%16 (ct = 0..3) as B fragments of the 16x16x32 MFMA:
+    // key block kb holds keys 32 kb + 8 (lane/16) + e.
     const float* S = state0 + (((long)r * p.n_layers + l) * p.h_v + h) * (long)(kD * kD);
-    const float* Sl = S + (long)(8 * (lane / kTile)) * kD + j0 + t;
-    bf16x8 bhi[2][kD / 16], blo[2][kD / 16];
+    const float* Sl = S + (long)(8 * (lane / 16)) * kD + j0 + lane % 16;
+    bf16x8 bhi[4][kD / 32], blo[4][kD / 32];
     // Each fp32 value x is held as hi + lo: hi = x truncated to bf16, lo = the exact
     // remainder x - hi rounded to nearest bf16 (|x - hi - lo| <= 2^-15 |x|).
 #pragma unroll
-    for (int ct = 0; ct < 2; ++ct)
+    for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
-        for (int s = 0; s < kD / 16; ++s) {
+        for (int kb = 0; kb < kD / 32; ++kb) {
             uint32_t hw[4], lw[4];
 #pragma unroll
             for (int e2 = 0; e2 < 4; ++e2) {
-                const uint32_t x0 = __float_as_uint(Sl[(long)(16 * s + 2 * e2) * kD + kTile * ct]);
-                const uint32_t x1 = __float_as_uint(Sl[(long)(16 * s + 2 * e2 + 1) * kD + kTile * ct]);
+                const uint32_t x0 = __float_as_uint(Sl[(long)(32 * kb + 2 * e2) * kD + 16 * ct]);
+                const uint32_t x1 = __float_as_uint(Sl[(long)(32 * kb + 2 * e2 + 1) * kD + 16 * ct]);
                 hw[e2] = __builtin_amdgcn_perm(x1, x0, 0x07060302u);  // {hi(x1), hi(x0)}: upper halves
                 lw[e2] = f32x2_to_bf16x2(__uint_as_float(x0) - __uint_as_float(x0 & 0xffff0000u),
                                          __uint_as_float(x1) - __uint_as_float(x1 & 0xffff0000u));
             }
-            bhi[ct][s] = __builtin_bit_cast(bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
-            blo[ct][s] = __builtin_bit_cast(bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
+            bhi[ct][kb] = __builtin_bit_cast(bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
+            blo[ct][kb] = __builtin_bit_cast(bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
         }
 
     // delta of the current path by depth; slot D takes the writes of nodes at depth D,
@@ -206,75 +212,105 @@ __global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* 
 #pragma unroll
     for (int m = 0; m <= D; ++m) dst[m] = 0.f;
     const int vcol = j0 + lane;
-    const int kb0 = lane / kTile;  // key block offset within a 16-key step
+    const int kb0 = lane / kTile;  // key block offset within a 16-key step (32x32x16 Gram)
     // Gram tiles of this wave: rows = chunk keys (mt 0, Gram rows 16..47) or path-stack
     // keys (mt 1, Gram rows 0..15); columns = the chunk's keys (nt 0) or queries (nt 1)
     constexpr int NT = NVH == 2 ? 1 : 2;
     const int mt = NVH == 2 ? (wave >> 1) : wave;
     const int arow = mt == 0 ? t : 2 * kTile + (t & (kStack - 1));
 
+    // R0 [k | q] of the 16 nodes of half hf of the chunk against the wave's 64 columns,
+    // then the 4 x 4 exchange of lane groups (permlane32, then permlane16 swaps) that
+    // leaves lane l with column j0 + l: pk[b][i], pq[b][i] belong to node 16 hf + 4 b + i.
+    auto half_products = [&](int hf, f32x4 (&pk)[4], f32x4 (&pq)[4]) {
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                pk[ct][i] = 0.f;
+                pq[ct][i] = 0.f;
+            }
+        const int nrow = 16 * hf + lane % 16;  // A rows: the half's nodes
+#pragma unroll
+        for (int kb = 0; kb < kD / 32; ++kb) {
+            const int sw = (4 * kb + lane / 16) ^ (nrow & 15);
+            const bf16x8 fk = as_bf16x8(tile.slot[nrow * 16 + sw]);
+            const bf16x8 fq = as_bf16x8(tile.slot[(kTile + nrow) * 16 + sw]);
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct) {
+                pk[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fk, bhi[ct][kb], pk[ct], 0, 0, 0);
+                pk[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fk, blo[ct][kb], pk[ct], 0, 0, 0);
+                pq[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fq, bhi[ct][kb], pq[ct], 0, 0, 0);
+                pq[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fq, blo[ct][kb], pq[ct], 0, 0, 0);
+            }
+        }
+    };
+    // Lane group g holds tile ct as nodes 4 g + i of columns 16 ct + lane%16; after the
+    // exchange lane group g holds, in block b, nodes 4 b + i of columns 16 g + lane%16.
+    auto exchange = [&](f32x4 (&x)[4]) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[c][i]), __float_as_uint(x[c + 2][i]),
+                                                                 false, false);
+                x[c][i] = __uint_as_float(sw[0]);
+                x[c + 2][i] = __uint_as_float(sw[1]);
+            }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int c = 0; c < 4; c += 2) {
+                const auto sw = __builtin_amdgcn_permlane16_swap(__float_as_uint(x[c][i]), __float_as_uint(x[c + 1][i]),
+                                                                 false, false);
+                x[c][i] = __uint_as_float(sw[0]);
+                x[c + 1][i] = __uint_as_float(sw[1]);
+            }
+    };
+
     for (int c0 = 0, buf = 0; c0 < N; c0 += kTile, buf ^= 1) {
         const bool more = c0 + kTile < N;
+        const bool two = c0 + kTile / 2 < N;  // the second half holds real nodes
         // this chunk's tile, value rows and lane view have landed for every wave
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
         if (more) v_issue(rowA, wl.v[buf ^ 1]);
 
         // ---- Gram (head-independent) into LDS
-        f32x16 gacc[NT];
+        {
+            f32x16 gacc[NT];
 #pragma unroll
-        for (int i = 0; i < NT; ++i)
+            for (int i = 0; i < NT; ++i)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) gacc[i][e] = 0.f;
+                for (int e = 0; e < 16; ++e) gacc[i][e] = 0.f;
 #pragma unroll
-        for (int s = 0; s < kD / 16; ++s) {
-            const int sw = (2 * s + kb0) ^ (t & 15);
-            const bf16x8 fa = as_bf16x8(tile.slot[arow * 16 + sw]);
+            for (int s = 0; s < kD / 16; ++s) {
+                const int sw = (2 * s + kb0) ^ (t & 15);
+                const bf16x8 fa = as_bf16x8(tile.slot[arow * 16 + sw]);
+#pragma unroll
+                for (int i = 0; i < NT; ++i) {
+                    const int nt = NVH == 2 ? (wave & 1) : i;
+                    const bf16x8 fb = as_bf16x8(tile.slot[(nt * kTile + t) * 16 + sw]);
+                    gacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, gacc[i], 0, 0, 0);
+                }
+            }
+            // MFMA 32x32 output: lane holds column lane%32, rows 8(e/4) + 4(lane/32) + e%4
 #pragma unroll
             for (int i = 0; i < NT; ++i) {
                 const int nt = NVH == 2 ? (wave & 1) : i;
-                const bf16x8 fb = as_bf16x8(tile.slot[(nt * kTile + t) * 16 + sw]);
-                gacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, gacc[i], 0, 0, 0);
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int row = 8 * (e / 4) + 4 * (lane / kTile) + e % 4;
+                    if (mt == 0)
+                        G[(kStack + row) * kGS + nt * kTile + t] = gacc[i][e];
+                    else if (e < 8)  // rows 0..15: the stack slots
+                        G[row * kGS + nt * kTile + t] = gacc[i][e];
+                }
             }
         }
-        // MFMA 32x32 output: lane holds column lane%32, rows 8(e/4) + 4(lane/32) + e%4
-#pragma unroll
-        for (int i = 0; i < NT; ++i) {
-            const int nt = NVH == 2 ? (wave & 1) : i;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int row = 8 * (e / 4) + 4 * (lane / kTile) + e % 4;
-                if (mt == 0)
-                    G[(kStack + row) * kGS + nt * kTile + t] = gacc[i][e];
-                else if (e < 8)  // rows 0..15: the stack slots
-                    G[row * kGS + nt * kTile + t] = gacc[i][e];
-            }
-        }
-
-        // ---- R0 [K | Q] for the chunk's 32 nodes against the wave's 64 columns
-        f32x16 ak[2], aq[2];
-#pragma unroll
-        for (int ct = 0; ct < 2; ++ct)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                ak[ct][e] = 0.f;
-                aq[ct][e] = 0.f;
-            }
-#pragma unroll
-        for (int s = 0; s < kD / 16; ++s) {
-            const int sw = (2 * s + kb0) ^ (t & 15);
-            const bf16x8 fk = as_bf16x8(tile.slot[t * 16 + sw]);
-            const bf16x8 fq = as_bf16x8(tile.slot[(kTile + t) * 16 + sw]);
-#pragma unroll
-            for (int ct = 0; ct < 2; ++ct) {
-                ak[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fk, bhi[ct][s], ak[ct], 0, 0, 0);
-                ak[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fk, blo[ct][s], ak[ct], 0, 0, 0);
-                aq[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fq, bhi[ct][s], aq[ct], 0, 0, 0);
-                aq[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fq, blo[ct][s], aq[ct], 0, 0, 0);
-            }
-        }
-        __syncthreads();  // the Gram is complete and every wave has read the tile
-        if (more) tile_issue(rowA);
+        f32x4 pk[4], pq[4];
+        half_products(0, pk, pq);
+        __syncthreads();  // the Gram is complete
 
         // ---- coefficient records of the wave's head (lanes 0..31: A, lanes 32..63: B)
         if (lane < kTile + kStack) wl.alpha[lane < kTile ? kStack + lane : lane - kTile] = __expf(info.g);
@@ -310,45 +346,44 @@ __global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* 
             if (c0 + 2 * kTile < N) rowB = lane_row(c0 + 2 * kTile);
         }
 
-        // Lane l holds column 32 ct + l%32 of tile ct for nodes 8(e/4) + 4(l/32) + e%4.
-        // Swapping tile 0's upper half-wave with tile 1's lower half-wave leaves every
-        // lane with one column (j0 + lane): [0][e] = node 8(e/4) + e%4, [1][e] = node 8(e/4) + 4 + e%4.
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const auto sk = __builtin_amdgcn_permlane32_swap(__float_as_uint(ak[0][e]), __float_as_uint(ak[1][e]), false, false);
-            ak[0][e] = __uint_as_float(sk[0]);
-            ak[1][e] = __uint_as_float(sk[1]);
-            const auto sq = __builtin_amdgcn_permlane32_swap(__float_as_uint(aq[0][e]), __float_as_uint(aq[1][e]), false, false);
-            aq[0][e] = __uint_as_float(sq[0]);
-            aq[1][e] = __uint_as_float(sq[1]);
-        }
         const float* rec = wl.rec;
         const uint16_t* vs = reinterpret_cast<const uint16_t*>(wl.v[buf]);
-        // Straight-line over all 32 slots: slots past the chunk's end hold exact copies of
-        // its last node (tile rows, value row, record), so they recompute that node's
-        // delta and output bit for bit and store the same value to the same place.
+        // Straight-line over the 16 slots of a half: slots past the chunk's end hold exact
+        // copies of its last node (tile rows, value row, record), so they recompute that
+        // node's delta and output bit for bit and store the same value to the same place.
+        auto recursion = [&](int hf, const f32x4 (&pk)[4], const f32x4 (&pq)[4]) {
 #pragma unroll
-        for (int n = 0; n < kTile; ++n) {
-            const int e = 4 * (n / 8) + n % 4;
-            const float pk = ((n / 4) & 1) ? ak[1][e] : ak[0][e];
-            const float pq = ((n / 4) & 1) ? aq[1][e] : aq[0][e];
-            const float* cf = rec + n * W;
-            const int rn = __builtin_amdgcn_readfirstlane(__float_as_int(cf[0]));  // uniform
-            const int d = __builtin_amdgcn_readfirstlane(__float_as_int(cf[1]));
-            const float bn = cf[2], gm = cf[3], cn = cf[4];
-            const float vj = __uint_as_float(((uint32_t)vs[n * 64 + lane]) << 16);
-            float sa = 0.f, sb = 0.f;
+            for (int i = 0; i < 16; ++i) {
+                const int n = 16 * hf + i;
+                const float* cf = rec + n * W;
+                const int rn = __builtin_amdgcn_readfirstlane(__float_as_int(cf[0]));  // uniform
+                const int d = __builtin_amdgcn_readfirstlane(__float_as_int(cf[1]));
+                const float bn = cf[2], gm = cf[3], cn = cf[4];
+                const float vj = __uint_as_float(((uint32_t)vs[n * 64 + lane]) << 16);
+                float sa = 0.f, sb = 0.f;
 #pragma unroll
-            for (int m = 0; m < D; ++m) {
-                sa = __builtin_fmaf(cf[8 + m], dst[m], sa);
-                sb = __builtin_fmaf(cf[8 + D + m], dst[m], sb);
+                for (int m = 0; m < D; ++m) {
+                    sa = __builtin_fmaf(cf[8 + m], dst[m], sa);
+                    sb = __builtin_fmaf(cf[8 + D + m], dst[m], sb);
+                }
+                const float u = __builtin_fmaf(-gm, pk[i / 4][i % 4], vj);  // v - gamma R0 k
+                const float delta = __builtin_fmaf(bn, u, -sa);              // beta u - sum A delta
+                const float ov = __builtin_fmaf(cn, delta, __builtin_fmaf(gm, pq[i / 4][i % 4], sb));
+                dst[d < D ? d : D] = delta;  // uniform index: an indexed register write
+                uint16_t* orow = out + ((krow0 + rn) * p.h_v + h) * kD;
+                orow[vcol] = f32_to_bf16(ov);
             }
-            const float u = __builtin_fmaf(-gm, pk, vj);           // v - gamma R0 k
-            const float delta = __builtin_fmaf(bn, u, -sa);        // beta u - sum A delta
-            const float ov = __builtin_fmaf(cn, delta, __builtin_fmaf(gm, pq, sb));
-            dst[d < D ? d : D] = delta;  // uniform index: an indexed register write
-            uint16_t* orow = out + ((krow0 + rn) * p.h_v + h) * kD;
-            orow[vcol] = f32_to_bf16(ov);
+        };
+        exchange(pk);
+        exchange(pq);
+        recursion(0, pk, pq);
+        if (two) half_products(1, pk, pq);
+        __syncthreads();  // every wave has read the tile: it may be refilled
+        if (more) tile_issue(rowA);
+        if (two) {
+            exchange(pk);
+            exchange(pq);
+            recursion(1, pk, pq);
         }
         rowC = rowA;
         rowA = rowB;
