@@ -351,26 +351,46 @@ __global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* 
         // Straight-line over the 16 slots of a half: slots past the chunk's end hold exact
         // copies of its last node (tile rows, value row, record), so they recompute that
         // node's delta and output bit for bit and store the same value to the same place.
+        // One node's record in registers: {row, depth} as ints, {beta, gamma, k.q}, A, B.
+        struct NodeRec {
+            int rn, d;
+            float bn, gm, cn;
+            float a[D], b[D];
+        };
+        auto load_rec = [&](int n, NodeRec& c) {
+            const float* cf = rec + n * W;
+            c.rn = __builtin_amdgcn_readfirstlane(__float_as_int(cf[0]));  // uniform
+            c.d = __builtin_amdgcn_readfirstlane(__float_as_int(cf[1]));
+            c.bn = cf[2];
+            c.gm = cf[3];
+            c.cn = cf[4];
+#pragma unroll
+            for (int m = 0; m < D; ++m) {
+                c.a[m] = cf[8 + m];
+                c.b[m] = cf[8 + D + m];
+            }
+        };
         auto recursion = [&](int hf, const f32x4 (&pk)[4], const f32x4 (&pq)[4]) {
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const int n = 16 * hf + i;
-                const float* cf = rec + n * W;
-                const int rn = __builtin_amdgcn_readfirstlane(__float_as_int(cf[0]));  // uniform
-                const int d = __builtin_amdgcn_readfirstlane(__float_as_int(cf[1]));
-                const float bn = cf[2], gm = cf[3], cn = cf[4];
+                NodeRec cur;
+                load_rec(n, cur);
                 const float vj = __uint_as_float(((uint32_t)vs[n * 64 + lane]) << 16);
-                float sa = 0.f, sb = 0.f;
+                // sums over the path stack as even/odd partial sums (half the dependent chain)
+                float sa0 = 0.f, sa1 = 0.f, sb0 = 0.f, sb1 = 0.f;
 #pragma unroll
-                for (int m = 0; m < D; ++m) {
-                    sa = __builtin_fmaf(cf[8 + m], dst[m], sa);
-                    sb = __builtin_fmaf(cf[8 + D + m], dst[m], sb);
+                for (int m = 0; m < D; m += 2) {
+                    sa0 = __builtin_fmaf(cur.a[m], dst[m], sa0);
+                    sb0 = __builtin_fmaf(cur.b[m], dst[m], sb0);
+                    sa1 = __builtin_fmaf(cur.a[m + 1], dst[m + 1], sa1);
+                    sb1 = __builtin_fmaf(cur.b[m + 1], dst[m + 1], sb1);
                 }
-                const float u = __builtin_fmaf(-gm, pk[i / 4][i % 4], vj);  // v - gamma R0 k
-                const float delta = __builtin_fmaf(bn, u, -sa);              // beta u - sum A delta
-                const float ov = __builtin_fmaf(cn, delta, __builtin_fmaf(gm, pq[i / 4][i % 4], sb));
-                dst[d < D ? d : D] = delta;  // uniform index: an indexed register write
-                uint16_t* orow = out + ((krow0 + rn) * p.h_v + h) * kD;
+                const float u = __builtin_fmaf(-cur.gm, pk[i / 4][i % 4], vj);  // v - gamma R0 k
+                const float delta = __builtin_fmaf(cur.bn, u, -(sa0 + sa1));     // beta u - sum A delta
+                const float ov = __builtin_fmaf(cur.cn, delta, __builtin_fmaf(cur.gm, pq[i / 4][i % 4], sb0 + sb1));
+                dst[cur.d < D ? cur.d : D] = delta;  // uniform index: an indexed register write
+                uint16_t* orow = out + ((krow0 + cur.rn) * p.h_v + h) * kD;
                 orow[vcol] = f32_to_bf16(ov);
             }
         };
