@@ -10,11 +10,17 @@ heads, each node counted once), the roofline of the dominant kernel (verify) wit
 its duration measured by HIP events on the launch stream, the other kernels'
 durations, and the fp64 CPU oracle timed on a bounded sample of the same workload.
 
-  python bench.py [--steps K] [--warmup W] [--config batched] [--policy paths]
+  python bench.py [--steps K] [--warmup W] [--config batched] [--policy wy]
+  python bench.py --copy-probe     # plain 1 GiB device copy x3 (HBM counter calibration)
+
+The roofline's `traffic` (measured HBM bytes per verify call) is reported from
+profiles/traffic.json only while the verify kernel's sources hash to the value the
+counters were taken with; after any change to them it is null until re-measured.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -26,6 +32,47 @@ sys.path.insert(0, ROOT)
 METRIC = "tree GDN head-node updates/sec + % of HBM/VALU roofline, 1 MI355X"
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, published
 PEAK_VALU_F32_TFS = 157.3      # MI355X fp32 vector, published (256 CU x 2.4 GHz)
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "traffic.json")
+# sources that determine the code of each policy's verify kernels
+VERIFY_SOURCES = {
+    "wy": ["verify_wy.hip", "device_common.h", "internal.h", "launch.h"],
+    "paths": ["verify_scan.hip", "device_common.h", "internal.h", "launch.h"],
+}
+
+
+def verify_source_hash(policy):
+    files = VERIFY_SOURCES.get(policy, VERIFY_SOURCES["paths"])
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2609_23900_amd", "csrc", f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(policy, config):
+    """Measured HBM bytes per verify call, if recorded for exactly these kernel sources."""
+    try:
+        with open(TRAFFIC_RECORD) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    for r in rec.get("records", []):
+        if r.get("policy") == policy and r.get("config") == config and r.get("sources_sha256") == verify_source_hash(policy):
+            return r
+    return None
+
+
+def copy_probe():
+    """A plain device copy of known size (1 GiB read + 1 GiB written, three times)."""
+    import torch
+    n = 256 * 1024 * 1024
+    a = torch.ones(n, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n * 4, "copies": 3}), flush=True)
 
 WORKLOAD_TEXT = {
     "tiny": "Fig. 1 tree, 1 request, 1 head, d=16, fp32 operands",
@@ -112,7 +159,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="batched")
-    ap.add_argument("--policy", default="paths")
+    ap.add_argument("--policy", default="wy")
+    ap.add_argument("--copy-probe", action="store_true", help="only run the counter-calibration copy")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     args = ap.parse_args()
@@ -120,6 +168,10 @@ def main():
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the step shards "
               "by request with no cross-GPU exchange; see the design notes)", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_probe:
+        copy_probe()
+        return
 
     import torch
 
@@ -178,6 +230,11 @@ def main():
         ach = ab["verify_flops"] / (ver_ms * 1e-3) / 1e12
         roof = {"bound": "alu", "achieved": round(ach, 2), "peak": PEAK_VALU_F32_TFS,
                 "unit": "TFLOP/s", "frac": round(ach / PEAK_VALU_F32_TFS, 4), "traffic": None}
+    tr = recorded_traffic(args.policy, args.config)
+    if tr is not None:
+        roof["traffic"] = {"fetch_bytes": tr["fetch_bytes"], "write_bytes": tr["write_bytes"],
+                           "total_bytes": tr["fetch_bytes"] + tr["write_bytes"], "unit": "B per verify call",
+                           "source": "profiles/traffic.json"}
     roof["kernel"] = "verify"
     roof["per_launch"] = (f"{ab['verify_flops'] / 1e9:.2f} GFLOP, {ab['verify_bytes'] / 1e6:.1f} MB "
                           f"algorithmic per verify call")
