@@ -69,23 +69,8 @@ struct KQTile {
     uint4 slot[kTileRows * 16];
 };
 
-// Per-wave LDS: the chunk's coefficient records, value rows (double-buffered: the
-// next chunk's are in flight while this one is used) and the decays of the candidates.
-template <int D>
-struct WaveLds {
-    float rec[kTile * Rec<D>::kWords];
-    uint4 v[2][kTile * 8];  // [node][8 segments of 8 bf16] of the wave's 64 columns
-    float alpha[64];        // exp(g) of candidate c (stack slots, then the chunk's nodes)
-};
-
-template <int D, int NVH>
-constexpr size_t wy_lds_bytes() {
-    return sizeof(KQTile) + sizeof(float) * kCand * kGS + 2 * NVH * sizeof(WaveLds<D>);
-}
-static_assert(sizeof(float) * kCand * kGS % 16 == 0, "keeps the per-wave areas 16-byte aligned");
-
 // Per-lane view of one chunk. Lanes 0..31 and 32..63 both describe node t = lane % 32
-// (depth, candidate slots, beta); g is that of the lane's row (see lane_row).
+// (depth, candidate slots, beta); g is that of the lane's row (see lane_info).
 template <int D>
 struct LaneInfo {
     int dep;
@@ -95,21 +80,28 @@ struct LaneInfo {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
 
+// Two waves per SIMD for D = 8 (79 KB of LDS per 4-wave block); with D = 16 the
+// records make a 4-wave block too large for two per CU, so one wave per SIMD.
 template <int D, int NVH>
-__global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* __restrict__ kmat,
+__global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, const uint16_t* __restrict__ kmat,
                                                     const uint16_t* __restrict__ qmat,
                                                     const uint16_t* __restrict__ vmat, const float* __restrict__ gmat,
                                                     const float* __restrict__ bmat, const float* __restrict__ state0,
                                                     uint16_t* __restrict__ out) {
     constexpr int W = Rec<D>::kWords;
     constexpr int nthr = 128 * NVH;
-    extern __shared__ uint4 lds[];
-    KQTile& tile = *reinterpret_cast<KQTile*>(lds);
-    float* G = reinterpret_cast<float*>(lds + sizeof(KQTile) / 16);
+    // LDS, one object per role: the compiler orders LDS reads after the direct
+    // global-to-LDS copies only where they may touch the same object.
+    __shared__ KQTile tile;                        // block: chunk keys, queries, path-stack keys
+    __shared__ float G[kCand * kGS];               // block: Gram [candidate][chunk key | chunk query]
+    __shared__ float recs[2 * NVH][kTile * W];     // per wave: the chunk's coefficient records
+    __shared__ float alphas[2 * NVH][64];          // per wave: exp(g) of the candidates
+    __shared__ uint4 vbufs[2 * NVH][2][kTile * 8]; // per wave: value rows, double-buffered
     const int tid = (int)threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: head and half in SGPRs
     const int lane = tid & 63;
-    WaveLds<D>& wl = reinterpret_cast<WaveLds<D>*>(G + kCand * kGS)[wave];
+    float* wrec = recs[wave];
+    float* walpha = alphas[wave];
 
     int blk = xcd_remap(blockIdx.x, gridDim.x);
     const int pairs = p.group / NVH;
@@ -131,56 +123,90 @@ __global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* 
     const long krow0 = (long)l * p.total_rows;
     const int t = lane % kTile;  // node of this lane in the chunk views
 
-    // Row of this lane for the chunk at c0: node t's on lanes 0..31, path-stack slot
-    // lane - 32's on lanes 32..47 where that slot is used, node t's otherwise. Positions
-    // past the end repeat the last node, so padding slots are exact copies of it.
-    auto lane_row = [&](int c0) {
-        const int a = prow[min(c0 + t, N - 1)];
-        const int s = stacks[(c0 / kTile) * kStack + (lane & (kStack - 1))];
-        return (lane >= kTile && lane < kTile + kStack && s >= 0) ? s : a;
+    // Rows of the chunk at c0 as seen by this lane: n = node t's (every lane; positions
+    // past the end repeat the last node, so padding slots are exact copies of it) and
+    // s = path-stack slot lane%16's, -1 beyond the first node's depth (clamped to row 0
+    // where used: those Gram rows are never referenced). Both loads are unconditional
+    // and nothing is computed from them until they are used.
+    struct Rows {
+        int n, s;
     };
-    auto lane_info = [&](int c0, int row, LaneInfo<D>& li) {
+    auto lane_rows = [&](int c0) {
+        Rows rw;
+        rw.n = prow[min(c0 + t, N - 1)];
+        rw.s = stacks[(c0 / kTile) * kStack + (lane & (kStack - 1))];
+        return rw;
+    };
+    // g of lane rows (stack slot lane-32's on lanes 32..47, node t's otherwise), node t's
+    // depth, candidate slots and beta
+    auto lane_info = [&](int c0, const Rows& rw, LaneInfo<D>& li) {
         const int pos = min(c0 + t, N - 1);
         li.dep = pdep[pos];
 #pragma unroll
         for (int w = 0; w < D / 4; ++w) li.ci[w] = pci[(long)kPreCiWords * pos + w];
-        li.g = gmat[(krow0 + row) * p.h_v + h];
-        li.b = bmat[(krow0 + __shfl(row, t)) * p.h_v + h];  // node t's row sits on lane t
+        const int grow = (lane >= kTile && lane < kTile + kStack) ? max(rw.s, 0) : rw.n;
+        li.g = gmat[(krow0 + grow) * p.h_v + h];
+        li.b = bmat[(krow0 + rw.n) * p.h_v + h];
     };
-    // block-shared tile rows of the chunk whose lane rows are `row`
-    auto tile_issue = [&](int row) {
-        int tl = tid;
-        asm volatile("" : "+v"(tl));  // recomputed per call rather than kept live across the loop
+    // Block-shared tile rows of the chunk. In round j a wave fills tile rows nr0 .. nr0+3
+    // (16 slots each), so the four source rows are read with readlane: no LDS access,
+    // hence no ordering behind copies still in flight.
+    constexpr int kTileRounds = kTileRows * 16 / nthr;
+    auto tile_issue = [&](const Rows& rw) {
+        int ln = lane;
+        asm volatile("" : "+v"(ln));  // recomputed per call rather than kept live across the loop
 #pragma unroll
-        for (int j = 0; j < kTileRows * 16 / nthr; ++j) {
-            const int gi = j * nthr + tl;
-            const int nr = gi >> 4;
-            const int kb = (gi & 15) ^ (nr & 15);
-            const int src = __shfl(row, nr < 2 * kTile ? nr % kTile : kTile + nr - 2 * kTile);
-            const uint16_t* mat = (nr >= kTile && nr < 2 * kTile) ? qmat : kmat;
+        for (int j = 0; j < kTileRounds; ++j) {
+            const int nr0 = (j * nthr + 64 * wave) >> 4;  // uniform
+            // a round lies wholly in the key/query rows or wholly in the stack rows
+            constexpr int kRoundRows = nthr / 16;
+            static_assert(2 * kTile % kRoundRows == 0, "rounds do not straddle the stack rows");
+            const bool stack_round = j * kRoundRows >= 2 * kTile;  // compile-time per round
+            int rq[4];
+#pragma unroll
+            for (int k4 = 0; k4 < 4; ++k4) {
+                const int nr = nr0 + k4;
+                rq[k4] = stack_round ? max(__builtin_amdgcn_readlane(rw.s, nr - 2 * kTile), 0)
+                                     : __builtin_amdgcn_readlane(rw.n, nr % kTile);
+            }
+            const int g4 = ln >> 4;
+            const int src = g4 == 0 ? rq[0] : g4 == 1 ? rq[1] : g4 == 2 ? rq[2] : rq[3];
+            const int nr = nr0 + g4;
+            const int kb = (ln & 15) ^ (nr & 15);
+            const uint16_t* mat = (!stack_round && nr >= kTile) ? qmat : kmat;
             __builtin_amdgcn_global_load_lds(mat + ((krow0 + src) * p.h_k + hk) * kD + 8 * kb,
                                              (lds_void*)&tile.slot[j * nthr + 64 * wave], 16, 0, 0);
         }
     };
+    // Block barrier after this wave's LDS writes have completed. Unlike __syncthreads it
+    // does not wait for global memory operations (copies into other LDS objects, output
+    // stores) that nothing across the barrier depends on.
+    auto lds_barrier = [&]() {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
     // the wave's value rows: slot q = 64 i + lane holds node q / 8, columns j0 + 8 (q % 8) .. + 7
-    auto v_issue = [&](int row, uint4* dst) {
+    auto v_issue = [&](const Rows& rw, uint4* dst) {
         int ln = lane;
         asm volatile("" : "+v"(ln));  // recomputed per call rather than kept live across the loop
+        int rn[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rn[i] = __shfl(rw.n, (64 * i + ln) >> 3);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int q = 64 * i + ln;
-            const int rn = __shfl(row, q >> 3);
-            __builtin_amdgcn_global_load_lds(vmat + ((krow0 + rn) * p.h_v + h) * kD + j0 + 8 * (q & 7),
+            __builtin_amdgcn_global_load_lds(vmat + ((krow0 + rn[i]) * p.h_v + h) * kD + j0 + 8 * (q & 7),
                                              (lds_void*)&dst[64 * i], 16, 0, 0);
         }
     };
 
-    int rowC = lane_row(0);  // this chunk
+    Rows rowC = lane_rows(0);  // this chunk
+    v_issue(rowC, vbufs[wave][0]);  // (its shuffles precede every copy)
     tile_issue(rowC);
-    v_issue(rowC, wl.v[0]);
     LaneInfo<D> info;
     lane_info(0, rowC, info);
-    int rowA = N > kTile ? lane_row(kTile) : rowC;  // next chunk
+    Rows rowA = N > kTile ? lane_rows(kTile) : rowC;  // next chunk
 
     // R0 columns j0 + 16 ct + lane%16 (ct = 0..3) as B fragments of the 16x16x32 MFMA:
     // key block kb holds keys 32 kb + 8 (lane/16) + e.
@@ -271,10 +297,14 @@ __global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* 
     for (int c0 = 0, buf = 0; c0 < N; c0 += kTile, buf ^= 1) {
         const bool more = c0 + kTile < N;
         const bool two = c0 + kTile / 2 < N;  // the second half holds real nodes
-        // this chunk's tile, value rows and lane view have landed for every wave
+        // This chunk's tile, value rows and lane view have landed for every wave. The empty
+        // asm consumes the lane view here, so that no first use of it later waits on the
+        // copies issued below.
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        if (more) v_issue(rowA, wl.v[buf ^ 1]);
+        asm volatile("" ::"v"(info.dep), "v"(info.g), "v"(info.b), "v"(info.ci[0]), "v"(info.ci[D / 4 - 1]),
+                     "v"(rowC.n), "v"(rowA.n), "v"(rowA.s));
+        lds_barrier();
+        if (more) v_issue(rowA, vbufs[wave][buf ^ 1]);
 
         // ---- Gram (head-independent) into LDS
         {
@@ -310,44 +340,46 @@ __global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* 
         }
         f32x4 pk[4], pq[4];
         half_products(0, pk, pq);
-        __syncthreads();  // the Gram is complete
+        lds_barrier();  // the Gram is complete
 
         // ---- coefficient records of the wave's head (lanes 0..31: A, lanes 32..63: B)
-        if (lane < kTile + kStack) wl.alpha[lane < kTile ? kStack + lane : lane - kTile] = __expf(info.g);
+        if (lane < kTile + kStack) walpha[lane < kTile ? kStack + lane : lane - kTile] = __expf(info.g);
         {
             const bool isB = lane >= kTile;
             const float* Gc = G + (isB ? kTile : 0) + t;
             const float sc = isB ? 1.f : info.b;
-            float gam = wl.alpha[kStack + t];  // Gamma(a_{d-1} -> t) = alpha_t
+            float gam = walpha[kStack + t];  // Gamma(a_{d-1} -> t) = alpha_t
             float cv[D];
 #pragma unroll
             for (int m = D - 1; m >= 0; --m) {
+                // ci is 0 past the depth: the reads stay in bounds and are masked, so they
+                // are issued together instead of one conditional round trip per depth
                 const bool live = m < info.dep;
                 const int ci = live ? (int)((info.ci[m / 4] >> (8 * (m % 4))) & 0xffu) : 0;
-                const float gv = Gc[ci * kGS], av = wl.alpha[ci];  // in bounds either way
-                cv[m] = live ? (sc * gam) * gv : 0.f;
-                gam = live ? gam * av : gam;  // then Gamma(a_{m-1} -> t); finally gamma_t
+                const float gv = Gc[ci * kGS], av = walpha[ci];
+                cv[m] = (sc * gam) * gv * (live ? 1.f : 0.f);
+                gam *= live ? av : 1.f;  // then Gamma(a_{m-1} -> t); finally gamma_t
             }
-            float* rt = wl.rec + t * W;
+            float* rt = wrec + t * W;
 #pragma unroll
             for (int q4 = 0; q4 < D / 4; ++q4)
                 *reinterpret_cast<float4*>(rt + 8 + (isB ? D : 0) + 4 * q4) =
                     make_float4(cv[4 * q4], cv[4 * q4 + 1], cv[4 * q4 + 2], cv[4 * q4 + 3]);
             if (!isB) {
                 *reinterpret_cast<float4*>(rt) =
-                    make_float4(__int_as_float(rowC), __int_as_float(info.dep), info.b, gam);
+                    make_float4(__int_as_float(rowC.n), __int_as_float(info.dep), info.b, gam);
                 *reinterpret_cast<float4*>(rt + 4) = make_float4(G[(kStack + t) * kGS + kTile + t], 0.f, 0.f, 0.f);
             }
         }
         // next chunk's lane view (lands during the recursion)
-        int rowB = rowA;
+        Rows rowB = rowA;
         if (more) {
             lane_info(c0 + kTile, rowA, info);
-            if (c0 + 2 * kTile < N) rowB = lane_row(c0 + 2 * kTile);
+            if (c0 + 2 * kTile < N) rowB = lane_rows(c0 + 2 * kTile);
         }
 
-        const float* rec = wl.rec;
-        const uint16_t* vs = reinterpret_cast<const uint16_t*>(wl.v[buf]);
+        const float* rec = wrec;
+        const uint16_t* vs = reinterpret_cast<const uint16_t*>(vbufs[wave][buf]);
         // Straight-line over the 16 slots of a half: slots past the chunk's end hold exact
         // copies of its last node (tile rows, value row, record), so they recompute that
         // node's delta and output bit for bit and store the same value to the same place.
@@ -398,7 +430,7 @@ __global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* 
         exchange(pq);
         recursion(0, pk, pq);
         if (two) half_products(1, pk, pq);
-        __syncthreads();  // every wave has read the tile: it may be refilled
+        lds_barrier();  // every wave has read the tile: it may be refilled
         if (more) tile_issue(rowA);
         if (two) {
             exchange(pk);
@@ -413,15 +445,7 @@ __global__ __launch_bounds__(256, 2) void wy_kernel(WyParams p, const uint16_t* 
 template <int D, int NVH>
 hipError_t launch_wy_kernel(const lumo_gdn_dims& d, const WyParams& p, const GdnArgs& a, hipStream_t s) {
     const long nb = (long)d.n_req * d.n_layers * d.h_k * (p.group / NVH);
-    constexpr size_t bytes = wy_lds_bytes<D, NVH>();
-    static bool attr_set = false;  // LDS above the 64 KB default (same value for every call)
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&wy_kernel<D, NVH>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-        if (e != hipSuccess) return e;
-        attr_set = true;
-    }
-    hipLaunchKernelGGL((wy_kernel<D, NVH>), dim3((unsigned)nb), dim3(128 * NVH), bytes, s, p,
+    hipLaunchKernelGGL((wy_kernel<D, NVH>), dim3((unsigned)nb), dim3(128 * NVH), 0, s, p,
                        static_cast<const uint16_t*>(a.k), static_cast<const uint16_t*>(a.q),
                        static_cast<const uint16_t*>(a.v), a.g, a.beta, a.state0, static_cast<uint16_t*>(a.o));
     return hipGetLastError();
