@@ -83,7 +83,7 @@ template <int DK, int OPT>
 __device__ __forceinline__ void row_update_lds(float (&S)[DK], const uint4* kr, float vj, float alpha, float beta) {
     constexpr int E = 16 / (int)sizeof(typename Op<OPT>::T);  // elements per 16-byte segment
     constexpr int C = DK < 32 ? DK : 32;
-    float u = 0.f;
+    Dot4 u;
 #pragma unroll
     for (int c0 = 0; c0 < DK; c0 += C) {
         asm volatile("" ::: "memory");
@@ -92,10 +92,10 @@ __device__ __forceinline__ void row_update_lds(float (&S)[DK], const uint4* kr, 
             float kf[E];
             unpack_seg<OPT>(kr[c / E], kf);
 #pragma unroll
-            for (int i = 0; i < E; ++i) u = __builtin_fmaf(S[c + i], kf[i], u);
+            for (int i = 0; i < E; ++i) u.add(c + i, S[c + i], kf[i]);
         }
     }
-    const float delta = beta * __builtin_fmaf(-alpha, u, vj);
+    const float delta = beta * __builtin_fmaf(-alpha, u.sum(), vj);
 #pragma unroll
     for (int c0 = 0; c0 < DK; c0 += C) {
         asm volatile("" ::: "memory");
@@ -147,7 +147,7 @@ __device__ __forceinline__ void replay_stage(const ReplayParams& p, const typena
 }
 
 template <int DK, int OPT>
-__global__ __launch_bounds__(64, 3) void replay_kernel(ReplayParams p, const typename Op<OPT>::T* __restrict__ k,
+__global__ __launch_bounds__(64, 2) void replay_kernel(ReplayParams p, const typename Op<OPT>::T* __restrict__ k,
                                                    const typename Op<OPT>::T* __restrict__ v,
                                                    const float* __restrict__ g, const float* __restrict__ beta,
                                                    float* __restrict__ state, const int32_t* __restrict__ path_out,

@@ -65,6 +65,23 @@ __device__ __forceinline__ int opaque(int x) {
     return x;
 }
 
+// Dot product of a value row with a key or query row: element i goes into partial sum
+// i % 4 (each in increasing i), then (s0 + s1) + (s2 + s3). Four independent chains
+// instead of one of length d_k. Every kernel that applies the update uses this order,
+// so verified and committed states agree bit for bit.
+struct Dot4 {
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    __device__ __forceinline__ void add(int i, float a, float b) {  // i is a compile-time index
+        switch (i & 3) {
+            case 0: s0 = __builtin_fmaf(a, b, s0); break;
+            case 1: s1 = __builtin_fmaf(a, b, s1); break;
+            case 2: s2 = __builtin_fmaf(a, b, s2); break;
+            default: s3 = __builtin_fmaf(a, b, s3); break;
+        }
+    }
+    __device__ __forceinline__ float sum() const { return (s0 + s1) + (s2 + s3); }
+};
+
 // One gated delta-rule node update (Eq. (2)-(3)) for one value row j of the head
 // matrix, S[i] = R[j][i]. `kp` is the node's key row (wave-uniform address, scalar
 // loads chunk by chunk).
@@ -76,15 +93,15 @@ template <int DK, int OPT>
 __device__ __forceinline__ void gdn_row_update(float (&S)[DK], const typename Op<OPT>::T* __restrict__ kp,
                                                float vj, float alpha, float beta) {
     constexpr int C = kChunk < DK ? kChunk : DK;
-    float u = 0.f;
+    Dot4 u;
 #pragma unroll
     for (int c = 0; c < DK; c += C) {
         float kf[C];
         Op<OPT>::template ld_row<C>(kp + opaque(c), kf);
 #pragma unroll
-        for (int i = 0; i < C; ++i) u = __builtin_fmaf(S[c + i], kf[i], u);
+        for (int i = 0; i < C; ++i) u.add(c + i, S[c + i], kf[i]);
     }
-    const float delta = beta * __builtin_fmaf(-alpha, u, vj);
+    const float delta = beta * __builtin_fmaf(-alpha, u.sum(), vj);
 #pragma unroll
     for (int c = 0; c < DK; c += C) {
         float kf[C];
@@ -98,15 +115,15 @@ __device__ __forceinline__ void gdn_row_update(float (&S)[DK], const typename Op
 template <int DK, int OPT>
 __device__ __forceinline__ float gdn_row_output(const float (&S)[DK], const typename Op<OPT>::T* __restrict__ qp) {
     constexpr int C = kChunk < DK ? kChunk : DK;
-    float o = 0.f;
+    Dot4 o;
 #pragma unroll
     for (int c = 0; c < DK; c += C) {
         float qf[C];
         Op<OPT>::template ld_row<C>(qp + opaque(c), qf);
 #pragma unroll
-        for (int i = 0; i < C; ++i) o = __builtin_fmaf(S[c + i], qf[i], o);
+        for (int i = 0; i < C; ++i) o.add(c + i, S[c + i], qf[i]);
     }
-    return o;
+    return o.sum();
 }
 
 // ---------------------------------------------------------------- launch geometry
