@@ -96,7 +96,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     __shared__ float G[kCand * kGS];               // block: Gram [candidate][chunk key | chunk query]
     __shared__ float recs[2 * NVH][kTile * W];     // per wave: the chunk's coefficient records
     __shared__ float alphas[2 * NVH][64];          // per wave: exp(g) of the candidates
-    __shared__ uint4 vbufs[2 * NVH][2][kTile * 8]; // per wave: value rows, double-buffered
+    __shared__ uint4 vbufs[2 * NVH][2][kTile * 8]; // per wave: value rows, then outputs; double-buffered
     const int tid = (int)threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: head and half in SGPRs
     const int lane = tid & 63;
@@ -122,6 +122,11 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     const int32_t* stacks = p.blob + p.o_chunk_stack + (long)kStack * p.blob[p.o_chunk_off + r];
     const long krow0 = (long)l * p.total_rows;
     const int t = lane % kTile;  // node of this lane in the chunk views
+    // Inside the chunk loop the lane index is re-laundered at every chunk, so values
+    // derived from it (LDS addresses and offsets) are recomputed rather than kept live
+    // across the loop, which would not fit in the registers.
+    int ln = lane;
+    int tn = t;
 
     // Rows of the chunk at c0 as seen by this lane: n = node t's (every lane; positions
     // past the end repeat the last node, so padding slots are exact copies of it) and
@@ -186,6 +191,20 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
     };
+    // The recursion leaves node n's output (bf16, this wave's 64 columns) in place of its
+    // value entries; a chunk's output rows then go out as 16-byte stores (slot q: node
+    // q / 8, columns j0 + 8 (q % 8) ..), rows taken from the records. Padding slots repeat
+    // the last node's row and values. nodes = 16 when the second half was not computed.
+    auto flush = [&](const uint4* ob, int nodes) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if (16 * i >= 2 * nodes) break;  // uniform
+            const int q = 64 * i + ln;
+            const uint4 val = ob[q];
+            const int rn = __float_as_int(wrec[(q >> 3) * W]);
+            *reinterpret_cast<uint4*>(out + ((krow0 + rn) * p.h_v + h) * kD + j0 + 8 * (q & 7)) = val;
+        }
+    };
     // the wave's value rows: slot q = 64 i + lane holds node q / 8, columns j0 + 8 (q % 8) .. + 7
     auto v_issue = [&](const Rows& rw, uint4* dst) {
         int ln = lane;
@@ -237,13 +256,10 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     float dst[D + 1];
 #pragma unroll
     for (int m = 0; m <= D; ++m) dst[m] = 0.f;
-    const int vcol = j0 + lane;
-    const int kb0 = lane / kTile;  // key block offset within a 16-key step (32x32x16 Gram)
     // Gram tiles of this wave: rows = chunk keys (mt 0, Gram rows 16..47) or path-stack
     // keys (mt 1, Gram rows 0..15); columns = the chunk's keys (nt 0) or queries (nt 1)
     constexpr int NT = NVH == 2 ? 1 : 2;
     const int mt = NVH == 2 ? (wave >> 1) : wave;
-    const int arow = mt == 0 ? t : 2 * kTile + (t & (kStack - 1));
 
     // R0 [k | q] of the 16 nodes of half hf of the chunk against the wave's 64 columns,
     // then the 4 x 4 exchange of lane groups (permlane32, then permlane16 swaps) that
@@ -256,10 +272,10 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                 pk[ct][i] = 0.f;
                 pq[ct][i] = 0.f;
             }
-        const int nrow = 16 * hf + lane % 16;  // A rows: the half's nodes
+        const int nrow = 16 * hf + ln % 16;  // A rows: the half's nodes
 #pragma unroll
         for (int kb = 0; kb < kD / 32; ++kb) {
-            const int sw = (4 * kb + lane / 16) ^ (nrow & 15);
+            const int sw = (4 * kb + ln / 16) ^ (nrow & 15);
             const bf16x8 fk = as_bf16x8(tile.slot[nrow * 16 + sw]);
             const bf16x8 fq = as_bf16x8(tile.slot[(kTile + nrow) * 16 + sw]);
 #pragma unroll
@@ -304,7 +320,16 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         asm volatile("" ::"v"(info.dep), "v"(info.g), "v"(info.b), "v"(info.ci[0]), "v"(info.ci[D / 4 - 1]),
                      "v"(rowC.n), "v"(rowA.n), "v"(rowA.s));
         lds_barrier();
-        if (more) v_issue(rowA, vbufs[wave][buf ^ 1]);
+        ln = lane;
+        asm volatile("" : "+v"(ln));
+        tn = ln % kTile;
+        const int kb0 = ln / kTile;  // key block offset within a 16-key step (32x32x16 Gram)
+        const int arow = mt == 0 ? tn : 2 * kTile + (tn & (kStack - 1));
+        if (c0 > 0) flush(vbufs[wave][buf ^ 1], kTile);  // the previous chunk had two halves
+        if (more) {
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the flush has read the buffer
+            v_issue(rowA, vbufs[wave][buf ^ 1]);
+        }
 
         // ---- Gram (head-independent) into LDS
         {
@@ -315,12 +340,12 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                 for (int e = 0; e < 16; ++e) gacc[i][e] = 0.f;
 #pragma unroll
             for (int s = 0; s < kD / 16; ++s) {
-                const int sw = (2 * s + kb0) ^ (t & 15);
+                const int sw = (2 * s + kb0) ^ (tn & 15);
                 const bf16x8 fa = as_bf16x8(tile.slot[arow * 16 + sw]);
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
                     const int nt = NVH == 2 ? (wave & 1) : i;
-                    const bf16x8 fb = as_bf16x8(tile.slot[(nt * kTile + t) * 16 + sw]);
+                    const bf16x8 fb = as_bf16x8(tile.slot[(nt * kTile + tn) * 16 + sw]);
                     gacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, gacc[i], 0, 0, 0);
                 }
             }
@@ -330,11 +355,11 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                 const int nt = NVH == 2 ? (wave & 1) : i;
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
-                    const int row = 8 * (e / 4) + 4 * (lane / kTile) + e % 4;
+                    const int row = 8 * (e / 4) + 4 * (ln / kTile) + e % 4;
                     if (mt == 0)
-                        G[(kStack + row) * kGS + nt * kTile + t] = gacc[i][e];
+                        G[(kStack + row) * kGS + nt * kTile + tn] = gacc[i][e];
                     else if (e < 8)  // rows 0..15: the stack slots
-                        G[row * kGS + nt * kTile + t] = gacc[i][e];
+                        G[row * kGS + nt * kTile + tn] = gacc[i][e];
                 }
             }
         }
@@ -343,12 +368,12 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         lds_barrier();  // the Gram is complete
 
         // ---- coefficient records of the wave's head (lanes 0..31: A, lanes 32..63: B)
-        if (lane < kTile + kStack) walpha[lane < kTile ? kStack + lane : lane - kTile] = __expf(info.g);
+        if (ln < kTile + kStack) walpha[ln < kTile ? kStack + ln : ln - kTile] = __expf(info.g);
         {
-            const bool isB = lane >= kTile;
-            const float* Gc = G + (isB ? kTile : 0) + t;
+            const bool isB = ln >= kTile;
+            const float* Gc = G + (isB ? kTile : 0) + tn;
             const float sc = isB ? 1.f : info.b;
-            float gam = walpha[kStack + t];  // Gamma(a_{d-1} -> t) = alpha_t
+            float gam = walpha[kStack + tn];  // Gamma(a_{d-1} -> t) = alpha_t
             float cv[D];
 #pragma unroll
             for (int m = D - 1; m >= 0; --m) {
@@ -360,7 +385,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                 cv[m] = (sc * gam) * gv * (live ? 1.f : 0.f);
                 gam *= live ? av : 1.f;  // then Gamma(a_{m-1} -> t); finally gamma_t
             }
-            float* rt = wrec + t * W;
+            float* rt = wrec + tn * W;
 #pragma unroll
             for (int q4 = 0; q4 < D / 4; ++q4)
                 *reinterpret_cast<float4*>(rt + 8 + (isB ? D : 0) + 4 * q4) =
@@ -368,7 +393,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
             if (!isB) {
                 *reinterpret_cast<float4*>(rt) =
                     make_float4(__int_as_float(rowC.n), __int_as_float(info.dep), info.b, gam);
-                *reinterpret_cast<float4*>(rt + 4) = make_float4(G[(kStack + t) * kGS + kTile + t], 0.f, 0.f, 0.f);
+                *reinterpret_cast<float4*>(rt + 4) = make_float4(G[(kStack + tn) * kGS + kTile + tn], 0.f, 0.f, 0.f);
             }
         }
         // next chunk's lane view (lands during the recursion)
@@ -379,7 +404,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         }
 
         const float* rec = wrec;
-        const uint16_t* vs = reinterpret_cast<const uint16_t*>(vbufs[wave][buf]);
+        uint16_t* vs = reinterpret_cast<uint16_t*>(vbufs[wave][buf]);
         // Straight-line over the 16 slots of a half: slots past the chunk's end hold exact
         // copies of its last node (tile rows, value row, record), so they recompute that
         // node's delta and output bit for bit and store the same value to the same place.
@@ -408,7 +433,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                 const int n = 16 * hf + i;
                 NodeRec cur;
                 load_rec(n, cur);
-                const float vj = __uint_as_float(((uint32_t)vs[n * 64 + lane]) << 16);
+                const float vj = __uint_as_float(((uint32_t)vs[n * 64 + ln]) << 16);
                 // sums over the path stack as even/odd partial sums (half the dependent chain)
                 float sa0 = 0.f, sa1 = 0.f, sb0 = 0.f, sb1 = 0.f;
 #pragma unroll
@@ -422,8 +447,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                 const float delta = __builtin_fmaf(cur.bn, u, -(sa0 + sa1));     // beta u - sum A delta
                 const float ov = __builtin_fmaf(cur.cn, delta, __builtin_fmaf(cur.gm, pq[i / 4][i % 4], sb0 + sb1));
                 dst[cur.d < D ? cur.d : D] = delta;  // uniform index: an indexed register write
-                uint16_t* orow = out + ((krow0 + cur.rn) * p.h_v + h) * kD;
-                orow[vcol] = f32_to_bf16(ov);
+                vs[n * 64 + ln] = f32_to_bf16(ov);     // over the consumed value entry
             }
         };
         exchange(pk);
@@ -440,6 +464,9 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         rowC = rowA;
         rowA = rowB;
     }
+    // the last chunk's outputs
+    const int cl = (N - 1) / kTile;  // index of the last chunk
+    flush(vbufs[wave][cl & 1], cl * kTile + kTile / 2 < N ? kTile : kTile / 2);
 }
 
 template <int D, int NVH>
