@@ -220,17 +220,32 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         }
     };
 
+    // R0 columns j0 + 16 ct + lane%16 (ct = 0..3) as B fragments of the 16x16x32 MFMA:
+    // key block kb holds keys 32 kb + 8 (lane/16) + e.
+    const float* S = state0 + (((long)r * p.n_layers + l) * p.h_v + h) * (long)(kD * kD);
+    const float* Sl = S + (long)(8 * (lane / 16)) * kD + j0 + lane % 16;
+    uint32_t raw[4][kD / 32][8];
+    auto slab_load = [&](int ct) {
+#pragma unroll
+        for (int kb = 0; kb < kD / 32; ++kb)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) raw[ct][kb][e] = __float_as_uint(Sl[(long)(32 * kb + e) * kD + 16 * ct]);
+    };
+    // The chunk's rows are loaded first and half the state slab behind them, so that the
+    // row-dependent copies below wait for the rows only (at most 63 loads issued after
+    // them) while the slab is already in flight; then the other half.
     Rows rowC = lane_rows(0);  // this chunk
+    slab_load(0);
+    slab_load(1);
+    asm volatile("" ::: "memory");
     v_issue(rowC, vbufs[wave][0]);  // (its shuffles precede every copy)
     tile_issue(rowC);
     LaneInfo<D> info;
     lane_info(0, rowC, info);
     Rows rowA = N > kTile ? lane_rows(kTile) : rowC;  // next chunk
+    slab_load(2);
+    slab_load(3);
 
-    // R0 columns j0 + 16 ct + lane%16 (ct = 0..3) as B fragments of the 16x16x32 MFMA:
-    // key block kb holds keys 32 kb + 8 (lane/16) + e.
-    const float* S = state0 + (((long)r * p.n_layers + l) * p.h_v + h) * (long)(kD * kD);
-    const float* Sl = S + (long)(8 * (lane / 16)) * kD + j0 + lane % 16;
     bf16x8 bhi[4][kD / 32], blo[4][kD / 32];
     // Each fp32 value x is held as hi + lo: hi = x truncated to bf16, lo = the exact
     // remainder x - hi rounded to nearest bf16 (|x - hi - lo| <= 2^-15 |x|).
@@ -241,8 +256,8 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
             uint32_t hw[4], lw[4];
 #pragma unroll
             for (int e2 = 0; e2 < 4; ++e2) {
-                const uint32_t x0 = __float_as_uint(Sl[(long)(32 * kb + 2 * e2) * kD + 16 * ct]);
-                const uint32_t x1 = __float_as_uint(Sl[(long)(32 * kb + 2 * e2 + 1) * kD + 16 * ct]);
+                const uint32_t x0 = raw[ct][kb][2 * e2];
+                const uint32_t x1 = raw[ct][kb][2 * e2 + 1];
                 hw[e2] = __builtin_amdgcn_perm(x1, x0, 0x07060302u);  // {hi(x1), hi(x0)}: upper halves
                 lw[e2] = f32x2_to_bf16x2(__uint_as_float(x0) - __uint_as_float(x0 & 0xffff0000u),
                                          __uint_as_float(x1) - __uint_as_float(x1 & 0xffff0000u));
