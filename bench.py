@@ -11,6 +11,10 @@ its duration measured by HIP events on the launch stream, the other kernels'
 durations, and the fp64 CPU oracle timed on a bounded sample of the same workload.
 
   python bench.py [--steps K] [--warmup W] [--config batched] [--policy wy]
+                  [--commit deferred|eager]
+  (deferred: each step's verification also publishes the previous step's accepted
+   path, in the same pass over the state, and the commit derives the path and the conv
+   history only; eager: the commit replays the path itself; wy policy only)
   python bench.py --copy-probe     # plain 1 GiB device copy x3 (HBM counter calibration)
 
 The roofline's `traffic` (measured HBM bytes per verify call) is reported from
@@ -49,7 +53,7 @@ def verify_source_hash(policy):
     return h.hexdigest()
 
 
-def recorded_traffic(policy, config):
+def recorded_traffic(policy, config, commit="eager"):
     """Measured HBM bytes per verify call, if recorded for exactly these kernel sources."""
     try:
         with open(TRAFFIC_RECORD) as fh:
@@ -57,7 +61,8 @@ def recorded_traffic(policy, config):
     except (OSError, ValueError):
         return None
     for r in rec.get("records", []):
-        if r.get("policy") == policy and r.get("config") == config and r.get("sources_sha256") == verify_source_hash(policy):
+        if (r.get("policy") == policy and r.get("config") == config and r.get("commit", "eager") == commit
+                and r.get("sources_sha256") == verify_source_hash(policy)):
             return r
     return None
 
@@ -103,8 +108,11 @@ def alg_bytes_flops(wl):
     active = sum(1 for p, a in zip(wl.parents, wl.accepted) if a >= 0)
     c_bytes = active * wl.n_layers * wl.h_v * 2 * mat + c_upd * ((wl.d_k * opb) / grp + wl.d_v * opb + 8)
     c_flops = c_upd * 4 * wl.d_k * wl.d_v
+    # publication folded into the next verification: the state is read there anyway, so
+    # what it adds is the state written back and the path's operand rows
+    pub_bytes = c_bytes - active * wl.n_layers * wl.h_v * mat
     conv_bytes = wl.total_nodes * wl.n_layers * wl.channels * opb * 2 + wl.n_layers * wl.channels * 16
-    return dict(verify_bytes=v_bytes, verify_flops=v_flops, commit_bytes=c_bytes,
+    return dict(verify_bytes=v_bytes, verify_flops=v_flops, commit_bytes=c_bytes, pub_bytes=pub_bytes,
                 commit_flops=c_flops, conv_bytes=conv_bytes, commit_updates=c_upd)
 
 
@@ -160,6 +168,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="batched")
     ap.add_argument("--policy", default="wy")
+    ap.add_argument("--commit", choices=("deferred", "eager"), default="deferred")
     ap.add_argument("--copy-probe", action="store_true", help="only run the counter-calibration copy")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
@@ -180,6 +189,7 @@ def main():
     from lumo_synth import configs
 
     policy = L.POLICIES[args.policy]
+    deferred = args.commit == "deferred" and policy == L.LUMO_POLICY_WY
     log(f"[bench] generating {args.config}")
     wl = configs.build(args.config)
     log(f"[bench] uploading; policy {args.policy}")
@@ -192,10 +202,13 @@ def main():
         st.conv(stream)
         if ev is not None:
             ev[1].record(stream)
-        st.verify(stream)
+        if deferred:
+            st.verify_pending(st, stream)  # publishes the previous step's path, then verifies
+        else:
+            st.verify(stream)
         if ev is not None:
             ev[2].record(stream)
-        st.commit(stream)
+        st.commit(stream, defer=deferred)
         if ev is not None:
             ev[3].record(stream)
 
@@ -223,35 +236,39 @@ def main():
     ab = alg_bytes_flops(wl)
     hn = wl.head_node_updates
     if policy == L.LUMO_POLICY_WY:
-        ach = ab["verify_bytes"] / (ver_ms * 1e-3) / 1e9
+        vb = ab["verify_bytes"] + (ab["pub_bytes"] if deferred else 0)
+        ach = vb / (ver_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
     else:
         ach = ab["verify_flops"] / (ver_ms * 1e-3) / 1e12
         roof = {"bound": "alu", "achieved": round(ach, 2), "peak": PEAK_VALU_F32_TFS,
                 "unit": "TFLOP/s", "frac": round(ach / PEAK_VALU_F32_TFS, 4), "traffic": None}
-    tr = recorded_traffic(args.policy, args.config)
+    mode = "deferred" if deferred else "eager"
+    tr = recorded_traffic(args.policy, args.config, mode)
     if tr is not None:
         roof["traffic"] = {"fetch_bytes": tr["fetch_bytes"], "write_bytes": tr["write_bytes"],
                            "total_bytes": tr["fetch_bytes"] + tr["write_bytes"], "unit": "B per verify call",
                            "source": "profiles/traffic.json"}
-    roof["kernel"] = "verify"
-    roof["per_launch"] = (f"{ab['verify_flops'] / 1e9:.2f} GFLOP, {ab['verify_bytes'] / 1e6:.1f} MB "
+    roof["kernel"] = "verify + publication of the previous path" if deferred else "verify"
+    roof["per_launch"] = (f"{ab['verify_flops'] / 1e9:.2f} GFLOP, "
+                          f"{(ab['verify_bytes'] + (ab['pub_bytes'] if deferred else 0)) / 1e6:.1f} MB "
                           f"algorithmic per verify call")
     kernels = {
         "conv_gather_ms": round(conv_ms, 4),
         "conv_hbm_frac": round(ab["conv_bytes"] / (conv_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         "verify_ms": round(ver_ms, 4),
         "commit_ms": round(com_ms, 4),
-        "commit_hbm_frac": round(ab["commit_bytes"] / (com_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
     }
+    if not deferred:
+        kernels["commit_hbm_frac"] = round(ab["commit_bytes"] / (com_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
     out = {
         "metric": METRIC, "value": round(hn / (ms_step * 1e-3), 1), "unit": "head-node updates/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded trees and operands shaped like the paper's workloads)",
         "config": {"workload": f"{args.config}: {WORKLOAD_TEXT[args.config]}",
-                   "policy": args.policy, "head_node_updates_per_step": hn,
+                   "policy": args.policy, "commit": mode, "head_node_updates_per_step": hn,
                    "operands": "bf16" if wl.op_dtype == 1 else "f32"},
         "roofline": roof, "kernels": kernels,
     }

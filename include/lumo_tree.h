@@ -9,7 +9,8 @@
  *   lumo_tree_gdn_verify   device: every node's recurrent output from its ancestry
  *   lumo_gdn_commit        device: derive the accepted path, replay it into the
  *                          native state, publish the convolution history
- * plus a captured-graph form of the commit.
+ * plus a captured-graph form of the commit, and lumo_tree_gdn_verify_pending,
+ * which folds the replay of one iteration into the verification of the next.
  *
  * Conventions shared by every entry point
  *   - Device pointers are HIP device (or managed) memory owned by the caller.
@@ -214,6 +215,37 @@ lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lumo_tree_desc
                                  int32_t flags, void* stream);
 
 /*
+ * lumo_tree_gdn_verify_pending - publish the previous iteration's accepted path into
+ * the state bank and verify this iteration's tree from the published state, in one
+ * pass over the state (Alg. 1: publication of iteration t-1 precedes verification of
+ * iteration t; deferred into this call, each state tile is read once and written once
+ * instead of being read twice and written once). For every request r, layer l and
+ * value head h:
+ *   state[r][l][h] <- the state after replaying the pending path of r with the
+ *                     update of lumo_gdn_commit and the pending operands, in place;
+ *   o              <- as lumo_tree_gdn_verify with state0 = that published state.
+ *   desc, q, k, v, g, beta, o   this iteration; desc's plan must use LUMO_POLICY_WY
+ *                               (bf16 operands, d_k = d_v = 128, paths of at most
+ *                               17 nodes), else LUMO_EUNSUPPORTED
+ *   state                       in/out: the state bank before the pending publication
+ *   pend_desc                   the previous iteration's descriptor (same n_req)
+ *   max_path, path_out, path_len  as written by lumo_gdn_commit for pend_desc;
+ *                               path_len[r] <= 0 leaves request r's state as it is
+ *   pend_k, pend_v, pend_g, pend_beta  the previous iteration's operands (device,
+ *                               rows of pend_desc)
+ * The replay sums its dot products in another order than lumo_gdn_commit, so the
+ * published state agrees with it to fp32 rounding, not bitwise. Requests with no
+ * nodes in this iteration are still published.
+ */
+lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                         const void* q, const void* k, const void* v,
+                                         const float* g, const float* beta, float* state, void* o,
+                                         const lumo_tree_desc* pend_desc, int32_t max_path,
+                                         const int32_t* path_out, const int32_t* path_len,
+                                         const void* pend_k, const void* pend_v,
+                                         const float* pend_g, const float* pend_beta, void* stream);
+
+/*
  * lumo_gdn_commit - publish the accepted path (Alg. 1 publication; Alg. 2 replay;
  * device-selected path Sec. V-A; conv history Sec. V-C).
  *   accepted_node  device [n_req]: request-local accepted node, -1 = none
@@ -225,7 +257,10 @@ lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lumo_tree_desc
  *   k, v, g, beta  the operands recorded for verification (q is not needed)
  *   state          in/out: the pre-tree state, replaced in place by the state after
  *                  replaying the path with the update of lumo_tree_gdn_verify
- *                  (bitwise the same arithmetic); untouched for an empty path
+ *                  (bitwise the same arithmetic); untouched for an empty path.
+ *                  NULL defers the replay to the next lumo_tree_gdn_verify_pending
+ *                  (k, v, g, beta may then be NULL too): only path_out, path_len and
+ *                  the conv history are written
  *   x, conv_hist   nullable pair: when given, conv_hist[r][l] becomes the last
  *                  three entries of (conv_hist[r][l], x rows of the path), in place
  */

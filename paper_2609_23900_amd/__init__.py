@@ -4,7 +4,7 @@ kernels; torch tensors only provide device memory and the current HIP stream.
 
 The functions keep the names of the C ABI (include/lumo_tree.h):
   lumo_tree_plan, lumo_tree_gdn_workspace_bytes, lumo_tree_conv_gather,
-  lumo_tree_gdn_verify, lumo_gdn_commit, lumo_gdn_commit_graph_create,
+  lumo_tree_gdn_verify, lumo_tree_gdn_verify_pending, lumo_gdn_commit, lumo_gdn_commit_graph_create,
   lumo_gdn_commit_graph_launch, lumo_gdn_commit_graph_destroy, lumo_last_error,
   lumo_version.
 Device arguments are torch tensors on the GPU (or None where the ABI allows NULL);
@@ -73,6 +73,7 @@ def _load():
     L.lumo_tree_gdn_workspace_bytes.restype = SZ
     L.lumo_tree_conv_gather.argtypes = [PD, PT, I32, P, P, P, P, I32, P, P]
     L.lumo_tree_gdn_verify.argtypes = [PD, PT, P, P, P, P, P, P, P, P, P, SZ, I32, P]
+    L.lumo_tree_gdn_verify_pending.argtypes = [PD, PT, P, P, P, P, P, P, P, PT, I32, P, P, P, P, P, P, P]
     L.lumo_gdn_commit.argtypes = [PD, PT, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
     L.lumo_gdn_commit_graph_create.argtypes = [PD, PT, I32, P, P, P, P, P, P, P, P, I32, P, P,
                                                ctypes.POINTER(ctypes.c_void_p)]
@@ -82,7 +83,7 @@ def _load():
     L.lumo_last_error.restype = ctypes.c_char_p
     L.lumo_version.restype = ctypes.c_char_p
     for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_gdn_verify",
-              "lumo_gdn_commit", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
+              "lumo_tree_gdn_verify_pending", "lumo_gdn_commit", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -185,6 +186,16 @@ def lumo_tree_gdn_verify(d, desc: TreeDesc, q, k, v, g, beta, state0, o, node_st
                                      _dptr(v), _dptr(g), _dptr(beta), _dptr(state0), _dptr(o),
                                      _dptr(node_states), _dptr(workspace), ws_bytes, int(flags),
                                      _stream(stream)))
+
+
+def lumo_tree_gdn_verify_pending(d, desc: TreeDesc, q, k, v, g, beta, state, o, pend_desc: TreeDesc,
+                                 max_path, path_out, path_len, pend_k, pend_v, pend_g, pend_beta,
+                                 stream=None):
+    _check(_lib.lumo_tree_gdn_verify_pending(
+        ctypes.byref(d), ctypes.byref(desc.desc), _dptr(q), _dptr(k), _dptr(v), _dptr(g),
+        _dptr(beta), _dptr(state), _dptr(o), ctypes.byref(pend_desc.desc), int(max_path),
+        _dptr(path_out), _dptr(path_len), _dptr(pend_k), _dptr(pend_v), _dptr(pend_g),
+        _dptr(pend_beta), _stream(stream)))
 
 
 def lumo_gdn_commit(d, desc: TreeDesc, max_path, accepted_node, path_out, path_len, k, v, g, beta,

@@ -153,6 +153,54 @@ extern "C" lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lum
     return LUMO_OK;
 }
 
+extern "C" lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                                    const void* q, const void* k, const void* v, const float* g,
+                                                    const float* beta, float* state, void* o,
+                                                    const lumo_tree_desc* pend_desc, int32_t max_path,
+                                                    const int32_t* path_out, const int32_t* path_len,
+                                                    const void* pend_k, const void* pend_v, const float* pend_g,
+                                                    const float* pend_beta, void* stream) {
+    static const char* fn = "lumo_tree_gdn_verify_pending";
+    clear_error();
+    LUMO_TRY(check_dims(dims, fn));
+    LUMO_TRY(check_desc(dims, desc, fn));
+    if (!pend_desc) return fail(LUMO_EINVAL, "%s: pend_desc is NULL", fn);
+    LUMO_TRY(check_desc(dims, pend_desc, fn));
+    if (desc->plan.policy != LUMO_POLICY_WY)
+        return fail(LUMO_EUNSUPPORTED, "%s: needs a plan built for LUMO_POLICY_WY (plan policy %d)", fn,
+                    desc->plan.policy);
+    if (dims->op_dtype != LUMO_BF16 || dims->d_k != 128 || dims->d_v != 128)
+        return fail(LUMO_EUNSUPPORTED, "%s: the WY policy is built for bf16 operands with d_k = d_v = 128", fn);
+    if (desc->plan.max_depth > kWyMaxDepth)
+        return fail(LUMO_EUNSUPPORTED, "%s: the WY policy handles paths of at most %d nodes (plan has %d)", fn,
+                    kWyMaxDepth, desc->plan.max_depth);
+    if (max_path < 1 || max_path > 4096) return fail(LUMO_EINVAL, "%s: max_path %d (1..4096)", fn, max_path);
+    if (dims->n_req == 0) return LUMO_OK;
+    LUMO_TRY(check_ptr(state, fn, "state"));
+    LUMO_TRY(check_ptr(path_out, fn, "path_out"));
+    LUMO_TRY(check_ptr(path_len, fn, "path_len"));
+    if (pend_desc->plan.total_nodes > 0) {
+        LUMO_TRY(check_ptr(pend_k, fn, "pend_k"));
+        LUMO_TRY(check_ptr(pend_v, fn, "pend_v"));
+        LUMO_TRY(check_ptr(pend_g, fn, "pend_g"));
+        LUMO_TRY(check_ptr(pend_beta, fn, "pend_beta"));
+    }
+    if (desc->plan.total_nodes > 0) {
+        LUMO_TRY(check_ptr(q, fn, "q"));
+        LUMO_TRY(check_ptr(k, fn, "k"));
+        LUMO_TRY(check_ptr(v, fn, "v"));
+        LUMO_TRY(check_ptr(g, fn, "g"));
+        LUMO_TRY(check_ptr(beta, fn, "beta"));
+        LUMO_TRY(check_ptr(o, fn, "o"));
+    }
+    GdnArgs a{q, k, v, g, beta, state, o, nullptr, nullptr};
+    PendArgs pa{pend_desc, max_path, path_out, path_len, pend_k, pend_v, pend_g, pend_beta, state};
+    hipError_t e = launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream), &pa);
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not available in this build", fn);
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
 namespace {
 
 lumo_status check_commit(const lumo_gdn_dims* dims, const lumo_tree_desc* desc, int32_t max_path,
@@ -166,11 +214,13 @@ lumo_status check_commit(const lumo_gdn_dims* dims, const lumo_tree_desc* desc, 
     LUMO_TRY(check_ptr(accepted, fn, "accepted_node"));
     LUMO_TRY(check_ptr(path_out, fn, "path_out"));
     LUMO_TRY(check_ptr(path_len, fn, "path_len"));
-    LUMO_TRY(check_ptr(k, fn, "k"));
-    LUMO_TRY(check_ptr(v, fn, "v"));
-    LUMO_TRY(check_ptr(g, fn, "g"));
-    LUMO_TRY(check_ptr(beta, fn, "beta"));
-    LUMO_TRY(check_ptr(state, fn, "state"));
+    LUMO_TRY(check_ptr(state, fn, "state", true));
+    if (state) {  // a NULL state defers the replay: the operands are not read
+        LUMO_TRY(check_ptr(k, fn, "k"));
+        LUMO_TRY(check_ptr(v, fn, "v"));
+        LUMO_TRY(check_ptr(g, fn, "g"));
+        LUMO_TRY(check_ptr(beta, fn, "beta"));
+    }
     if ((x == nullptr) != (conv_hist == nullptr))
         return fail(LUMO_EINVAL, "%s: x and conv_hist must both be given or both be NULL", fn);
     if (x) {

@@ -274,6 +274,7 @@ hipError_t launch_commit(const lumo_gdn_dims& d, const lumo_tree_desc& desc, con
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
 
+    if (a.state) {  // NULL: the replay is deferred to the next verification
     ReplayParams rp;
     rp.blob = desc.blob;
     rp.o_node_off = pl.o_node_off;
@@ -290,6 +291,7 @@ hipError_t launch_commit(const lumo_gdn_dims& d, const lumo_tree_desc& desc, con
     e = d.op_dtype == LUMO_BF16 ? launch_replay<1>(d.d_k, dim3((unsigned)blocks), s, rp, a)
                                 : launch_replay<0>(d.d_k, dim3((unsigned)blocks), s, rp, a);
     if (e != hipSuccess) return e;
+    }
 
     if (a.x && a.conv_hist) {
         HistParams hp;

@@ -23,8 +23,25 @@ struct GdnArgs {
 // Sequential path scans (PATHS / TWO_LEVEL / RECOMPUTE): one launch per dependency level.
 hipError_t launch_scan(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s);
 
-// Tree WY form on MFMA: one launch, no workspace.
-hipError_t launch_wy(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s);
+// A pending accepted path of the previous iteration, replayed into the state bank by
+// the WY kernel before it verifies (lumo_tree_gdn_verify_pending).
+struct PendArgs {
+    const lumo_tree_desc* desc;  // previous iteration's descriptor
+    int32_t max_path;
+    const int32_t* path_out;
+    const int32_t* path_len;
+    const void* k;
+    const void* v;
+    const float* g;
+    const float* beta;
+    float* state;  // in/out; the verification reads the published state from here
+};
+
+// Tree WY form on MFMA: one launch, no workspace. With `pend`, the pending path is
+// published into pend->state first (a.state0 is ignored) and requests without nodes
+// in `desc` are still published.
+hipError_t launch_wy(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s,
+                     const PendArgs* pend = nullptr);
 constexpr int kWyMaxDepth = 17;  // nodes on a root-to-leaf path
 
 struct CommitArgs {

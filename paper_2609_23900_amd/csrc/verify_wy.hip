@@ -61,6 +61,21 @@ struct WyParams {
     int32_t n_layers, total_rows, h_k, h_v, group;
 };
 
+// The previous iteration's accepted path, published into the state bank before the
+// verification reads it (deferred publication).
+struct PendParams {
+    const int32_t* blob;  // the previous iteration's plan
+    int32_t o_node_off, o_row, total_rows, max_path;
+    const int32_t* path_out;
+    const int32_t* path_len;
+    const uint16_t* k;
+    const uint16_t* v;
+    const float* g;
+    const float* beta;
+    float* state;
+};
+constexpr int kPend = 16;  // path entries staged per round of the deferred publication
+
 // Block-shared staging of one chunk: [key 32 | query 32 | path-stack key 16] rows of
 // 16 slots of 8 bf16; key block kb of row n sits in slot kb ^ (n & 15), so the
 // fragment reads of a half-wave (32 rows, one key block) spread over all banks.
@@ -80,21 +95,33 @@ struct LaneInfo {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
 
+// The sum of x over the four 16-lane rows, in every lane (the same bits in all four:
+// (x0 + x1) + (x2 + x3)).
+__device__ __forceinline__ float row_group_sum(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // Two waves per SIMD for D = 8 (79 KB of LDS per 4-wave block); with D = 16 the
 // records make a 4-wave block too large for two per CU, so one wave per SIMD.
-template <int D, int NVH>
+// PEND: the state bank (state0 = pd.state) first receives the replay of the previous
+// iteration's accepted path (Eq. (2)-(3) per path node), is stored back, and the
+// verification then starts from it; requests without nodes are published only.
+template <int D, int NVH, bool PEND>
 __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, const uint16_t* __restrict__ kmat,
                                                     const uint16_t* __restrict__ qmat,
                                                     const uint16_t* __restrict__ vmat, const float* __restrict__ gmat,
                                                     const float* __restrict__ bmat, const float* __restrict__ state0,
-                                                    uint16_t* __restrict__ out) {
+                                                    uint16_t* __restrict__ out, PendParams pd) {
     constexpr int W = Rec<D>::kWords;
     constexpr int nthr = 128 * NVH;
     // LDS, one object per role: the compiler orders LDS reads after the direct
     // global-to-LDS copies only where they may touch the same object.
     __shared__ KQTile tile;                        // block: chunk keys, queries, path-stack keys
-    __shared__ float G[kCand * kGS];               // block: Gram [candidate][chunk key | chunk query]
-    __shared__ float recs[2 * NVH][kTile * W];     // per wave: the chunk's coefficient records
+    __shared__ __attribute__((aligned(16))) float G[kCand * kGS];  // block: Gram [candidate][chunk key | chunk query]
+    __shared__ __attribute__((aligned(16))) float recs[2 * NVH][kTile * W];  // per wave: the chunk's coefficient records
     __shared__ float alphas[2 * NVH][64];          // per wave: exp(g) of the candidates
     __shared__ uint4 vbufs[2 * NVH][2][kTile * 8]; // per wave: value rows, then outputs; double-buffered
     const int tid = (int)threadIdx.x;
@@ -115,7 +142,12 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     const int j0 = 64 * (wave & 1);
     const int base = p.blob[p.o_node_off + r];
     const int N = p.blob[p.o_node_off + r + 1] - base;
-    if (N <= 0) return;  // uniform over the block
+    int plen = 0;  // pending path length; an empty or invalid path leaves the state as it is
+    if constexpr (PEND) {
+        plen = pd.path_len[r];
+        if (plen > pd.max_path || pd.blob[pd.o_node_off + r + 1] <= pd.blob[pd.o_node_off + r]) plen = 0;
+    }
+    if (N <= 0 && plen <= 0) return;  // uniform over the block
     const int32_t* prow = p.blob + p.o_pre_row + base;
     const int32_t* pdep = p.blob + p.o_pre_depth + base;
     const uint32_t* pci = reinterpret_cast<const uint32_t*>(p.blob + p.o_pre_ci) + (long)kPreCiWords * base;
@@ -234,17 +266,125 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     // The chunk's rows are loaded first and half the state slab behind them, so that the
     // row-dependent copies below wait for the rows only (at most 63 loads issued after
     // them) while the slab is already in flight; then the other half.
-    Rows rowC = lane_rows(0);  // this chunk
-    slab_load(0);
-    slab_load(1);
-    asm volatile("" ::: "memory");
-    v_issue(rowC, vbufs[wave][0]);  // (its shuffles precede every copy)
-    tile_issue(rowC);
+    // Deferred publication: the pending path's key rows (block-shared, in the Gram's
+    // space) and the wave's value entries (in its record space) are staged kPend entries
+    // at a time; lane e holds entry e's decay and beta. Each entry applies
+    //   u = R k,  delta = beta (v - alpha u),  R <- alpha R + delta k
+    // to the slab in registers (lane: 4 columns x 32 keys; u summed over the four lane
+    // rows that share a column), then the slab is stored back.
+    auto pend_publish = [&]() {
+        const int pbase = pd.blob[pd.o_node_off + r];
+        const int pn = pd.blob[pd.o_node_off + r + 1] - pbase;
+        const int32_t* ppath = pd.path_out + (long)r * pd.max_path;
+        const long prow0 = (long)l * pd.total_rows;
+        uint4* kst = reinterpret_cast<uint4*>(G);       // kPend key rows x 16 slots
+        uint4* vst = reinterpret_cast<uint4*>(wrec);    // kPend entries x 64 values (8 slots)
+        const uint16_t* vsh = reinterpret_cast<const uint16_t*>(wrec);
+        for (int e0 = 0; e0 < plen; e0 += kPend) {
+            const int ne = min(plen - e0, kPend);
+            if (e0 > 0) lds_barrier();  // every wave has read the previous entries' key rows
+            const int node = min(max(ppath[e0 + min(lane % kPend, ne - 1)], 0), pn - 1);
+            const int row = pd.blob[pd.o_row + pbase + node];
+            const long gl = (prow0 + row) * p.h_v + h;
+            const float pa = __expf(pd.g[gl]);
+            const float pb = pd.beta[gl];
+            int rv[kPend * 8 / 64];
+#pragma unroll
+            for (int i = 0; i < kPend * 8 / 64; ++i) rv[i] = __shfl(row, (64 * i + lane) >> 3);
+            constexpr int kKRounds = kPend * 16 / nthr;
+#pragma unroll
+            for (int j = 0; j < kKRounds; ++j) {
+                const int nr0 = (j * nthr + 64 * wave) >> 4;  // uniform: this wave fills rows nr0 .. nr0+3
+                int rq[4];
+#pragma unroll
+                for (int k4 = 0; k4 < 4; ++k4) rq[k4] = __builtin_amdgcn_readlane(row, nr0 + k4);
+                const int g4 = lane >> 4;
+                const int src = g4 == 0 ? rq[0] : g4 == 1 ? rq[1] : g4 == 2 ? rq[2] : rq[3];
+                __builtin_amdgcn_global_load_lds(pd.k + ((prow0 + src) * p.h_k + hk) * kD + 8 * (lane & 15),
+                                                 (lds_void*)&kst[j * nthr + 64 * wave], 16, 0, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < kPend * 8 / 64; ++i) {
+                const int q = 64 * i + lane;
+                __builtin_amdgcn_global_load_lds(pd.v + ((prow0 + rv[i]) * p.h_v + h) * kD + j0 + 8 * (q & 7),
+                                                 (lds_void*)&vst[64 * i], 16, 0, 0);
+            }
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            for (int e = 0; e < ne; ++e) {
+                const float ae = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pa), e));
+                const float be = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pb), e));
+                float kf[kD / 32][8];
+#pragma unroll
+                for (int kb = 0; kb < kD / 32; ++kb) {
+                    const uint4 w = kst[e * 16 + 4 * kb + (lane >> 4)];  // keys 32 kb + 8 (lane/16) ..
+                    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                    for (int e2 = 0; e2 < 4; ++e2) {
+                        kf[kb][2 * e2] = bf16_lo(ww[e2]);
+                        kf[kb][2 * e2 + 1] = bf16_hi(ww[e2]);
+                    }
+                }
+                float dl[4];
+#pragma unroll
+                for (int ct = 0; ct < 4; ++ct) {
+                    float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+                    for (int kb = 0; kb < kD / 32; ++kb)
+#pragma unroll
+                        for (int e8 = 0; e8 < 8; ++e8) {
+                            float& acc = (kb & 1) ? s1 : s0;
+                            acc = __builtin_fmaf(__uint_as_float(raw[ct][kb][e8]), kf[kb][e8], acc);
+                        }
+                    const float u = row_group_sum(s0 + s1);
+                    const float vj = bf16_lo((uint32_t)vsh[e * 64 + 16 * ct + lane % 16]);
+                    dl[ct] = be * __builtin_fmaf(-ae, u, vj);
+                }
+#pragma unroll
+                for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+                    for (int kb = 0; kb < kD / 32; ++kb)
+#pragma unroll
+                        for (int e8 = 0; e8 < 8; ++e8)
+                            raw[ct][kb][e8] = __float_as_uint(
+                                __builtin_fmaf(dl[ct], kf[kb][e8], ae * __uint_as_float(raw[ct][kb][e8])));
+            }
+        }
+        float* Sw = pd.state + (((long)r * p.n_layers + l) * p.h_v + h) * (long)(kD * kD) +
+                    (long)(8 * (lane / 16)) * kD + j0 + lane % 16;
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+            for (int kb = 0; kb < kD / 32; ++kb)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) Sw[(long)(32 * kb + e) * kD + 16 * ct] = __uint_as_float(raw[ct][kb][e]);
+    };
+
+    Rows rowC, rowA;  // this chunk, the next
     LaneInfo<D> info;
-    lane_info(0, rowC, info);
-    Rows rowA = N > kTile ? lane_rows(kTile) : rowC;  // next chunk
-    slab_load(2);
-    slab_load(3);
+    if (!PEND || plen <= 0) {
+        rowC = lane_rows(0);
+        slab_load(0);
+        slab_load(1);
+        asm volatile("" ::: "memory");
+        v_issue(rowC, vbufs[wave][0]);  // (its shuffles precede every copy)
+        tile_issue(rowC);
+        lane_info(0, rowC, info);
+        rowA = N > kTile ? lane_rows(kTile) : rowC;
+        slab_load(2);
+        slab_load(3);
+    } else {
+        if (N > 0) rowC = lane_rows(0);
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) slab_load(ct);
+        pend_publish();
+        if (N <= 0) return;  // uniform: nothing to verify for this request
+        v_issue(rowC, vbufs[wave][0]);
+        tile_issue(rowC);
+        lane_info(0, rowC, info);
+        rowA = N > kTile ? lane_rows(kTile) : rowC;
+    }
 
     bf16x8 bhi[4][kD / 32], blo[4][kD / 32];
     // Each fp32 value x is held as hi + lo: hi = x truncated to bf16, lo = the exact
@@ -484,17 +624,20 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     flush(vbufs[wave][cl & 1], cl * kTile + kTile / 2 < N ? kTile : kTile / 2);
 }
 
-template <int D, int NVH>
-hipError_t launch_wy_kernel(const lumo_gdn_dims& d, const WyParams& p, const GdnArgs& a, hipStream_t s) {
+template <int D, int NVH, bool PEND>
+hipError_t launch_wy_kernel(const lumo_gdn_dims& d, const WyParams& p, const GdnArgs& a, hipStream_t s,
+                            const PendParams& pp) {
     const long nb = (long)d.n_req * d.n_layers * d.h_k * (p.group / NVH);
-    hipLaunchKernelGGL((wy_kernel<D, NVH>), dim3((unsigned)nb), dim3(128 * NVH), 0, s, p,
+    hipLaunchKernelGGL((wy_kernel<D, NVH, PEND>), dim3((unsigned)nb), dim3(128 * NVH), 0, s, p,
                        static_cast<const uint16_t*>(a.k), static_cast<const uint16_t*>(a.q),
-                       static_cast<const uint16_t*>(a.v), a.g, a.beta, a.state0, static_cast<uint16_t*>(a.o));
+                       static_cast<const uint16_t*>(a.v), a.g, a.beta, PEND ? pp.state : a.state0,
+                       static_cast<uint16_t*>(a.o), pp);
     return hipGetLastError();
 }
 
-template <int D>
-hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s) {
+template <int D, bool PEND>
+hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s,
+                       const PendParams& pp) {
     const lumo_plan& pl = desc.plan;
     WyParams p;
     p.blob = desc.blob;
@@ -511,17 +654,38 @@ hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.group = d.h_v / d.h_k;
     // one block per (request, layer, key head, pair of value heads): the pair's waves
     // share the staged key and query rows and the Gram
-    if (p.group % 2 == 0) return launch_wy_kernel<D, 2>(d, p, a, s);
-    return launch_wy_kernel<D, 1>(d, p, a, s);
+    if (p.group % 2 == 0) return launch_wy_kernel<D, 2, PEND>(d, p, a, s, pp);
+    return launch_wy_kernel<D, 1, PEND>(d, p, a, s, pp);
 }
 
 }  // namespace
 
-hipError_t launch_wy(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s) {
+hipError_t launch_wy(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s,
+                     const PendArgs* pend) {
     if (desc.plan.max_depth > kStack + 1) return hipErrorNotSupported;
-    if (desc.plan.total_nodes == 0) return hipSuccess;
     // path-stack registers: depths 0..7 suffice when no path is longer than 9 nodes
-    return desc.plan.max_depth <= 9 ? launch_wy_d<8>(d, desc, a, s) : launch_wy_d<16>(d, desc, a, s);
+    const bool d8 = desc.plan.max_depth <= 9;
+    if (!pend) {
+        if (desc.plan.total_nodes == 0) return hipSuccess;
+        const PendParams none{};
+        return d8 ? launch_wy_d<8, false>(d, desc, a, s, none) : launch_wy_d<16, false>(d, desc, a, s, none);
+    }
+    if (d.n_req == 0) return hipSuccess;  // requests without nodes are still published
+    const lumo_plan& pl = pend->desc->plan;
+    PendParams pp;
+    pp.blob = pend->desc->blob;
+    pp.o_node_off = pl.o_node_off;
+    pp.o_row = pl.o_row;
+    pp.total_rows = pl.total_rows;
+    pp.max_path = pend->max_path;
+    pp.path_out = pend->path_out;
+    pp.path_len = pend->path_len;
+    pp.k = static_cast<const uint16_t*>(pend->k);
+    pp.v = static_cast<const uint16_t*>(pend->v);
+    pp.g = pend->g;
+    pp.beta = pend->beta;
+    pp.state = pend->state;
+    return d8 ? launch_wy_d<8, true>(d, desc, a, s, pp) : launch_wy_d<16, true>(d, desc, a, s, pp);
 }
 
 }  // namespace lumo

@@ -11,7 +11,8 @@ import numpy as np
 import torch
 
 from . import (LUMO_BF16, LumoError, TreeDesc, dims, lumo_gdn_commit, lumo_gdn_commit_graph_create,
-               lumo_tree_conv_gather, lumo_tree_gdn_verify, lumo_tree_gdn_workspace_bytes)
+               lumo_tree_conv_gather, lumo_tree_gdn_verify, lumo_tree_gdn_verify_pending,
+               lumo_tree_gdn_workspace_bytes)
 
 
 def to_device(a: np.ndarray, device="cuda", bf16=False) -> torch.Tensor:
@@ -79,11 +80,22 @@ class GdnTreeStep:
                              self.t["g"], self.t["beta"], self.state if state0 is None else state0,
                              self.o, self.node_states, self.ws, 0, stream)
 
-    def commit(self, stream=None, with_conv=True):
+    def verify_pending(self, prev: "GdnTreeStep", stream=None, state=None):
+        """Publish prev's accepted path (written by prev.commit(defer=True)) into the
+        state bank and verify this step's tree from it, in one launch. The state bank is
+        self.state unless given."""
+        lumo_tree_gdn_verify_pending(self.dims, self.desc, self.t["q"], self.t["k"], self.t["v"],
+                                     self.t["g"], self.t["beta"],
+                                     self.state if state is None else state, self.o, prev.desc,
+                                     prev.max_path, prev.path_out, prev.path_len, prev.t["k"],
+                                     prev.t["v"], prev.t["g"], prev.t["beta"], stream)
+
+    def commit(self, stream=None, with_conv=True, defer=False):
+        """Accepted path, conv history and (unless defer) the replay into self.state."""
         use_conv = with_conv and self.has_conv
         lumo_gdn_commit(self.dims, self.desc, self.max_path, self.accepted, self.path_out,
                         self.path_len, self.t["k"], self.t["v"], self.t["g"], self.t["beta"],
-                        self.state, self.channels if use_conv else 0,
+                        None if defer else self.state, self.channels if use_conv else 0,
                         self.x if use_conv else None, self.hist if use_conv else None, stream)
 
     def commit_graph(self, with_conv=True):

@@ -181,3 +181,35 @@ def test_wy_needs_no_workspace():
                                   L.LUMO_POLICY_WY)
     d = _dims(h_k=2, h_v=4, d_k=128, d_v=128, op_dtype=1, n_layers=3)
     assert L.lumo_tree_gdn_workspace_bytes(d, plan) == 0
+
+
+def _pending(d, desc, pdesc, max_path=4, state=FAKE, pend_desc=True):
+    P = ctypes.c_void_p
+    return L._lib.lumo_tree_gdn_verify_pending(
+        ctypes.byref(d), ctypes.byref(desc), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+        P(state) if state else None, P(FAKE), ctypes.byref(pdesc) if pend_desc else None,
+        max_path, P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), None)
+
+
+def test_verify_pending_rejects_bad_arguments():
+    dw = _dims(h_k=2, h_v=4, d_k=128, d_v=128, op_dtype=1)
+    wy, _b1 = _desc(policy=L.LUMO_POLICY_WY)
+    paths, _b2 = _desc(policy=L.LUMO_POLICY_PATHS)
+    two, _b3 = _desc(n_req=2)
+    assert _pending(dw, paths, paths) == L.LUMO_EUNSUPPORTED      # needs a WY plan
+    assert _pending(_dims(), wy, paths) == L.LUMO_EUNSUPPORTED    # fp32, d = 16
+    assert _pending(dw, wy, paths, max_path=0) == L.LUMO_EINVAL
+    assert _pending(dw, wy, paths, max_path=5000) == L.LUMO_EINVAL
+    assert _pending(dw, wy, two) == L.LUMO_EDESC                  # request counts differ
+    assert _pending(dw, wy, paths, pend_desc=False) == L.LUMO_EINVAL
+    assert _pending(dw, wy, paths, state=0) == L.LUMO_EINVAL
+    assert "state" in L.lumo_last_error()
+    assert _pending(dw, wy, paths, state=FAKE + 4) == L.LUMO_EINVAL
+
+
+def test_verify_pending_empty_batch_is_a_no_op():
+    plan, blob = L.lumo_tree_plan(np.array([0], np.int32), np.zeros(0, np.int32),
+                                  np.zeros(0, np.int32), L.LUMO_POLICY_WY)
+    desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
+    d = _dims(n_req=0, h_k=1, h_v=1, d_k=128, d_v=128, op_dtype=1)
+    assert _pending(d, desc, desc) == L.LUMO_OK

@@ -394,3 +394,139 @@ def test_wy_deep_chain_and_ragged_requests():
     st = run(wl, L.LUMO_POLICY_WY, with_conv=False, commit=False)
     inst = [(r, l, h) for r in range(4) for l in range(2) for h in (0, 3, 7)]
     gu.check_outputs(wl, gu.to_np(st.o), inst)
+
+
+# ---------------------------------------------------------------- deferred publication
+
+def _pending_pair(h_k, h_v, seed=31):
+    """Two iterations over the same 5 requests: a chain of 20 accepted whole (two staging
+    rounds), a short path into a request with no nodes next time, an empty and an
+    invalid pending path, and a random tree of two chunks."""
+    rng = np.random.default_rng(seed)
+    prev_par = [trees.chain(20), np.array([-1, 0, 0, 1], np.int32), np.array([-1], np.int32),
+                trees.FIG1_PARENT, trees.random_tree(rng, 40, 8, trees.bmax_uniform(3))]
+    cur_par = [trees.random_tree(rng, 30, 8, trees.bmax_uniform(3)), np.zeros(0, np.int32),
+               trees.chain(5), np.zeros(0, np.int32),
+               trees.random_tree(rng, 50, 9, trees.bmax_uniform(4))]
+    prev = pins.make_wl(prev_par, d_k=128, d_v=128, h_k=h_k, h_v=h_v, op_dtype=ops.BF16,
+                        n_rows=[20, 5, 1, 9, 40], n_layers=2, max_path=24)
+    prev.arrays = ops.make_gdn_operands(seed, n_req=5, n_layers=2, total_rows=prev.total_rows,
+                                        h_k=h_k, h_v=h_v, d_k=128, d_v=128, op_dtype=ops.BF16)
+    deep = int(np.argmax(trees.depths(prev_par[4])))
+    prev.accepted = np.array([19, 3, -1, 99, deep], np.int32)
+    cur = pins.make_wl(cur_par, d_k=128, d_v=128, h_k=h_k, h_v=h_v, op_dtype=ops.BF16,
+                       n_rows=[31, 2, 5, 0, 50], n_layers=2, max_path=16)
+    cur.arrays = ops.make_gdn_operands(seed + 1, n_req=5, n_layers=2, total_rows=cur.total_rows,
+                                       h_k=h_k, h_v=h_v, d_k=128, d_v=128, op_dtype=ops.BF16)
+    return prev, cur
+
+
+def _step(wl, policy, with_conv=False):
+    a = {k: v for k, v in wl.arrays.items() if with_conv or k not in ("x", "hist", "w")}
+    return GdnTreeStep(n_req=wl.n_req, n_layers=wl.n_layers, h_k=wl.h_k, h_v=wl.h_v, d_k=wl.d_k,
+                       d_v=wl.d_v, op_dtype=wl.op_dtype, node_off=wl.node_off,
+                       parent=wl.parent_flat, n_rows=wl.n_rows, arrays=a, policy=policy,
+                       max_path=wl.max_path, accepted=wl.accepted,
+                       channels=wl.channels if with_conv else 0)
+
+
+@pytest.mark.parametrize("h_k,h_v", [(2, 4), (4, 4)])
+def test_verify_pending_parity(h_k, h_v):
+    """Published state = the oracle's commit of the previous iteration; outputs = the
+    oracle's verification from that state; untouched requests stay bitwise."""
+    prev, cur = _pending_pair(h_k, h_v)
+    say(f"[gpu] verify_pending h_k={h_k} h_v={h_v}")
+    sp = _step(prev, L.LUMO_POLICY_PATHS)
+    sp.commit(defer=True)
+    torch.cuda.synchronize()
+    # the oracle refuses the invalid path of request 3; an invalid path publishes nothing,
+    # as an empty one does, and reports length -1
+    acc = prev.accepted.copy()
+    acc[3] = -1
+    ref_state, po, pl = oracle.commit(prev, accepted=acc)
+    pl[3] = -1
+    assert np.array_equal(sp.path_len.cpu().numpy(), pl)
+    assert np.array_equal(sp.path_out.cpu().numpy(), po)
+    assert torch.equal(sp.state, sp.state0)  # the deferred commit did not replay
+    sc = _step(cur, L.LUMO_POLICY_WY)
+    sc.verify_pending(sp, state=sp.state)
+    torch.cuda.synchronize()
+    st = sp.state.cpu().numpy()
+    s0 = sp.state0.cpu().numpy()
+    inst = [(r, l, h) for r in range(5) for l in range(2) for h in range(h_v)]
+    for (r, l, h) in inst:
+        if pl[r] <= 0:
+            assert np.array_equal(st[r, l, h], s0[r, l, h]), (r, l, h)
+    worst = gu.check_states(prev, st, ref_state, inst)
+    say(f"  published state worst max-rel {worst:.3e}")
+    a2 = dict(cur.arrays)
+    a2["state0"] = ref_state.astype(np.float32)
+    live = [(r, l, h) for (r, l, h) in inst if len(cur.parents[r]) > 0]
+    worst = gu.check_outputs(cur, gu.to_np(sc.o), live, arrays=a2)
+    say(f"  outputs worst max-rel {worst:.3e}")
+
+
+def test_verify_pending_without_pending_is_plain_verify():
+    """No pending path anywhere: bitwise the plain WY verification, state untouched."""
+    wl = workload("layer1")
+    s1 = run(wl, L.LUMO_POLICY_WY, with_conv=False, commit=False)
+    s2 = _step(wl, L.LUMO_POLICY_WY)
+    s2.accepted.fill_(-1)
+    s2.commit(defer=True)
+    s2.verify_pending(s2)
+    torch.cuda.synchronize()
+    assert int(s2.path_len.cpu()[0]) == 0
+    assert torch.equal(s1.o, s2.o)
+    assert torch.equal(s2.state, s2.state0)
+
+
+def test_verify_pending_full_size_sampled():
+    """The batched workload, its accepted paths deferred into the next verification."""
+    wl = workload("batched")
+    say("[gpu] verify_pending batched")
+    st = GdnTreeStep.from_workload(wl, policy=L.LUMO_POLICY_WY, with_conv=False)
+    st.commit(defer=True)
+    st.verify_pending(st)
+    torch.cuda.synchronize()
+    ref_state, _, pl = oracle.commit(wl)
+    assert np.array_equal(st.path_len.cpu().numpy(), pl)
+    inst = gu.sample_instances(wl, 24, seed=21)
+    gu.check_states(wl, st.state.cpu().numpy(), ref_state, inst)
+    a2 = dict(wl.arrays)
+    a2["state0"] = ref_state.astype(np.float32)
+    gu.check_outputs(wl, gu.to_np(st.o), inst, arrays=a2)
+
+
+def test_deferred_loop_matches_eager_loop():
+    """Three iterations: deferred publication + final flush agrees with eager commits
+    (states to fp32 rounding, outputs to bf16 rounding) and with the oracle chain."""
+    wls = [configs.build("layer1", seed=s, with_conv=False) for s in (101, 102, 103)]
+    eager = [_step(w, L.LUMO_POLICY_WY) for w in wls]
+    dfr = [_step(w, L.LUMO_POLICY_WY) for w in wls]
+    bank_e = eager[0].state
+    bank_d = dfr[0].state
+    for i in range(3):
+        eager[i].verify(state0=bank_e)
+        lumo_commit_into(eager[i], bank_e)
+        if i == 0:
+            dfr[0].verify(state0=bank_d)
+        else:
+            dfr[i].verify_pending(dfr[i - 1], state=bank_d)
+        dfr[i].commit(defer=True)
+    lumo_commit_into(dfr[2], bank_d)  # flush the last pending path
+    torch.cuda.synchronize()
+    for i in range(3):
+        a, b = gu.to_np(eager[i].o), gu.to_np(dfr[i].o)
+        rows = oracle.plan.flat_rows(wls[i].parents, wls[i].row_off)
+        assert gu.max_rel(b[:, rows], a[:, rows]) <= 2 ** -7, i
+    ref = wls[0].arrays["state0"]
+    for w in wls:
+        ref, _, _ = oracle.commit(w, state_in=ref.astype(np.float32))
+    inst = gu.sample_instances(wls[0], 16, seed=4)
+    gu.check_states(wls[0], bank_d.cpu().numpy(), ref, inst)
+    gu.check_states(wls[0], bank_e.cpu().numpy(), ref, inst)
+
+
+def lumo_commit_into(st, bank):
+    L.lumo_gdn_commit(st.dims, st.desc, st.max_path, st.accepted, st.path_out, st.path_len,
+                      st.t["k"], st.t["v"], st.t["g"], st.t["beta"], bank)
