@@ -74,6 +74,8 @@ def paths(parent) -> list:
 
 
 def spine(parent) -> list:
+    if len(parent) == 0:  # a request without nodes has an empty spine
+        return []
     ch = children(parent)
     s = [0]
     while ch[s[-1]]:

@@ -141,6 +141,142 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
     }
 }
 
+// Depth-first variant (bf16, paths of at most 16 nodes). One block walks one request's
+// tree in preorder for one layer and 2048 channels; each thread keeps, for its 8
+// channels, the x entries of the current root path (after the three history entries)
+// in registers, so every x row is read from memory exactly once. A node at depth d has
+// the window (ext[d], ext[d+1], ext[d+2], x_node) with ext = (history, path by depth);
+// taps, accumulation order, activation and cast are those of conv_kernel.
+constexpr int kDfsWin = 512;  // preorder positions staged in LDS at a time
+constexpr int kDfsGroup = 4;  // nodes whose rows are loaded one group ahead
+
+struct ConvDfsParams {
+    const int32_t* blob;
+    int32_t o_node_off, o_pre_row, o_pre_depth;
+    int32_t n_req, total_rows, n_layers, channels, n_cchunks, act;
+    const uint16_t* x;
+    const uint16_t* hist;
+    const float* w;
+    const float* bias;
+    uint16_t* y;
+};
+
+__device__ __forceinline__ void dfs_pin(uint4& a) {
+    asm volatile("" : "+v"(a.x), "+v"(a.y), "+v"(a.z), "+v"(a.w));
+}
+
+// The window's three older entries for a node at depth d (< DD), and the node's own
+// entry recorded at depth d: a chain of uniform branches to static register indices.
+// The empty asm statements keep the compiler from merging the branches into one
+// indexed access, which would move the array to scratch memory.
+template <int DD, int D = 0>
+__device__ __forceinline__ void dfs_taps(int d, uint4 (&ext)[DD + 3], const uint4 xt, uint4& t0, uint4& t1,
+                                         uint4& t2) {
+    if constexpr (D + 1 < DD) {
+        if (d != D) {
+            dfs_taps<DD, D + 1>(d, ext, xt, t0, t1, t2);
+            return;
+        }
+    }
+    t0 = ext[D];
+    t1 = ext[D + 1];
+    t2 = ext[D + 2];
+    ext[3 + D] = xt;
+    dfs_pin(t0);
+    dfs_pin(t1);
+    dfs_pin(t2);
+    asm volatile("" ::"n"(D) : "memory");
+}
+
+template <int DD>
+__global__ __launch_bounds__(256) void conv_dfs_kernel(ConvDfsParams p) {
+    int t = xcd_remap(blockIdx.x, gridDim.x);
+    const int cc = t % p.n_cchunks;
+    t /= p.n_cchunks;
+    const int r = t % p.n_req;
+    const int l = t / p.n_req;
+    const int base = p.blob[p.o_node_off + r];
+    const int N = p.blob[p.o_node_off + r + 1] - base;
+    if (N <= 0) return;  // uniform over the block
+    const int tid = (int)threadIdx.x;
+    const int c0ch = (cc * 256 + tid) * 8;
+    const bool has_c = c0ch < p.channels;
+    const int c = has_c ? c0ch : p.channels - 8;
+    float wt[32];
+    const float4* wp = reinterpret_cast<const float4*>(p.w + ((long)l * p.channels + c) * 4);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float4 q = wp[e];
+        wt[4 * e] = q.x; wt[4 * e + 1] = q.y; wt[4 * e + 2] = q.z; wt[4 * e + 3] = q.w;
+    }
+    float b0[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) b0[e] = p.bias ? p.bias[(long)l * p.channels + c + e] : 0.f;
+    uint4 ext[DD + 3];
+    const uint16_t* hr = p.hist + ((long)r * p.n_layers + l) * 3 * p.channels + c;
+#pragma unroll
+    for (int e = 0; e < 3; ++e) ext[e] = *reinterpret_cast<const uint4*>(hr + (long)e * p.channels);
+#pragma unroll
+    for (int e = 3; e < DD + 3; ++e) ext[e] = make_uint4(0, 0, 0, 0);  // written before read in preorder
+    const uint16_t* xl = p.x + (long)l * p.total_rows * p.channels + c;
+    uint16_t* yl = p.y + (long)l * p.total_rows * p.channels + c;
+    const int32_t* prow = p.blob + p.o_pre_row + base;
+    const int32_t* pdep = p.blob + p.o_pre_depth + base;
+    __shared__ int2 info[kDfsWin];  // (row, depth) of preorder positions w0 ..
+    for (int w0 = 0; w0 < N; w0 += kDfsWin) {
+        const int nw = min(kDfsWin, N - w0);
+        __syncthreads();  // the previous window's entries have been read
+        for (int i = tid; i < nw; i += 256) info[i] = make_int2(prow[w0 + i], pdep[w0 + i]);
+        __syncthreads();
+        uint4 buf[2][kDfsGroup];
+        auto issue = [&](int g, uint4 (&b)[kDfsGroup]) __attribute__((always_inline)) {
+#pragma unroll
+            for (int i = 0; i < kDfsGroup; ++i) {
+                const int row = __builtin_amdgcn_readfirstlane(info[min(g * kDfsGroup + i, nw - 1)].x);
+                b[i] = *reinterpret_cast<const uint4*>(xl + (long)row * p.channels);
+            }
+        };
+        auto compute = [&](int g, const uint4 (&b)[kDfsGroup]) __attribute__((always_inline)) {
+#pragma unroll
+            for (int i = 0; i < kDfsGroup; ++i) {
+                const int j = g * kDfsGroup + i;
+                if (j >= nw) break;  // uniform
+                const int2 in = info[j];
+                const int row = __builtin_amdgcn_readfirstlane(in.x);
+                const int d = __builtin_amdgcn_readfirstlane(in.y);
+                uint4 tp[4];
+                dfs_taps<DD>(d, ext, b[i], tp[0], tp[1], tp[2]);
+                tp[3] = b[i];
+                float acc[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[e] = b0[e];
+#pragma unroll
+                for (int tap = 0; tap < 4; ++tap) {
+                    float xv[8];
+                    Vec8<1>::unpack(tp[tap], xv);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[e] = __builtin_fmaf(wt[4 * e + tap], xv[e], acc[e]);
+                }
+                if (p.act == 1) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[e] = acc[e] * __builtin_amdgcn_rcpf(1.f + __expf(-acc[e]));
+                }
+                if (has_c) Vec8<1>::st(yl + (long)row * p.channels, acc);
+            }
+        };
+        const int ng = (nw + kDfsGroup - 1) / kDfsGroup;
+        issue(0, buf[0]);
+        for (int g = 0; g < ng; g += 2) {
+            if (g + 1 < ng) issue(g + 1, buf[1]);
+            compute(g, buf[0]);
+            if (g + 1 < ng) {
+                if (g + 2 < ng) issue(g + 2, buf[0]);
+                compute(g + 1, buf[1]);
+            }
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const ConvArgs& a, hipStream_t s) {
@@ -162,6 +298,30 @@ hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.w = a.w;
     p.bias = a.bias;
     p.y = a.y;
+    if (d.op_dtype == LUMO_BF16 && pl.max_depth <= 16) {
+        ConvDfsParams q;
+        q.blob = desc.blob;
+        q.o_node_off = pl.o_node_off;
+        q.o_pre_row = pl.o_pre_row;
+        q.o_pre_depth = pl.o_pre_depth;
+        q.n_req = d.n_req;
+        q.total_rows = pl.total_rows;
+        q.n_layers = d.n_layers;
+        q.channels = a.channels;
+        q.n_cchunks = p.n_cchunks;
+        q.act = a.act;
+        q.x = static_cast<const uint16_t*>(a.x);
+        q.hist = static_cast<const uint16_t*>(a.hist);
+        q.w = a.w;
+        q.bias = a.bias;
+        q.y = static_cast<uint16_t*>(a.y);
+        const long nb = (long)d.n_layers * d.n_req * q.n_cchunks;
+        if (pl.max_depth <= 8)
+            hipLaunchKernelGGL(conv_dfs_kernel<8>, dim3((unsigned)nb), dim3(256), 0, s, q);
+        else
+            hipLaunchKernelGGL(conv_dfs_kernel<16>, dim3((unsigned)nb), dim3(256), 0, s, q);
+        return hipGetLastError();
+    }
     const long blocks = (long)d.n_layers * p.n_cchunks * ((pl.total_nodes + kNodesPerBlock - 1) / kNodesPerBlock);
     if (d.op_dtype == LUMO_BF16)
         hipLaunchKernelGGL(conv_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, s, p);

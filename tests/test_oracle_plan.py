@@ -70,3 +70,12 @@ def test_paper_geometry():
 def test_validate_rejects(bad):
     with pytest.raises(ValueError):
         plan.validate(bad)
+
+
+def test_request_without_nodes():
+    """An empty request contributes no rows and no sources; its neighbours keep theirs."""
+    empty = np.zeros(0, np.int32)
+    assert plan.spine(empty) == [] and plan.slot_map(empty) == []
+    rows = plan.flat_rows([np.array([-1, 0], np.int32), empty, np.array([-1], np.int32)],
+                          np.array([0, 2, 2], np.int32))
+    assert rows.tolist() == [0, 1, 2]
