@@ -68,16 +68,23 @@ def recorded_traffic(policy, config, commit="eager"):
 
 
 def copy_probe():
-    """A plain device copy of known size (1 GiB read + 1 GiB written, three times)."""
+    """A plain device copy of known size (1 GiB read + 1 GiB written, three times): the
+    calibration of the HBM byte counters, and the practical read+write rate."""
     import torch
     n = 256 * 1024 * 1024
     a = torch.ones(n, device="cuda")
     b = torch.empty_like(a)
     torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
     for _ in range(3):
         b.copy_(a)
+    e1.record()
     torch.cuda.synchronize()
-    print(json.dumps({"copy_probe_bytes": n * 4, "copies": 3}), flush=True)
+    ms = e0.elapsed_time(e1) / 3
+    print(json.dumps({"copy_probe_bytes": n * 4, "copies": 3, "ms_per_copy": round(ms, 4),
+                      "read_plus_write_GBps": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}), flush=True)
 
 WORKLOAD_TEXT = {
     "tiny": "Fig. 1 tree, 1 request, 1 head, d=16, fp32 operands",

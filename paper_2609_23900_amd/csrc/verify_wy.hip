@@ -32,6 +32,12 @@
 //             (the preorder path stack is exactly the ancestry).
 // This replaces sequential scans; the arithmetic differs from them in rounding only
 // (tolerance-level, not bitwise). The commit stays a sequential replay.
+//
+// Deferred publication (PEND): before the slab is split, each wave replays the previous
+// iteration's accepted path on it with the sequential update (Eq. (2)-(3), one path
+// node at a time, in fp32), stores it back to the state bank, and verifies from it. The
+// state is then read once and written once per iteration; the publication of Alg. 1
+// still precedes the verification that depends on it, per state tile.
 #include "device_common.h"
 #include "internal.h"
 #include "launch.h"
