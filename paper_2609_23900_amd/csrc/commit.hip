@@ -1,14 +1,16 @@
 // Accepted-path publication (LumoTree Alg. 1 publication, Alg. 2 replay, Sec. V-A).
 //
-// Three fixed-shape launches, all driven by device data only (no host path list):
-//   1. path kernel    accepted node -> root-first path and its length (bit-exact)
+// Fixed-shape launches, all driven by device data only (no host path list):
+//   1. path + history kernel  accepted node -> root-first path and its length
+//                     (bit-exact); conv history <- last three of (history, x rows of
+//                     the path). Without conv operands, the path kernel alone.
 //   2. replay kernel  one wavefront per (request, layer, value head, value tile):
 //                     load the pre-tree state tile, apply the recorded updates of the
 //                     path with the same row update the verifier uses, store in place;
 //                     before the loop the path's first key rows are copied to LDS
 //                     (direct global-to-LDS loads, in flight with the state load) and
-//                     its rows, decays, betas and value entries are fetched into lanes
-//   3. history kernel conv history <- last three of (history, x rows of the path)
+//                     its rows, decays, betas and value entries are fetched into lanes.
+//                     Skipped when the state is NULL (publication deferred).
 // Empty or invalid paths leave the state and the history untouched.
 #include "device_common.h"
 #include "internal.h"
@@ -203,39 +205,65 @@ __global__ __launch_bounds__(64, 2) void replay_kernel(ReplayParams p, const typ
 struct HistParams {
     const int32_t* blob;
     int32_t o_node_off, o_row;
-    const int32_t* path_out;
-    const int32_t* path_len;
-    int32_t max_path, n_layers, total_rows, channels, n_cchunks;
+    int32_t n_layers, total_rows, channels, n_cchunks;
     const void* x;
     void* hist;
 };
 
-// 8 channels per thread: 16 bytes of bf16, 32 bytes of fp32.
+// Path derivation and conv-history publication in one launch (with conv operands).
+// Every block of request r derives r's path length with the path kernel's rule; the
+// block (r, layer 0, channel chunk 0) also writes path_out and path_len. The history
+// needs only the path's last three nodes: the accepted node and its two nearest
+// ancestors, read straight from the parent table.
 template <int OPT>
-__global__ __launch_bounds__(256) void hist_kernel(HistParams p) {
+__global__ __launch_bounds__(256) void path_hist_kernel(PathParams pp, HistParams p) {
     using T = typename Op<OPT>::T;
     const int cc = blockIdx.x % p.n_cchunks;
     const int l = (blockIdx.x / p.n_cchunks) % p.n_layers;
     const int r = blockIdx.x / (p.n_cchunks * p.n_layers);
-    const int len = p.path_len[r];
+    const int base = p.blob[p.o_node_off + r];
+    const int n = p.blob[p.o_node_off + r + 1] - base;
+    const int a = pp.accepted[r];
+    int len;
+    if (a < -1 || a >= n) {
+        len = -1;
+    } else if (a == -1) {
+        len = 0;
+    } else {
+        len = pp.blob[pp.o_depth + base + a] + 1;
+        if (len > pp.max_path) len = -1;
+    }
+    if (l == 0 && cc == 0 && threadIdx.x < 64) {
+        int32_t* po = pp.path_out + (long)r * pp.max_path;
+        for (int i = (int)threadIdx.x; i < pp.max_path; i += 64)
+            if (i >= len) po[i] = -1;
+        if (threadIdx.x == 0) {
+            int x = a;
+            for (int i = len - 1; i >= 0; --i) {  // len <= depth + 1: the walk ends at the root
+                po[i] = x;
+                x = pp.blob[pp.o_parent + base + x];
+            }
+            pp.path_len[r] = len;
+        }
+    }
     if (len <= 0) return;
     const int c = (cc * 256 + (int)threadIdx.x) * 8;
     if (c >= p.channels) return;
-    const int base = p.blob[p.o_node_off + r];
     T* hist = static_cast<T*>(p.hist) + (((long)r * p.n_layers + l) * 3) * p.channels;
     const T* x = static_cast<const T*>(p.x);
+    // entry e of the new history is entry len + e of (history, x rows of the path); for
+    // len + e >= 3 that is path node len + e - 3, the (2 - e)-th ancestor of the accepted node
+    int node[3];
+    node[2] = a;
+    node[1] = len >= 2 ? pp.blob[pp.o_parent + base + a] : -1;
+    node[0] = len >= 3 ? pp.blob[pp.o_parent + base + node[1]] : -1;
     constexpr int W = 16 / sizeof(T) >= 8 ? 1 : 2;  // uint4 loads per 8 channels
     uint4 val[3][W];
 #pragma unroll
     for (int e = 0; e < 3; ++e) {
-        const int pos = len + e;  // entry e of the last three of (3 + len) entries
-        const T* src;
-        if (pos < 3) {
-            src = hist + (long)pos * p.channels + c;
-        } else {
-            const int row = p.blob[p.o_row + base + p.path_out[(long)r * p.max_path + pos - 3]];
-            src = x + ((long)l * p.total_rows + row) * p.channels + c;
-        }
+        const int pos = len + e;
+        const T* src = pos < 3 ? hist + (long)pos * p.channels + c
+                               : x + ((long)l * p.total_rows + p.blob[p.o_row + base + node[e]]) * p.channels + c;
 #pragma unroll
         for (int w = 0; w < W; ++w) val[e][w] = reinterpret_cast<const uint4*>(src)[w];
     }
@@ -270,7 +298,26 @@ hipError_t launch_commit(const lumo_gdn_dims& d, const lumo_tree_desc& desc, con
     if (d.n_req == 0) return hipSuccess;
     PathParams pp{desc.blob, pl.o_node_off, pl.o_parent, pl.o_depth, d.n_req, a.max_path,
                   a.accepted, a.path_out, a.path_len};
-    hipLaunchKernelGGL(path_kernel, dim3((d.n_req + 255) / 256), dim3(256), 0, s, pp);
+    const bool conv = a.x && a.conv_hist;
+    if (conv) {  // path and history together (the replay only needs the path, written first)
+        HistParams hp;
+        hp.blob = desc.blob;
+        hp.o_node_off = pl.o_node_off;
+        hp.o_row = pl.o_row;
+        hp.n_layers = d.n_layers;
+        hp.total_rows = pl.total_rows;
+        hp.channels = a.channels;
+        hp.n_cchunks = (a.channels + 2047) / 2048;
+        hp.x = a.x;
+        hp.hist = a.conv_hist;
+        const long hb = (long)d.n_req * d.n_layers * hp.n_cchunks;
+        if (d.op_dtype == LUMO_BF16)
+            hipLaunchKernelGGL(path_hist_kernel<1>, dim3((unsigned)hb), dim3(256), 0, s, pp, hp);
+        else
+            hipLaunchKernelGGL(path_hist_kernel<0>, dim3((unsigned)hb), dim3(256), 0, s, pp, hp);
+    } else {
+        hipLaunchKernelGGL(path_kernel, dim3((d.n_req + 255) / 256), dim3(256), 0, s, pp);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
 
@@ -293,27 +340,6 @@ hipError_t launch_commit(const lumo_gdn_dims& d, const lumo_tree_desc& desc, con
     if (e != hipSuccess) return e;
     }
 
-    if (a.x && a.conv_hist) {
-        HistParams hp;
-        hp.blob = desc.blob;
-        hp.o_node_off = pl.o_node_off;
-        hp.o_row = pl.o_row;
-        hp.path_out = a.path_out;
-        hp.path_len = a.path_len;
-        hp.max_path = a.max_path;
-        hp.n_layers = d.n_layers;
-        hp.total_rows = pl.total_rows;
-        hp.channels = a.channels;
-        hp.n_cchunks = (a.channels + 2047) / 2048;
-        hp.x = a.x;
-        hp.hist = a.conv_hist;
-        const long hb = (long)d.n_req * d.n_layers * hp.n_cchunks;
-        if (d.op_dtype == LUMO_BF16)
-            hipLaunchKernelGGL(hist_kernel<1>, dim3((unsigned)hb), dim3(256), 0, s, hp);
-        else
-            hipLaunchKernelGGL(hist_kernel<0>, dim3((unsigned)hb), dim3(256), 0, s, hp);
-        e = hipGetLastError();
-    }
     return e;
 }
 
