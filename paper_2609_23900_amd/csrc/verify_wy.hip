@@ -258,20 +258,27 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         }
     };
 
-    // R0 columns j0 + 16 ct + lane%16 (ct = 0..3) as B fragments of the 16x16x32 MFMA:
-    // key block kb holds keys 32 kb + 8 (lane/16) + e.
+    // R0 as B fragments of the 16x16x32 MFMA: column n = lane%16 of tile ct is state
+    // column j0 + 4 n + ct, and key block kb holds keys 32 kb + 8 (lane/16) + e. A lane
+    // thus holds 4 adjacent columns of each of its keys: one 16-byte load (and store)
+    // per key. After the lane exchange of the products, lane l serves state column
+    // j0 + 4 (l % 16) + l / 16.
     const float* S = state0 + (((long)r * p.n_layers + l) * p.h_v + h) * (long)(kD * kD);
-    const float* Sl = S + (long)(8 * (lane / 16)) * kD + j0 + lane % 16;
+    const float* Sl = S + (long)(8 * (lane / 16)) * kD + j0 + 4 * (lane % 16);
     uint32_t raw[4][kD / 32][8];
-    auto slab_load = [&](int ct) {
+    auto slab_load = [&](int kb) {
 #pragma unroll
-        for (int kb = 0; kb < kD / 32; ++kb)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) raw[ct][kb][e] = __float_as_uint(Sl[(long)(32 * kb + e) * kD + 16 * ct]);
+        for (int e = 0; e < 8; ++e) {
+            const uint4 w = *reinterpret_cast<const uint4*>(Sl + (long)(32 * kb + e) * kD);
+            raw[0][kb][e] = w.x;
+            raw[1][kb][e] = w.y;
+            raw[2][kb][e] = w.z;
+            raw[3][kb][e] = w.w;
+        }
     };
     // The chunk's rows are loaded first and half the state slab behind them, so that the
-    // row-dependent copies below wait for the rows only (at most 63 loads issued after
-    // them) while the slab is already in flight; then the other half.
+    // row-dependent copies below wait for the rows only (16 loads issued after them)
+    // while the slab is already in flight; then the other half.
     // Deferred publication: the pending path's key rows (block-shared, in the Gram's
     // space) and the wave's value entries (in its record space) are staged kPend entries
     // at a time; lane e holds entry e's decay and beta. Each entry applies
@@ -344,7 +351,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                             acc = __builtin_fmaf(__uint_as_float(raw[ct][kb][e8]), kf[kb][e8], acc);
                         }
                     const float u = row_group_sum(s0 + s1);
-                    const float vj = bf16_lo((uint32_t)vsh[e * 64 + 16 * ct + lane % 16]);
+                    const float vj = bf16_lo((uint32_t)vsh[e * 64 + 4 * (lane % 16) + ct]);
                     dl[ct] = be * __builtin_fmaf(-ae, u, vj);
                 }
 #pragma unroll
@@ -358,13 +365,13 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
             }
         }
         float* Sw = pd.state + (((long)r * p.n_layers + l) * p.h_v + h) * (long)(kD * kD) +
-                    (long)(8 * (lane / 16)) * kD + j0 + lane % 16;
+                    (long)(8 * (lane / 16)) * kD + j0 + 4 * (lane % 16);
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct)
+        for (int kb = 0; kb < kD / 32; ++kb)
 #pragma unroll
-            for (int kb = 0; kb < kD / 32; ++kb)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) Sw[(long)(32 * kb + e) * kD + 16 * ct] = __uint_as_float(raw[ct][kb][e]);
+            for (int e = 0; e < 8; ++e)
+                *reinterpret_cast<uint4*>(Sw + (long)(32 * kb + e) * kD) =
+                    make_uint4(raw[0][kb][e], raw[1][kb][e], raw[2][kb][e], raw[3][kb][e]);
     };
 
     Rows rowC, rowA;  // this chunk, the next
@@ -383,7 +390,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     } else {
         if (N > 0) rowC = lane_rows(0);
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct) slab_load(ct);
+        for (int kb = 0; kb < kD / 32; ++kb) slab_load(kb);
         pend_publish();
         if (N <= 0) return;  // uniform: nothing to verify for this request
         v_issue(rowC, vbufs[wave][0]);
@@ -485,6 +492,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         asm volatile("" : "+v"(ln));
         tn = ln % kTile;
         const int kb0 = ln / kTile;  // key block offset within a 16-key step (32x32x16 Gram)
+        const int pc = 4 * (ln % 16) + ln / 16;  // this lane's state column (after the exchange)
         const int arow = mt == 0 ? tn : 2 * kTile + (tn & (kStack - 1));
         if (c0 > 0) flush(vbufs[wave][buf ^ 1], kTile);  // the previous chunk had two halves
         if (more) {
@@ -594,7 +602,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                 const int n = 16 * hf + i;
                 NodeRec cur;
                 load_rec(n, cur);
-                const float vj = __uint_as_float(((uint32_t)vs[n * 64 + ln]) << 16);
+                const float vj = __uint_as_float(((uint32_t)vs[n * 64 + pc]) << 16);
                 // sums over the path stack as even/odd partial sums (half the dependent chain)
                 float sa0 = 0.f, sa1 = 0.f, sb0 = 0.f, sb1 = 0.f;
 #pragma unroll
@@ -608,7 +616,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                 const float delta = __builtin_fmaf(cur.bn, u, -(sa0 + sa1));     // beta u - sum A delta
                 const float ov = __builtin_fmaf(cur.cn, delta, __builtin_fmaf(cur.gm, pq[i / 4][i % 4], sb0 + sb1));
                 dst[cur.d < D ? cur.d : D] = delta;  // uniform index: an indexed register write
-                vs[n * 64 + ln] = f32_to_bf16(ov);     // over the consumed value entry
+                vs[n * 64 + pc] = f32_to_bf16(ov);     // over the consumed value entry
             }
         };
         exchange(pk);
