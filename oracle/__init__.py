@@ -35,7 +35,24 @@ def build(force: bool = True) -> str:
 class Dims(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in (
         "n_req", "n_layers", "h_k", "h_v", "d_k", "d_v", "op_dtype", "total_rows",
-        "gate_is_alpha")]
+        "gate_is_alpha", "prep_flags")] + [
+        ("qk_eps", ctypes.c_double), ("a_log", ctypes.c_void_p), ("dt_bias", ctypes.c_void_p)]
+
+
+PREP_QK_NORM, PREP_RAW_GATES = 1, 2
+
+
+class Prep:
+    """Sec. IV-B operand preparation: flags (PREP_QK_NORM | PREP_RAW_GATES), the
+    normalisation constant, and the per-(layer, value head) gate parameters."""
+
+    def __init__(self, flags, eps=1e-6, a_log=None, dt_bias=None):
+        self.flags = int(flags)
+        self.eps = float(eps)
+        self.a_log = _c(a_log, np.float32)
+        self.dt_bias = _c(dt_bias, np.float32)
+        if self.flags & PREP_RAW_GATES and (self.a_log is None or self.dt_bias is None):
+            raise ValueError("raw gates need a_log and dt_bias")
 
 
 def use_library(path=None):
@@ -84,9 +101,14 @@ def _op(a, op_dtype):
     return np.ascontiguousarray(a, dtype=np.float32 if op_dtype == 0 else np.uint16)
 
 
-def dims(wl, gate_is_alpha=False) -> Dims:
+def dims(wl, gate_is_alpha=False, prep: Prep | None = None) -> Dims:
+    """The oracle's dimensions; `prep` must stay alive while the result is used."""
+    if prep is None:
+        return Dims(wl.n_req, wl.n_layers, wl.h_k, wl.h_v, wl.d_k, wl.d_v, wl.op_dtype,
+                    wl.total_rows, int(gate_is_alpha), 0, 0.0, None, None)
     return Dims(wl.n_req, wl.n_layers, wl.h_k, wl.h_v, wl.d_k, wl.d_v, wl.op_dtype,
-                wl.total_rows, int(gate_is_alpha))
+                wl.total_rows, int(gate_is_alpha), prep.flags, prep.eps, _p(prep.a_log),
+                _p(prep.dt_bias))
 
 
 class _Ops:
@@ -100,9 +122,10 @@ class _Ops:
         self.state0 = _c(a["state0"], np.float32)
 
 
-def verify_nodes(wl, r, l, h, targets, *, arrays=None, gate_is_alpha=False, want_state=False):
+def verify_nodes(wl, r, l, h, targets, *, arrays=None, gate_is_alpha=False, want_state=False,
+                 prep=None):
     """o (and state) of the given request-local nodes of instance (r, l, h), fp64."""
-    d = dims(wl, gate_is_alpha)
+    d = dims(wl, gate_is_alpha, prep)
     par = _c(wl.parents[r], np.int32)
     rows = _c(plan.rows_of(wl.parents[r], int(wl.row_off[r])), np.int32)
     tg = _c(targets, np.int32)
@@ -117,9 +140,9 @@ def verify_nodes(wl, r, l, h, targets, *, arrays=None, gate_is_alpha=False, want
     return (o, st) if want_state else o
 
 
-def verify_all(wl, *, arrays=None, gate_is_alpha=False, n_threads=None):
+def verify_all(wl, *, arrays=None, gate_is_alpha=False, n_threads=None, prep=None):
     """All outputs [layers][rows][h_v][d_v] in fp64 (pad rows NaN)."""
-    d = dims(wl, gate_is_alpha)
+    d = dims(wl, gate_is_alpha, prep)
     rows = plan.flat_rows(wl.parents, wl.row_off)
     o = np.full((wl.n_layers, wl.total_rows, wl.h_v, wl.d_v), np.nan, np.float64)
     x = _Ops(wl, arrays)
@@ -133,9 +156,9 @@ def verify_all(wl, *, arrays=None, gate_is_alpha=False, n_threads=None):
 
 
 def commit(wl, accepted=None, *, arrays=None, state_in=None, gate_is_alpha=False,
-           max_path=None, n_threads=None):
+           max_path=None, n_threads=None, prep=None):
     """(published state fp64, path_out int32, path_len int32)."""
-    d = dims(wl, gate_is_alpha)
+    d = dims(wl, gate_is_alpha, prep)
     a = wl.arrays if arrays is None else arrays
     acc = _c(wl.accepted if accepted is None else accepted, np.int32)
     mp = int(wl.max_path if max_path is None else max_path)

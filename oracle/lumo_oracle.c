@@ -23,9 +23,18 @@
  *     packed rows); the window is the last four entries, taps applied oldest to
  *     newest.
  *
+ *   - Sec. IV-B operand preparation (optional, prep_flags): verification takes raw
+ *     gate inputs and normalises queries and keys itself. With ORC_PREP_QK_NORM
+ *     every query and key row x is used as x / sqrt(|x|^2 + qk_eps); with
+ *     ORC_PREP_RAW_GATES the g and beta arrays hold raw inputs a and b and
+ *         alpha = exp(-exp(A_log[l][h]) * softplus(a + dt_bias[l][h])),
+ *         beta  = 1 / (1 + exp(-b)),
+ *     the Gated DeltaNet gate parametrisation. The replay uses the same prepared
+ *     operands.
+ *
  * Readings where the paper is silent (gate parametrisation alpha = exp(g), the
- * root is itself an updated node, tap order, SiLU activation, history length 3)
- * are listed in the design notes of the repository.
+ * root is itself an updated node, tap order, SiLU activation, history length 3,
+ * the normalisation constant) are listed in the design notes of the repository.
  *
  * Layouts (physical rows; row of a node = absolute row index):
  *   q, k [layers][rows][h_k][d_k]; v [layers][rows][h_v][d_v];
@@ -47,7 +56,36 @@ typedef struct {
     int op_dtype;      /* 0 = float32, 1 = bfloat16 bit patterns */
     int total_rows;
     int gate_is_alpha; /* 0: g holds log(alpha); 1: g holds alpha itself (exact hand tests) */
+    int prep_flags;    /* ORC_PREP_QK_NORM | ORC_PREP_RAW_GATES (Sec. IV-B), 0 = none */
+    double qk_eps;     /* ORC_PREP_QK_NORM: added to |x|^2 under the square root */
+    const float* a_log;   /* ORC_PREP_RAW_GATES: [layers][h_v] */
+    const float* dt_bias; /* ORC_PREP_RAW_GATES: [layers][h_v] */
 } orc_dims;
+
+enum { ORC_PREP_QK_NORM = 1, ORC_PREP_RAW_GATES = 2 };
+
+/* Sec. IV-B: a query or key row divided by the square root of (its squared norm + eps). */
+static void qk_prepare(const orc_dims* d, double* x, int n) {
+    if (!(d->prep_flags & ORC_PREP_QK_NORM)) return;
+    double ss = 0.0;
+    for (int i = 0; i < n; ++i) ss += x[i] * x[i];
+    const double scale = sqrt(ss + d->qk_eps);
+    for (int i = 0; i < n; ++i) x[i] /= scale;
+}
+
+/* Decay and write strength of one (node, value head) from its g and beta entries. */
+static void gates(const orc_dims* d, int l, int h, double g_in, double b_in, double* alpha, double* beta) {
+    if (d->prep_flags & ORC_PREP_RAW_GATES) {
+        const long lh = (long)l * d->h_v + h;
+        const double x = g_in + (double)d->dt_bias[lh];
+        const double softplus = (x > 0.0 ? x : 0.0) + log1p(exp(-fabs(x)));  /* log(1 + e^x) */
+        *alpha = exp(-exp((double)d->a_log[lh]) * softplus);
+        *beta = 1.0 / (1.0 + exp(-b_in));
+    } else {
+        *alpha = d->gate_is_alpha ? g_in : exp(g_in);
+        *beta = b_in;
+    }
+}
 
 /* Decode one operand element to double. bfloat16 is the upper half of a float32. */
 static double ld_op(const void* base, long idx, int dtype) {
@@ -95,9 +133,10 @@ static void gdn_node_update(const orc_dims* d, double* R, double* Rk, double* kv
     const long kb = (((long)l * d->total_rows + row) * d->h_k + hk) * dk;
     const long vb = (((long)l * d->total_rows + row) * d->h_v + h) * dv;
     const long gb = ((long)l * d->total_rows + row) * d->h_v + h;
-    const double a = d->gate_is_alpha ? (double)g[gb] : exp((double)g[gb]);
-    const double b = (double)beta[gb];
+    double a, b;
+    gates(d, l, h, (double)g[gb], (double)beta[gb], &a, &b);
     for (int i = 0; i < dk; ++i) kv[i] = ld_op(k, kb + i, d->op_dtype);
+    qk_prepare(d, kv, dk);
     for (int j = 0; j < dv; ++j) vv[j] = ld_op(v, vb + j, d->op_dtype);
     /* R' = alpha R */
     for (long e = 0; e < (long)dv * dk; ++e) R[e] *= a;
@@ -118,6 +157,7 @@ static void gdn_output(const orc_dims* d, const double* R, int l, int row, int h
     const int hk = h / (d->h_v / d->h_k);
     const long qb = (((long)l * d->total_rows + row) * d->h_k + hk) * dk;
     for (int i = 0; i < dk; ++i) qv[i] = ld_op(q, qb + i, d->op_dtype);
+    qk_prepare(d, qv, dk);
     for (int j = 0; j < dv; ++j) {
         double s = 0.0;
         for (int i = 0; i < dk; ++i) s += R[(long)j * dk + i] * qv[i];

@@ -441,4 +441,121 @@ def pin_conv_hist_publish():
         assert np.array_equal(out[0, 0], np.array(seq[-3:], np.float64))
 
 
+# --------------------------------------------------------------------------- operand preparation
+
+def _prep_params(rng, wl, eps):
+    a_log = (0.5 * rng.standard_normal((wl.n_layers, wl.h_v))).astype(np.float32)
+    dt_bias = rng.standard_normal((wl.n_layers, wl.h_v)).astype(np.float32)
+    return oracle.Prep(oracle.PREP_QK_NORM | oracle.PREP_RAW_GATES, eps, a_log, dt_bias)
+
+
+def _prepared_operands(wl, a, r, l, h, prep):
+    """Sec. IV-B preparation written out with numpy: x / sqrt(|x|^2 + eps) for q and k,
+    alpha = exp(-exp(A_log) log(1 + e^(a + dt_bias))), beta = 1 / (1 + e^-b)."""
+    rows = _rows(wl, r)
+    hk = h // (wl.h_v // wl.h_k)
+    n = len(wl.parents[r])
+    K = np.stack([a["k"][l, rows[i], hk].astype(np.float64) for i in range(n)])
+    Q = np.stack([a["q"][l, rows[i], hk].astype(np.float64) for i in range(n)])
+    V = np.stack([a["v"][l, rows[i], h].astype(np.float64) for i in range(n)])
+    if prep.flags & oracle.PREP_QK_NORM:
+        K = K / np.sqrt((K * K).sum(1, keepdims=True) + prep.eps)
+        Q = Q / np.sqrt((Q * Q).sum(1, keepdims=True) + prep.eps)
+    graw = np.array([float(a["g"][l, rows[i], h]) for i in range(n)])
+    braw = np.array([float(a["beta"][l, rows[i], h]) for i in range(n)])
+    x = graw + float(prep.dt_bias[l, h])
+    al = np.exp(-np.exp(np.float64(prep.a_log[l, h])) * np.logaddexp(0.0, x))
+    be = 1.0 / (1.0 + np.exp(-braw))
+    return list(al), list(be), K, Q, V
+
+
+def pin_prep_half_gates():
+    """a = -dt_bias, A_log = 0 and b = 0 give alpha = exp(-log 2) = 1/2 and beta = 1/2:
+    the prepared run equals the run with alpha = beta = 1/2 given directly."""
+    rng = np.random.default_rng(61)
+    wl = make_wl([trees.FIG1_PARENT], d_k=4, d_v=3, h_k=1, h_v=2, n_layers=2)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    dt = rng.standard_normal((2, 2)).astype(np.float32)
+    prep = oracle.Prep(oracle.PREP_RAW_GATES, 0.0, np.zeros((2, 2), np.float32), dt)
+    raw = dict(a)
+    raw["g"] = np.broadcast_to(-dt[:, None, :], a["g"].shape).astype(np.float32).copy()
+    raw["beta"] = np.zeros_like(a["beta"])
+    half = dict(a)
+    half["g"] = np.full_like(a["g"], 0.5)
+    half["beta"] = np.full_like(a["beta"], 0.5)
+    for (l, h) in [(0, 0), (1, 1)]:
+        o1, s1 = oracle.verify_nodes(wl, 0, l, h, list(range(7)), arrays=raw, prep=prep, want_state=True)
+        o2, s2 = oracle.verify_nodes(wl, 0, l, h, list(range(7)), arrays=half, gate_is_alpha=True,
+                                     want_state=True)
+        np.testing.assert_allclose(o1, o2, rtol=1e-14, atol=1e-15)
+        np.testing.assert_allclose(s1, s2, rtol=1e-14, atol=1e-15)
+
+
+def pin_prep_chain_equals_matrix_scan():
+    """Normalised q, k and raw gates on a chain: the matrix-form scan of the operands
+    prepared with numpy (eps = 0.3, so its placement matters)."""
+    rng = np.random.default_rng(62)
+    wl = make_wl([trees.chain(9)], d_k=7, d_v=5, h_k=1, h_v=2, n_layers=2)
+    a = random_arrays(wl, rng)
+    a["k"] = (a["k"] * rng.uniform(0.2, 3.0, size=a["k"].shape[:-1] + (1,))).astype(np.float32)
+    wl.arrays = a
+    prep = _prep_params(rng, wl, 0.3)
+    for (l, h) in [(0, 1), (1, 0)]:
+        al, be, K, Q, V = _prepared_operands(wl, a, 0, l, h, prep)
+        want_o, want_s = chain_matrix_form(a["state0"][0, l, h], al, be, K, V, Q)
+        o, st = oracle.verify_nodes(wl, 0, l, h, list(range(9)), want_state=True, prep=prep)
+        np.testing.assert_allclose(o, want_o, rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(st, want_s, rtol=1e-12, atol=1e-13)
+
+
+def pin_prep_tree_equals_wy_closed_form():
+    rng = np.random.default_rng(63)
+    par = trees.random_tree(rng, 18, 6, trees.bmax_uniform(3))
+    wl = make_wl([par, trees.FIG1_PARENT], d_k=6, d_v=5, h_k=2, h_v=4, n_layers=2, n_rows=[20, 8])
+    a = random_arrays(wl, rng)
+    a["q"] = (3.0 * a["q"]).astype(np.float32)
+    wl.arrays = a
+    prep = _prep_params(rng, wl, 1e-6)
+    for (r, l, h) in [(0, 0, 1), (0, 1, 2), (1, 1, 3)]:
+        al, be, K, Q, V = _prepared_operands(wl, a, r, l, h, prep)
+        want = tree_wy_form(wl.parents[r], a["state0"][r, l, h], al, be, K, V, Q)
+        o = oracle.verify_nodes(wl, r, l, h, list(range(len(wl.parents[r]))), prep=prep)
+        np.testing.assert_allclose(o, want, rtol=1e-11, atol=1e-12)
+
+
+def pin_prep_qk_scale_invariance():
+    """With eps = 0 the normalisation removes any positive scale of a query or key row."""
+    rng = np.random.default_rng(64)
+    par = trees.random_tree(rng, 12, 5, trees.bmax_uniform(3))
+    wl = make_wl([par], d_k=5, d_v=4, h_k=1, h_v=2)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    prep = oracle.Prep(oracle.PREP_QK_NORM, 0.0)
+    b = dict(a)
+    b["k"] = (a["k"] * rng.uniform(0.1, 10.0, size=a["k"].shape[:-1] + (1,))).astype(np.float64)
+    b["q"] = (a["q"] * rng.uniform(0.1, 10.0, size=a["q"].shape[:-1] + (1,))).astype(np.float64)
+    # the scaled rows are rounded to fp32 by the oracle's loader; compare at that precision
+    for h in range(2):
+        o1 = oracle.verify_nodes(wl, 0, 0, h, list(range(12)), prep=prep)
+        o2 = oracle.verify_nodes(wl, 0, 0, h, list(range(12)), arrays=b, prep=prep)
+        np.testing.assert_allclose(o2, o1, rtol=2e-6, atol=2e-7)
+        o3 = oracle.verify_nodes(wl, 0, 0, h, list(range(12)), arrays=b)
+        assert not np.allclose(o3, o1, rtol=1e-3)
+
+
+def pin_prep_commit_equals_node_state():
+    """The replay of a path with prepared operands publishes the verified state of its last node."""
+    rng = np.random.default_rng(65)
+    par = trees.random_tree(rng, 14, 6, trees.bmax_uniform(3))
+    wl = make_wl([par], d_k=6, d_v=4, h_k=1, h_v=2, max_path=14)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    prep = _prep_params(rng, wl, 1e-3)
+    node = int(np.argmax(trees.depths(par)))
+    _, st = oracle.verify_nodes(wl, 0, 0, 1, [node], want_state=True, prep=prep)
+    pub, _, _ = oracle.commit(wl, accepted=np.array([node], np.int32), prep=prep)
+    np.testing.assert_array_equal(pub[0, 0, 1], st[0])
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]

@@ -42,6 +42,10 @@ MUTATIONS = {
                          "xv = ld_op(hist, (((long)r * n_layers + l) * 3 + (2 - pos)) * channels + c, op_dtype);"),
     "hist_publish_shift": ("const int pos = L + e;", "const int pos = L + e - 1 < 0 ? 0 : L + e - 1;"),
     "commit_skips_last": ("for (int p = 0; p < path_len[r]; ++p)", "for (int p = 0; p + 1 < path_len[r]; ++p)"),
+    "qk_norm_without_eps": ("const double scale = sqrt(ss + d->qk_eps);", "const double scale = sqrt(ss);"),
+    "query_not_normalised": ("    qk_prepare(d, qv, dk);\n", ""),
+    "raw_gate_without_dt_bias": ("const double x = g_in + (double)d->dt_bias[lh];", "const double x = g_in;"),
+    "raw_beta_sign": ("*beta = 1.0 / (1.0 + exp(-b_in));", "*beta = 1.0 / (1.0 + exp(b_in));"),
 }
 
 
