@@ -176,6 +176,9 @@ def main():
     ap.add_argument("--config", default="batched")
     ap.add_argument("--policy", default="wy")
     ap.add_argument("--commit", choices=("deferred", "eager"), default="deferred")
+    ap.add_argument("--prep", action="store_true",
+                    help="prepare operands in the kernels (query/key normalisation, gates from raw "
+                         "inputs; wy policy): g and beta are then read as raw inputs")
     ap.add_argument("--copy-probe", action="store_true", help="only run the counter-calibration copy")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
@@ -189,6 +192,7 @@ def main():
         copy_probe()
         return
 
+    import numpy as np
     import torch
 
     import paper_2609_23900_amd as L
@@ -200,7 +204,15 @@ def main():
     log(f"[bench] generating {args.config}")
     wl = configs.build(args.config)
     log(f"[bench] uploading; policy {args.policy}")
-    st = GdnTreeStep.from_workload(wl, policy=policy, keep_state0=False)
+    prep = None
+    if args.prep:
+        if policy != L.LUMO_POLICY_WY:
+            sys.exit("--prep needs the wy policy")
+        rng = np.random.default_rng(5)
+        a_log = torch.from_numpy((0.5 * rng.standard_normal((wl.n_layers, wl.h_v))).astype(np.float32)).cuda()
+        dt_bias = torch.from_numpy(rng.standard_normal((wl.n_layers, wl.h_v)).astype(np.float32)).cuda()
+        prep = L.Prep(L.LUMO_PREP_QK_NORM | L.LUMO_PREP_RAW_GATES, 1e-6, a_log, dt_bias)
+    st = GdnTreeStep.from_workload(wl, policy=policy, keep_state0=False, prep=prep)
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
@@ -276,6 +288,7 @@ def main():
         "data": "synthetic (seeded trees and operands shaped like the paper's workloads)",
         "config": {"workload": f"{args.config}: {WORKLOAD_TEXT[args.config]}",
                    "policy": args.policy, "commit": mode, "head_node_updates_per_step": hn,
+                   "operand_prep": "qk_norm+raw_gates" if args.prep else "none",
                    "operands": "bf16" if wl.op_dtype == 1 else "f32"},
         "roofline": roof, "kernels": kernels,
     }

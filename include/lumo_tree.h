@@ -9,8 +9,10 @@
  *   lumo_tree_gdn_verify   device: every node's recurrent output from its ancestry
  *   lumo_gdn_commit        device: derive the accepted path, replay it into the
  *                          native state, publish the convolution history
- * plus a captured-graph form of the commit, and lumo_tree_gdn_verify_pending,
- * which folds the replay of one iteration into the verification of the next.
+ * plus a captured-graph form of the commit; lumo_tree_gdn_verify_pending, which
+ * folds the replay of one iteration into the verification of the next; and forms
+ * that prepare the operands inside the kernels (lumo_gdn_prep: query/key
+ * normalisation, gates from raw inputs).
  *
  * Conventions shared by every entry point
  *   - Device pointers are HIP device (or managed) memory owned by the caller.
@@ -191,6 +193,30 @@ lumo_status lumo_tree_conv_gather(const lumo_gdn_dims* dims, const lumo_tree_des
                                   void* stream);
 
 /*
+ * lumo_gdn_prep - operand preparation inside the kernels (Sec. IV-B: verification
+ * takes raw gate inputs and normalises queries and keys itself). Applies to every
+ * node of the call (tree nodes, path nodes replayed, pending path nodes).
+ *   flags    LUMO_PREP_QK_NORM: every query and key row x (d_k elements) is used as
+ *              x / sqrt(sum_i x_i^2 + qk_eps), computed in fp32 from the operands;
+ *            LUMO_PREP_RAW_GATES: g and beta hold raw inputs a and b per (node, value
+ *              head), and
+ *                alpha = exp(-exp(a_log[l][h]) * softplus(a + dt_bias[l][h])),
+ *                beta  = 1 / (1 + exp(-b)),
+ *              softplus(x) = log(1 + exp(x)), in fp32.
+ *   qk_eps   >= 0, finite (LUMO_PREP_QK_NORM)
+ *   a_log, dt_bias  device fp32 [n_layers][h_v] (LUMO_PREP_RAW_GATES; else ignored)
+ * A NULL lumo_gdn_prep, or flags 0, means the operands are used as given.
+ */
+#define LUMO_PREP_QK_NORM 1
+#define LUMO_PREP_RAW_GATES 2
+typedef struct {
+    int32_t flags;
+    float qk_eps;
+    const float* a_log;
+    const float* dt_bias;
+} lumo_gdn_prep;
+
+/*
  * lumo_tree_gdn_verify - recurrent output of every tree node (Sec. III-B,
  * Eq. (2)-(3); path-parallel scan Sec. IV-A, Alg. 2). For each request r, layer l,
  * value head h and node i, with R_pi the state after the root-to-parent path
@@ -215,6 +241,17 @@ lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lumo_tree_desc
                                  int32_t flags, void* stream);
 
 /*
+ * lumo_tree_gdn_verify_prep - lumo_tree_gdn_verify with the operands prepared as
+ * `prep` says (nullable). Needs a plan built for LUMO_POLICY_WY (bf16 operands,
+ * d_k = d_v = 128, paths of at most 17 nodes), else LUMO_EUNSUPPORTED; no workspace,
+ * no node-state dump.
+ */
+lumo_status lumo_tree_gdn_verify_prep(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                      const lumo_gdn_prep* prep, const void* q, const void* k,
+                                      const void* v, const float* g, const float* beta,
+                                      const float* state0, void* o, void* stream);
+
+/*
  * lumo_tree_gdn_verify_pending - publish the previous iteration's accepted path into
  * the state bank and verify this iteration's tree from the published state, in one
  * pass over the state (Alg. 1: publication of iteration t-1 precedes verification of
@@ -233,12 +270,13 @@ lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lumo_tree_desc
  *                               path_len[r] <= 0 leaves request r's state as it is
  *   pend_k, pend_v, pend_g, pend_beta  the previous iteration's operands (device,
  *                               rows of pend_desc)
+ *   prep                        nullable; operand preparation of both iterations
  * The replay sums its dot products in another order than lumo_gdn_commit, so the
  * published state agrees with it to fp32 rounding, not bitwise. Requests with no
  * nodes in this iteration are still published.
  */
 lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
-                                         const void* q, const void* k, const void* v,
+                                         const lumo_gdn_prep* prep, const void* q, const void* k, const void* v,
                                          const float* g, const float* beta, float* state, void* o,
                                          const lumo_tree_desc* pend_desc, int32_t max_path,
                                          const int32_t* path_out, const int32_t* path_len,
@@ -269,6 +307,18 @@ lumo_status lumo_gdn_commit(const lumo_gdn_dims* dims, const lumo_tree_desc* des
                             int32_t* path_len, const void* k, const void* v, const float* g,
                             const float* beta, float* state, int32_t channels, const void* x,
                             void* conv_hist, void* stream);
+
+/*
+ * lumo_gdn_commit_prep - lumo_gdn_commit whose replay uses the operands prepared as
+ * `prep` says (nullable; any plan policy). The replay then agrees with a verification
+ * given the same `prep` to fp32 rounding.
+ */
+lumo_status lumo_gdn_commit_prep(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                 const lumo_gdn_prep* prep, int32_t max_path,
+                                 const int32_t* accepted_node, int32_t* path_out,
+                                 int32_t* path_len, const void* k, const void* v, const float* g,
+                                 const float* beta, float* state, int32_t channels,
+                                 const void* x, void* conv_hist, void* stream);
 
 /* Opaque captured commit (Sec. V-A: one fixed-shape committer graph). */
 typedef struct lumo_commit_graph lumo_commit_graph;

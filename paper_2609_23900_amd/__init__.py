@@ -4,7 +4,8 @@ kernels; torch tensors only provide device memory and the current HIP stream.
 
 The functions keep the names of the C ABI (include/lumo_tree.h):
   lumo_tree_plan, lumo_tree_gdn_workspace_bytes, lumo_tree_conv_gather,
-  lumo_tree_gdn_verify, lumo_tree_gdn_verify_pending, lumo_gdn_commit, lumo_gdn_commit_graph_create,
+  lumo_tree_gdn_verify, lumo_tree_gdn_verify_prep, lumo_tree_gdn_verify_pending, lumo_gdn_commit,
+  lumo_gdn_commit_prep, lumo_gdn_commit_graph_create,
   lumo_gdn_commit_graph_launch, lumo_gdn_commit_graph_destroy, lumo_last_error,
   lumo_version.
 Device arguments are torch tensors on the GPU (or None where the ABI allows NULL);
@@ -60,6 +61,27 @@ class lumo_tree_desc(ctypes.Structure):
     _fields_ = [("blob", ctypes.c_void_p), ("host_blob", ctypes.c_void_p), ("plan", lumo_plan)]
 
 
+LUMO_PREP_QK_NORM, LUMO_PREP_RAW_GATES = 1, 2
+
+
+class lumo_gdn_prep(ctypes.Structure):
+    _fields_ = [("flags", ctypes.c_int32), ("qk_eps", ctypes.c_float), ("a_log", ctypes.c_void_p),
+                ("dt_bias", ctypes.c_void_p)]
+
+
+class Prep:
+    """Operand preparation (lumo_gdn_prep): flags, qk_eps and, for raw gates, the device
+    tensors a_log and dt_bias [n_layers][h_v] fp32 (kept alive here)."""
+
+    def __init__(self, flags, qk_eps=1e-6, a_log=None, dt_bias=None):
+        self.a_log, self.dt_bias = a_log, dt_bias
+        self.c = lumo_gdn_prep(int(flags), float(qk_eps), _dptr(a_log), _dptr(dt_bias))
+
+
+def _prep_ptr(prep):
+    return None if prep is None else ctypes.byref(prep.c)
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built: run `python paper_2609_23900_amd/build.py` "
@@ -73,7 +95,11 @@ def _load():
     L.lumo_tree_gdn_workspace_bytes.restype = SZ
     L.lumo_tree_conv_gather.argtypes = [PD, PT, I32, P, P, P, P, I32, P, P]
     L.lumo_tree_gdn_verify.argtypes = [PD, PT, P, P, P, P, P, P, P, P, P, SZ, I32, P]
-    L.lumo_tree_gdn_verify_pending.argtypes = [PD, PT, P, P, P, P, P, P, P, PT, I32, P, P, P, P, P, P, P]
+    PP = ctypes.POINTER(lumo_gdn_prep)
+    L.lumo_tree_gdn_verify_prep.argtypes = [PD, PT, PP, P, P, P, P, P, P, P, P]
+    L.lumo_tree_gdn_verify_pending.argtypes = [PD, PT, PP, P, P, P, P, P, P, P, PT, I32, P, P, P, P, P, P,
+                                               P]
+    L.lumo_gdn_commit_prep.argtypes = [PD, PT, PP, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
     L.lumo_gdn_commit.argtypes = [PD, PT, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
     L.lumo_gdn_commit_graph_create.argtypes = [PD, PT, I32, P, P, P, P, P, P, P, P, I32, P, P,
                                                ctypes.POINTER(ctypes.c_void_p)]
@@ -83,7 +109,8 @@ def _load():
     L.lumo_last_error.restype = ctypes.c_char_p
     L.lumo_version.restype = ctypes.c_char_p
     for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_gdn_verify",
-              "lumo_tree_gdn_verify_pending", "lumo_gdn_commit", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
+              "lumo_tree_gdn_verify_prep", "lumo_tree_gdn_verify_pending", "lumo_gdn_commit",
+              "lumo_gdn_commit_prep", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -188,11 +215,18 @@ def lumo_tree_gdn_verify(d, desc: TreeDesc, q, k, v, g, beta, state0, o, node_st
                                      _stream(stream)))
 
 
+def lumo_tree_gdn_verify_prep(d, desc: TreeDesc, prep: Prep | None, q, k, v, g, beta, state0, o,
+                              stream=None):
+    _check(_lib.lumo_tree_gdn_verify_prep(ctypes.byref(d), ctypes.byref(desc.desc), _prep_ptr(prep),
+                                          _dptr(q), _dptr(k), _dptr(v), _dptr(g), _dptr(beta),
+                                          _dptr(state0), _dptr(o), _stream(stream)))
+
+
 def lumo_tree_gdn_verify_pending(d, desc: TreeDesc, q, k, v, g, beta, state, o, pend_desc: TreeDesc,
                                  max_path, path_out, path_len, pend_k, pend_v, pend_g, pend_beta,
-                                 stream=None):
+                                 stream=None, prep: Prep | None = None):
     _check(_lib.lumo_tree_gdn_verify_pending(
-        ctypes.byref(d), ctypes.byref(desc.desc), _dptr(q), _dptr(k), _dptr(v), _dptr(g),
+        ctypes.byref(d), ctypes.byref(desc.desc), _prep_ptr(prep), _dptr(q), _dptr(k), _dptr(v), _dptr(g),
         _dptr(beta), _dptr(state), _dptr(o), ctypes.byref(pend_desc.desc), int(max_path),
         _dptr(path_out), _dptr(path_len), _dptr(pend_k), _dptr(pend_v), _dptr(pend_g),
         _dptr(pend_beta), _stream(stream)))
@@ -204,6 +238,16 @@ def lumo_gdn_commit(d, desc: TreeDesc, max_path, accepted_node, path_out, path_l
                                 _dptr(accepted_node), _dptr(path_out), _dptr(path_len), _dptr(k),
                                 _dptr(v), _dptr(g), _dptr(beta), _dptr(state), int(channels),
                                 _dptr(x), _dptr(conv_hist), _stream(stream)))
+
+
+def lumo_gdn_commit_prep(d, desc: TreeDesc, prep: Prep | None, max_path, accepted_node, path_out,
+                         path_len, k, v, g, beta, state, channels=0, x=None, conv_hist=None,
+                         stream=None):
+    _check(_lib.lumo_gdn_commit_prep(ctypes.byref(d), ctypes.byref(desc.desc), _prep_ptr(prep),
+                                     int(max_path), _dptr(accepted_node), _dptr(path_out),
+                                     _dptr(path_len), _dptr(k), _dptr(v), _dptr(g), _dptr(beta),
+                                     _dptr(state), int(channels), _dptr(x), _dptr(conv_hist),
+                                     _stream(stream)))
 
 
 class CommitGraph:

@@ -57,6 +57,39 @@ lumo_status check_dims(const lumo_gdn_dims* d, const char* fn) {
     return LUMO_OK;
 }
 
+// The WY policy's shape limits (bf16, d_k = d_v = 128, at most kWyMaxDepth nodes per path).
+lumo_status check_wy(const lumo_gdn_dims* d, const lumo_tree_desc* desc, const char* fn) {
+    if (desc->plan.policy != LUMO_POLICY_WY)
+        return fail(LUMO_EUNSUPPORTED, "%s: needs a plan built for LUMO_POLICY_WY (plan policy %d)", fn,
+                    desc->plan.policy);
+    if (d->op_dtype != LUMO_BF16 || d->d_k != 128 || d->d_v != 128)
+        return fail(LUMO_EUNSUPPORTED, "%s: the WY policy is built for bf16 operands with d_k = d_v = 128", fn);
+    if (desc->plan.max_depth > kWyMaxDepth)
+        return fail(LUMO_EUNSUPPORTED, "%s: the WY policy handles paths of at most %d nodes (plan has %d)", fn,
+                    kWyMaxDepth, desc->plan.max_depth);
+    return LUMO_OK;
+}
+
+// Operand preparation: flags, constant and gate parameters; NULL means none.
+lumo_status check_prep(const lumo_gdn_prep* prep, const char* fn, PrepArgs& out) {
+    out = PrepArgs{};
+    if (!prep) return LUMO_OK;
+    if (prep->flags & ~(LUMO_PREP_QK_NORM | LUMO_PREP_RAW_GATES))
+        return fail(LUMO_EINVAL, "%s: prep flags 0x%x (known: QK_NORM 1, RAW_GATES 2)", fn, prep->flags);
+    if ((prep->flags & LUMO_PREP_QK_NORM) && !(prep->qk_eps >= 0.f && prep->qk_eps <= 3.0e38f))
+        return fail(LUMO_EINVAL, "%s: prep qk_eps must be finite and >= 0", fn);
+    if (prep->flags & LUMO_PREP_RAW_GATES) {
+        if (!prep->a_log || !prep->dt_bias) return fail(LUMO_EINVAL, "%s: raw gates need a_log and dt_bias", fn);
+        if ((reinterpret_cast<uintptr_t>(prep->a_log) | reinterpret_cast<uintptr_t>(prep->dt_bias)) & 3u)
+            return fail(LUMO_EINVAL, "%s: a_log and dt_bias must be 4-byte aligned", fn);
+    }
+    out.flags = prep->flags;
+    out.qk_eps = prep->qk_eps;
+    out.a_log = prep->a_log;
+    out.dt_bias = prep->dt_bias;
+    return LUMO_OK;
+}
+
 lumo_status check_desc(const lumo_gdn_dims* d, const lumo_tree_desc* desc, const char* fn) {
     if (!desc) return fail(LUMO_EINVAL, "%s: desc is NULL", fn);
     const lumo_plan& p = desc->plan;
@@ -129,11 +162,7 @@ extern "C" lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lum
     LUMO_TRY(check_ptr(node_states, fn, "node_states", true));
     if (policy == LUMO_POLICY_WY) {
         if (node_states) return fail(LUMO_EUNSUPPORTED, "%s: the WY policy keeps no per-node states", fn);
-        if (dims->op_dtype != LUMO_BF16 || dims->d_k != 128 || dims->d_v != 128)
-            return fail(LUMO_EUNSUPPORTED, "%s: the WY policy is built for bf16 operands with d_k = d_v = 128", fn);
-        if (desc->plan.max_depth > kWyMaxDepth)
-            return fail(LUMO_EUNSUPPORTED, "%s: the WY policy handles paths of at most %d nodes (plan has %d)", fn,
-                        kWyMaxDepth, desc->plan.max_depth);
+        LUMO_TRY(check_wy(dims, desc, fn));
     }
     const size_t need = lumo_tree_gdn_workspace_bytes(dims, &desc->plan);
     if (need) {
@@ -153,7 +182,34 @@ extern "C" lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lum
     return LUMO_OK;
 }
 
+extern "C" lumo_status lumo_tree_gdn_verify_prep(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                                 const lumo_gdn_prep* prep, const void* q, const void* k,
+                                                 const void* v, const float* g, const float* beta,
+                                                 const float* state0, void* o, void* stream) {
+    static const char* fn = "lumo_tree_gdn_verify_prep";
+    clear_error();
+    LUMO_TRY(check_dims(dims, fn));
+    LUMO_TRY(check_desc(dims, desc, fn));
+    LUMO_TRY(check_wy(dims, desc, fn));
+    PrepArgs pr;
+    LUMO_TRY(check_prep(prep, fn, pr));
+    if (desc->plan.total_nodes == 0) return LUMO_OK;
+    LUMO_TRY(check_ptr(q, fn, "q"));
+    LUMO_TRY(check_ptr(k, fn, "k"));
+    LUMO_TRY(check_ptr(v, fn, "v"));
+    LUMO_TRY(check_ptr(g, fn, "g"));
+    LUMO_TRY(check_ptr(beta, fn, "beta"));
+    LUMO_TRY(check_ptr(state0, fn, "state0"));
+    LUMO_TRY(check_ptr(o, fn, "o"));
+    GdnArgs a{q, k, v, g, beta, state0, o, nullptr, nullptr, pr};
+    hipError_t e = launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream));
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not available in this build", fn);
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
 extern "C" lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                                    const lumo_gdn_prep* prep,
                                                     const void* q, const void* k, const void* v, const float* g,
                                                     const float* beta, float* state, void* o,
                                                     const lumo_tree_desc* pend_desc, int32_t max_path,
@@ -166,14 +222,9 @@ extern "C" lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, c
     LUMO_TRY(check_desc(dims, desc, fn));
     if (!pend_desc) return fail(LUMO_EINVAL, "%s: pend_desc is NULL", fn);
     LUMO_TRY(check_desc(dims, pend_desc, fn));
-    if (desc->plan.policy != LUMO_POLICY_WY)
-        return fail(LUMO_EUNSUPPORTED, "%s: needs a plan built for LUMO_POLICY_WY (plan policy %d)", fn,
-                    desc->plan.policy);
-    if (dims->op_dtype != LUMO_BF16 || dims->d_k != 128 || dims->d_v != 128)
-        return fail(LUMO_EUNSUPPORTED, "%s: the WY policy is built for bf16 operands with d_k = d_v = 128", fn);
-    if (desc->plan.max_depth > kWyMaxDepth)
-        return fail(LUMO_EUNSUPPORTED, "%s: the WY policy handles paths of at most %d nodes (plan has %d)", fn,
-                    kWyMaxDepth, desc->plan.max_depth);
+    LUMO_TRY(check_wy(dims, desc, fn));
+    PrepArgs pr;
+    LUMO_TRY(check_prep(prep, fn, pr));
     if (max_path < 1 || max_path > 4096) return fail(LUMO_EINVAL, "%s: max_path %d (1..4096)", fn, max_path);
     if (dims->n_req == 0) return LUMO_OK;
     LUMO_TRY(check_ptr(state, fn, "state"));
@@ -193,7 +244,7 @@ extern "C" lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, c
         LUMO_TRY(check_ptr(beta, fn, "beta"));
         LUMO_TRY(check_ptr(o, fn, "o"));
     }
-    GdnArgs a{q, k, v, g, beta, state, o, nullptr, nullptr};
+    GdnArgs a{q, k, v, g, beta, state, o, nullptr, nullptr, pr};
     PendArgs pa{pend_desc, max_path, path_out, path_len, pend_k, pend_v, pend_g, pend_beta, state};
     hipError_t e = launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream), &pa);
     if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not available in this build", fn);
@@ -244,6 +295,25 @@ extern "C" lumo_status lumo_gdn_commit(const lumo_gdn_dims* dims, const lumo_tre
                           conv_hist, fn));
     if (dims->n_req == 0) return LUMO_OK;
     CommitArgs a{max_path, accepted_node, path_out, path_len, k, v, g, beta, state, channels, x, conv_hist};
+    hipError_t e = launch_commit(*dims, *desc, a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
+extern "C" lumo_status lumo_gdn_commit_prep(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                            const lumo_gdn_prep* prep, int32_t max_path,
+                                            const int32_t* accepted_node, int32_t* path_out, int32_t* path_len,
+                                            const void* k, const void* v, const float* g, const float* beta,
+                                            float* state, int32_t channels, const void* x, void* conv_hist,
+                                            void* stream) {
+    static const char* fn = "lumo_gdn_commit_prep";
+    clear_error();
+    LUMO_TRY(check_commit(dims, desc, max_path, accepted_node, path_out, path_len, k, v, g, beta, state, channels, x,
+                          conv_hist, fn));
+    PrepArgs pr;
+    LUMO_TRY(check_prep(prep, fn, pr));
+    if (dims->n_req == 0) return LUMO_OK;
+    CommitArgs a{max_path, accepted_node, path_out, path_len, k, v, g, beta, state, channels, x, conv_hist, pr};
     hipError_t e = launch_commit(*dims, *desc, a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return LUMO_OK;

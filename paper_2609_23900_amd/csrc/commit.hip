@@ -57,6 +57,7 @@ struct ReplayParams {
     const int32_t* blob;
     int32_t o_node_off, o_row;
     int32_t max_path, n_layers, total_rows, h_k, h_v, d_v, group, n_vtiles;
+    PrepArgs prep;  // operand preparation of the path's k, g, beta
 };
 
 // Path entries whose key row, row, decay, beta and value are fetched before the loop.
@@ -81,8 +82,10 @@ template <> __device__ __forceinline__ void unpack_seg<1>(const uint4 w, float (
 // The verifier's row update (gdn_row_update: same operations in the same order, so
 // the result is bitwise identical) with the key row read from LDS, 32 elements at a
 // time (the compiler barrier keeps it from hoisting the whole row into registers).
+// ks scales the key (1/|k| with query/key normalisation, else exactly 1).
 template <int DK, int OPT>
-__device__ __forceinline__ void row_update_lds(float (&S)[DK], const uint4* kr, float vj, float alpha, float beta) {
+__device__ __forceinline__ void row_update_lds(float (&S)[DK], const uint4* kr, float vj, float alpha, float beta,
+                                               float ks) {
     constexpr int E = 16 / (int)sizeof(typename Op<OPT>::T);  // elements per 16-byte segment
     constexpr int C = DK < 32 ? DK : 32;
     Dot4 u;
@@ -97,7 +100,7 @@ __device__ __forceinline__ void row_update_lds(float (&S)[DK], const uint4* kr, 
             for (int i = 0; i < E; ++i) u.add(c + i, S[c + i], kf[i]);
         }
     }
-    const float delta = beta * __builtin_fmaf(-alpha, u.sum(), vj);
+    const float delta = beta * __builtin_fmaf(-alpha, u.sum() * ks, vj) * ks;
 #pragma unroll
     for (int c0 = 0; c0 < DK; c0 += C) {
         asm volatile("" ::: "memory");
@@ -127,8 +130,14 @@ __device__ __forceinline__ void replay_stage(const ReplayParams& p, const typena
     const int ne = min(len - e0, kPrefetch);
     const int prow = p.blob[p.o_row + base + path[e0 + min(lane, ne - 1)]];
     const long gl = ((long)l * p.total_rows + prow) * p.h_v + h;
-    apre = __expf(g[gl]);
-    bpre = beta[gl];
+    float gv = g[gl], bv = beta[gl];
+    if (p.prep.flags & LUMO_PREP_RAW_GATES) {
+        const int lh = l * p.h_v + h;
+        gv = raw_log_alpha(gv, p.prep.a_log[lh], p.prep.dt_bias[lh]);
+        bv = raw_beta(bv);
+    }
+    apre = __expf(gv);
+    bpre = bv;
 #pragma unroll
     for (int i = 0; i < KR::kSlots / 64; ++i) {
         const int sl = 64 * i + lane;
@@ -190,10 +199,24 @@ __global__ __launch_bounds__(64, 2) void replay_kernel(ReplayParams p, const typ
             replay_stage<DK, OPT>(p, k, v, g, beta, path, base, len, e0, l, h, hk, vt, lane, krows, vrows, apre, bpre);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the staged rows have landed in LDS
         const int ne = min(len - e0, kPrefetch);
+        float kspre = 1.f;  // lane e: 1/sqrt(|k|^2 + eps) of entry e's key (normalisation)
+        if (p.prep.flags & LUMO_PREP_QK_NORM) {
+            constexpr int E = 16 / (int)sizeof(T);
+            const uint4* kr = krows + min(lane, ne - 1) * KR::kSeg;
+            float ss = 0.f;
+            for (int sg = 0; sg < KR::kSeg; ++sg) {
+                float f[E];
+                unpack_seg<OPT>(kr[sg], f);
+#pragma unroll
+                for (int i = 0; i < E; ++i) ss = __builtin_fmaf(f[i], f[i], ss);
+            }
+            kspre = __builtin_amdgcn_rsqf(ss + p.prep.qk_eps);
+        }
         for (int e = 0; e < ne; ++e) {
             const float ae = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(apre), e));
             const float be = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bpre), e));
-            row_update_lds<DK, OPT>(S, krows + e * KR::kSeg, Op<OPT>::ld(vl, e * 64 + lane), ae, be);
+            const float ke = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(kspre), e));
+            row_update_lds<DK, OPT>(S, krows + e * KR::kSeg, Op<OPT>::ld(vl, e * 64 + lane), ae, be, ke);
         }
     }
     if (act) {
@@ -334,6 +357,7 @@ hipError_t launch_commit(const lumo_gdn_dims& d, const lumo_tree_desc& desc, con
     rp.d_v = d.d_v;
     rp.group = d.h_v / d.h_k;
     rp.n_vtiles = (d.d_v + 63) / 64;
+    rp.prep = a.prep;
     const long blocks = (long)d.n_req * d.n_layers * d.h_v * rp.n_vtiles;
     e = d.op_dtype == LUMO_BF16 ? launch_replay<1>(d.d_k, dim3((unsigned)blocks), s, rp, a)
                                 : launch_replay<0>(d.d_k, dim3((unsigned)blocks), s, rp, a);

@@ -126,6 +126,17 @@ __device__ __forceinline__ float gdn_row_output(const float (&S)[DK], const type
     return o.sum();
 }
 
+// ---------------------------------------------------------------- operand preparation
+// Gates from raw inputs (Sec. IV-B; the Gated DeltaNet parametrisation):
+//   log alpha = -exp(a_log) softplus(a + dt_bias),  softplus(x) = max(x, 0) + log(1 + e^-|x|)
+//   beta = 1 / (1 + e^-b)
+__device__ __forceinline__ float raw_log_alpha(float a, float a_log, float dt_bias) {
+    const float x = a + dt_bias;
+    const float sp = fmaxf(x, 0.f) + log1pf(__expf(-fabsf(x)));
+    return -__expf(a_log) * sp;
+}
+__device__ __forceinline__ float raw_beta(float b) { return 1.f / (1.f + __expf(-b)); }
+
 // ---------------------------------------------------------------- launch geometry
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).
 // Remap so that consecutive logical block ids run on the same XCD: blocks that

@@ -8,6 +8,14 @@
 
 namespace lumo {
 
+// Operand preparation inside the kernels (lumo_gdn_prep); flags 0 = operands as given.
+struct PrepArgs {
+    int32_t flags = 0;
+    float qk_eps = 0.f;
+    const float* a_log = nullptr;
+    const float* dt_bias = nullptr;
+};
+
 struct GdnArgs {
     const void* q;
     const void* k;
@@ -18,6 +26,7 @@ struct GdnArgs {
     void* o;
     float* node_states;
     float* ws;
+    PrepArgs prep;  // WY kernel only
 };
 
 // Sequential path scans (PATHS / TWO_LEVEL / RECOMPUTE): one launch per dependency level.
@@ -57,6 +66,7 @@ struct CommitArgs {
     int32_t channels;
     const void* x;
     void* conv_hist;
+    PrepArgs prep;  // replay only
 };
 
 hipError_t launch_commit(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const CommitArgs& a, hipStream_t s);

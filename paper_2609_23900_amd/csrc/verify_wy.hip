@@ -65,6 +65,10 @@ struct WyParams {
     const int32_t* blob;
     int32_t o_node_off, o_pre_row, o_pre_depth, o_pre_ci, o_chunk_off, o_chunk_stack;
     int32_t n_layers, total_rows, h_k, h_v, group;
+    int32_t raw_gates;  // g and beta hold raw inputs (operand preparation)
+    float qk_eps;       // query/key normalisation constant (QKN kernels)
+    const float* a_log;
+    const float* dt_bias;
 };
 
 // The previous iteration's accepted path, published into the state bank before the
@@ -115,7 +119,10 @@ __device__ __forceinline__ float row_group_sum(float x) {
 // PEND: the state bank (state0 = pd.state) first receives the replay of the previous
 // iteration's accepted path (Eq. (2)-(3) per path node), is stored back, and the
 // verification then starts from it; requests without nodes are published only.
-template <int D, int NVH, bool PEND>
+// QKN: every query and key row x is used as x / sqrt(|x|^2 + eps) (Sec. IV-B). The
+// bf16 rows stay as they are in LDS and the MFMA products; the per-row factors scale
+// the Gram entries, R0 k, R0 q and k.q in the records, and the pending path's keys.
+template <int D, int NVH, bool PEND, bool QKN>
 __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, const uint16_t* __restrict__ kmat,
                                                     const uint16_t* __restrict__ qmat,
                                                     const uint16_t* __restrict__ vmat, const float* __restrict__ gmat,
@@ -130,6 +137,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     __shared__ __attribute__((aligned(16))) float recs[2 * NVH][kTile * W];  // per wave: the chunk's coefficient records
     __shared__ float alphas[2 * NVH][64];          // per wave: exp(g) of the candidates
     __shared__ uint4 vbufs[2 * NVH][2][kTile * 8]; // per wave: value rows, then outputs; double-buffered
+    __shared__ float nrm[kTileRows];               // QKN: 1/|row| of [stack keys 16 | chunk keys 32 | queries 32]
     const int tid = (int)threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: head and half in SGPRs
     const int lane = tid & 63;
@@ -146,6 +154,9 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     const int r = blk / p.n_layers;
     const int h = hk * p.group + pp * NVH + (wave >> 1);
     const int j0 = 64 * (wave & 1);
+    const bool rawg = p.raw_gates != 0;  // uniform
+    const float alog = rawg ? p.a_log[l * p.h_v + h] : 0.f;
+    const float dtb = rawg ? p.dt_bias[l * p.h_v + h] : 0.f;
     const int base = p.blob[p.o_node_off + r];
     const int N = p.blob[p.o_node_off + r + 1] - base;
     int plen = 0;  // pending path length; an empty or invalid path leaves the state as it is
@@ -299,8 +310,12 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
             const int node = min(max(ppath[e0 + min(lane % kPend, ne - 1)], 0), pn - 1);
             const int row = pd.blob[pd.o_row + pbase + node];
             const long gl = (prow0 + row) * p.h_v + h;
-            const float pa = __expf(pd.g[gl]);
-            const float pb = pd.beta[gl];
+            float pgv = pd.g[gl], pb = pd.beta[gl];
+            if (rawg) {
+                pgv = raw_log_alpha(pgv, alog, dtb);
+                pb = raw_beta(pb);
+            }
+            const float pa = __expf(pgv);
             int rv[kPend * 8 / 64];
 #pragma unroll
             for (int i = 0; i < kPend * 8 / 64; ++i) rv[i] = __shfl(row, (64 * i + lane) >> 3);
@@ -339,6 +354,18 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                         kf[kb][2 * e2 + 1] = bf16_hi(ww[e2]);
                     }
                 }
+                float sk = 1.f;  // QKN: 1/|k| of the entry's key (every lane holds a quarter of it)
+                if constexpr (QKN) {
+                    float ss0 = 0.f, ss1 = 0.f;
+#pragma unroll
+                    for (int kb = 0; kb < kD / 32; ++kb)
+#pragma unroll
+                        for (int e8 = 0; e8 < 8; ++e8) {
+                            float& acc = (kb & 1) ? ss1 : ss0;
+                            acc = __builtin_fmaf(kf[kb][e8], kf[kb][e8], acc);
+                        }
+                    sk = __builtin_amdgcn_rsqf(row_group_sum(ss0 + ss1) + p.qk_eps);
+                }
                 float dl[4];
 #pragma unroll
                 for (int ct = 0; ct < 4; ++ct) {
@@ -350,9 +377,9 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                             float& acc = (kb & 1) ? s1 : s0;
                             acc = __builtin_fmaf(__uint_as_float(raw[ct][kb][e8]), kf[kb][e8], acc);
                         }
-                    const float u = row_group_sum(s0 + s1);
+                    const float u = row_group_sum(s0 + s1) * sk;
                     const float vj = bf16_lo((uint32_t)vsh[e * 64 + 4 * (lane % 16) + ct]);
-                    dl[ct] = be * __builtin_fmaf(-ae, u, vj);
+                    dl[ct] = be * __builtin_fmaf(-ae, u, vj) * sk;
                 }
 #pragma unroll
                 for (int ct = 0; ct < 4; ++ct)
@@ -494,6 +521,27 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         const int kb0 = ln / kTile;  // key block offset within a 16-key step (32x32x16 Gram)
         const int pc = 4 * (ln % 16) + ln / 16;  // this lane's state column (after the exchange)
         const int arow = mt == 0 ? tn : 2 * kTile + (tn & (kStack - 1));
+        if constexpr (QKN) {
+            // 1/sqrt(|x|^2 + eps) of every tile row: 8 lanes per row, 16 elements each
+            for (int task = (int)threadIdx.x; task < kTileRows * 8; task += nthr) {
+                const int row = task >> 3, grp = task & 7;
+                const uint4 w0 = tile.slot[row * 16 + ((2 * grp) ^ (row & 15))];
+                const uint4 w1 = tile.slot[row * 16 + ((2 * grp + 1) ^ (row & 15))];
+                const uint32_t ww[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+                float ss = 0.f;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    ss = __builtin_fmaf(bf16_lo(ww[i]), bf16_lo(ww[i]), ss);
+                    ss = __builtin_fmaf(bf16_hi(ww[i]), bf16_hi(ww[i]), ss);
+                }
+                ss += __shfl_xor(ss, 1);
+                ss += __shfl_xor(ss, 2);
+                ss += __shfl_xor(ss, 4);
+                if (grp == 0)
+                    nrm[row < kTile ? kStack + row : row < 2 * kTile ? kCand + (row - kTile) : row - 2 * kTile] =
+                        __builtin_amdgcn_rsqf(ss + p.qk_eps);
+            }
+        }
         if (c0 > 0) flush(vbufs[wave][buf ^ 1], kTile);  // the previous chunk had two halves
         if (more) {
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the flush has read the buffer
@@ -537,11 +585,18 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         lds_barrier();  // the Gram is complete
 
         // ---- coefficient records of the wave's head (lanes 0..31: A, lanes 32..63: B)
-        if (ln < kTile + kStack) walpha[ln < kTile ? kStack + ln : ln - kTile] = __expf(info.g);
+        if (ln < kTile + kStack)
+            walpha[ln < kTile ? kStack + ln : ln - kTile] = __expf(rawg ? raw_log_alpha(info.g, alog, dtb) : info.g);
         {
             const bool isB = ln >= kTile;
             const float* Gc = G + (isB ? kTile : 0) + tn;
-            const float sc = isB ? 1.f : info.b;
+            const float bt = rawg ? raw_beta(info.b) : info.b;
+            float nk = 1.f, nq = 1.f;  // QKN: 1/|k_t|, 1/|q_t|
+            if constexpr (QKN) {
+                nk = nrm[kStack + tn];
+                nq = nrm[kCand + tn];
+            }
+            const float sc = isB ? nq : bt * nk;
             float gam = walpha[kStack + tn];  // Gamma(a_{d-1} -> t) = alpha_t
             float cv[D];
 #pragma unroll
@@ -550,7 +605,9 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                 // are issued together instead of one conditional round trip per depth
                 const bool live = m < info.dep;
                 const int ci = live ? (int)((info.ci[m / 4] >> (8 * (m % 4))) & 0xffu) : 0;
-                const float gv = Gc[ci * kGS], av = walpha[ci];
+                float gv = Gc[ci * kGS];
+                if constexpr (QKN) gv *= nrm[ci];
+                const float av = walpha[ci];
                 cv[m] = (sc * gam) * gv * (live ? 1.f : 0.f);
                 gam *= live ? av : 1.f;  // then Gamma(a_{m-1} -> t); finally gamma_t
             }
@@ -561,8 +618,9 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                     make_float4(cv[4 * q4], cv[4 * q4 + 1], cv[4 * q4 + 2], cv[4 * q4 + 3]);
             if (!isB) {
                 *reinterpret_cast<float4*>(rt) =
-                    make_float4(__int_as_float(rowC.n), __int_as_float(info.dep), info.b, gam);
-                *reinterpret_cast<float4*>(rt + 4) = make_float4(G[(kStack + tn) * kGS + kTile + tn], 0.f, 0.f, 0.f);
+                    make_float4(__int_as_float(rowC.n), __int_as_float(info.dep), bt, gam * nk);
+                *reinterpret_cast<float4*>(rt + 4) =
+                    make_float4(G[(kStack + tn) * kGS + kTile + tn] * (nk * nq), gam * nq, 0.f, 0.f);
             }
         }
         // next chunk's lane view (lands during the recursion)
@@ -580,7 +638,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         // One node's record in registers: {row, depth} as ints, {beta, gamma, k.q}, A, B.
         struct NodeRec {
             int rn, d;
-            float bn, gm, cn;
+            float bn, gm, cn, gq;  // gm: gamma for R0 k, gq: gamma for R0 q
             float a[D], b[D];
         };
         auto load_rec = [&](int n, NodeRec& c) {
@@ -590,6 +648,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
             c.bn = cf[2];
             c.gm = cf[3];
             c.cn = cf[4];
+            c.gq = QKN ? cf[5] : c.gm;
 #pragma unroll
             for (int m = 0; m < D; ++m) {
                 c.a[m] = cf[8 + m];
@@ -614,7 +673,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                 }
                 const float u = __builtin_fmaf(-cur.gm, pk[i / 4][i % 4], vj);  // v - gamma R0 k
                 const float delta = __builtin_fmaf(cur.bn, u, -(sa0 + sa1));     // beta u - sum A delta
-                const float ov = __builtin_fmaf(cur.cn, delta, __builtin_fmaf(cur.gm, pq[i / 4][i % 4], sb0 + sb1));
+                const float ov = __builtin_fmaf(cur.cn, delta, __builtin_fmaf(cur.gq, pq[i / 4][i % 4], sb0 + sb1));
                 dst[cur.d < D ? cur.d : D] = delta;  // uniform index: an indexed register write
                 vs[n * 64 + pc] = f32_to_bf16(ov);     // over the consumed value entry
             }
@@ -638,11 +697,11 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     flush(vbufs[wave][cl & 1], cl * kTile + kTile / 2 < N ? kTile : kTile / 2);
 }
 
-template <int D, int NVH, bool PEND>
+template <int D, int NVH, bool PEND, bool QKN>
 hipError_t launch_wy_kernel(const lumo_gdn_dims& d, const WyParams& p, const GdnArgs& a, hipStream_t s,
                             const PendParams& pp) {
     const long nb = (long)d.n_req * d.n_layers * d.h_k * (p.group / NVH);
-    hipLaunchKernelGGL((wy_kernel<D, NVH, PEND>), dim3((unsigned)nb), dim3(128 * NVH), 0, s, p,
+    hipLaunchKernelGGL((wy_kernel<D, NVH, PEND, QKN>), dim3((unsigned)nb), dim3(128 * NVH), 0, s, p,
                        static_cast<const uint16_t*>(a.k), static_cast<const uint16_t*>(a.q),
                        static_cast<const uint16_t*>(a.v), a.g, a.beta, PEND ? pp.state : a.state0,
                        static_cast<uint16_t*>(a.o), pp);
@@ -666,10 +725,16 @@ hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.h_k = d.h_k;
     p.h_v = d.h_v;
     p.group = d.h_v / d.h_k;
+    p.raw_gates = (a.prep.flags & LUMO_PREP_RAW_GATES) != 0;
+    p.qk_eps = a.prep.qk_eps;
+    p.a_log = a.prep.a_log;
+    p.dt_bias = a.prep.dt_bias;
     // one block per (request, layer, key head, pair of value heads): the pair's waves
     // share the staged key and query rows and the Gram
-    if (p.group % 2 == 0) return launch_wy_kernel<D, 2, PEND>(d, p, a, s, pp);
-    return launch_wy_kernel<D, 1, PEND>(d, p, a, s, pp);
+    const bool qkn = (a.prep.flags & LUMO_PREP_QK_NORM) != 0;
+    if (p.group % 2 == 0)
+        return qkn ? launch_wy_kernel<D, 2, PEND, true>(d, p, a, s, pp) : launch_wy_kernel<D, 2, PEND, false>(d, p, a, s, pp);
+    return qkn ? launch_wy_kernel<D, 1, PEND, true>(d, p, a, s, pp) : launch_wy_kernel<D, 1, PEND, false>(d, p, a, s, pp);
 }
 
 }  // namespace

@@ -10,8 +10,9 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import (LUMO_BF16, LumoError, TreeDesc, dims, lumo_gdn_commit, lumo_gdn_commit_graph_create,
-               lumo_tree_conv_gather, lumo_tree_gdn_verify, lumo_tree_gdn_verify_pending,
+from . import (LUMO_BF16, LumoError, TreeDesc, dims, lumo_gdn_commit_graph_create,
+               lumo_gdn_commit_prep, lumo_tree_conv_gather, lumo_tree_gdn_verify,
+               lumo_tree_gdn_verify_pending, lumo_tree_gdn_verify_prep,
                lumo_tree_gdn_workspace_bytes)
 
 
@@ -31,8 +32,9 @@ class GdnTreeStep:
 
     def __init__(self, *, n_req, n_layers, h_k, h_v, d_k, d_v, op_dtype, node_off, parent,
                  n_rows, arrays, policy=0, max_path=16, accepted=None, channels=0, act=1,
-                 device="cuda", with_node_states=False, keep_state0=True):
+                 device="cuda", with_node_states=False, keep_state0=True, prep=None):
         self.dims = dims(n_req, n_layers, h_k, h_v, d_k, d_v, op_dtype)
+        self.prep = prep  # a Prep (operand preparation inside the kernels) or None
         self.desc = TreeDesc.build(node_off, parent, n_rows, policy, device)
         self.plan = self.desc.plan
         self.max_path = int(max_path)
@@ -76,9 +78,14 @@ class GdnTreeStep:
                               self.bias, self.act, self.y, stream)
 
     def verify(self, stream=None, state0=None):
+        s0 = self.state if state0 is None else state0
+        if self.prep is not None:
+            lumo_tree_gdn_verify_prep(self.dims, self.desc, self.prep, self.t["q"], self.t["k"],
+                                      self.t["v"], self.t["g"], self.t["beta"], s0, self.o, stream)
+            return
         lumo_tree_gdn_verify(self.dims, self.desc, self.t["q"], self.t["k"], self.t["v"],
-                             self.t["g"], self.t["beta"], self.state if state0 is None else state0,
-                             self.o, self.node_states, self.ws, 0, stream)
+                             self.t["g"], self.t["beta"], s0, self.o, self.node_states, self.ws, 0,
+                             stream)
 
     def verify_pending(self, prev: "GdnTreeStep", stream=None, state=None):
         """Publish prev's accepted path (written by prev.commit(defer=True)) into the
@@ -88,15 +95,16 @@ class GdnTreeStep:
                                      self.t["g"], self.t["beta"],
                                      self.state if state is None else state, self.o, prev.desc,
                                      prev.max_path, prev.path_out, prev.path_len, prev.t["k"],
-                                     prev.t["v"], prev.t["g"], prev.t["beta"], stream)
+                                     prev.t["v"], prev.t["g"], prev.t["beta"], stream, self.prep)
 
     def commit(self, stream=None, with_conv=True, defer=False):
         """Accepted path, conv history and (unless defer) the replay into self.state."""
         use_conv = with_conv and self.has_conv
-        lumo_gdn_commit(self.dims, self.desc, self.max_path, self.accepted, self.path_out,
-                        self.path_len, self.t["k"], self.t["v"], self.t["g"], self.t["beta"],
-                        None if defer else self.state, self.channels if use_conv else 0,
-                        self.x if use_conv else None, self.hist if use_conv else None, stream)
+        lumo_gdn_commit_prep(self.dims, self.desc, self.prep, self.max_path, self.accepted,
+                             self.path_out, self.path_len, self.t["k"], self.t["v"], self.t["g"],
+                             self.t["beta"], None if defer else self.state,
+                             self.channels if use_conv else 0, self.x if use_conv else None,
+                             self.hist if use_conv else None, stream)
 
     def commit_graph(self, with_conv=True):
         use_conv = with_conv and self.has_conv

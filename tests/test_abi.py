@@ -186,7 +186,7 @@ def test_wy_needs_no_workspace():
 def _pending(d, desc, pdesc, max_path=4, state=FAKE, pend_desc=True):
     P = ctypes.c_void_p
     return L._lib.lumo_tree_gdn_verify_pending(
-        ctypes.byref(d), ctypes.byref(desc), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+        ctypes.byref(d), ctypes.byref(desc), None, P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
         P(state) if state else None, P(FAKE), ctypes.byref(pdesc) if pend_desc else None,
         max_path, P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), None)
 
@@ -213,3 +213,39 @@ def test_verify_pending_empty_batch_is_a_no_op():
     desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
     d = _dims(n_req=0, h_k=1, h_v=1, d_k=128, d_v=128, op_dtype=1)
     assert _pending(d, desc, desc) == L.LUMO_OK
+
+
+def _verify_prep(d, desc, prep):
+    P = ctypes.c_void_p
+    return L._lib.lumo_tree_gdn_verify_prep(ctypes.byref(d), ctypes.byref(desc),
+                                            ctypes.byref(prep) if prep is not None else None,
+                                            *([P(FAKE)] * 7), None)
+
+
+def test_prep_rejects_bad_arguments():
+    dw = _dims(h_k=2, h_v=4, d_k=128, d_v=128, op_dtype=1)
+    wy, _b1 = _desc(policy=L.LUMO_POLICY_WY)
+    paths, _b2 = _desc(policy=L.LUMO_POLICY_PATHS)
+    ok = L.lumo_gdn_prep(L.LUMO_PREP_QK_NORM, 1e-6, None, None)
+    assert _verify_prep(dw, paths, ok) == L.LUMO_EUNSUPPORTED          # needs a WY plan
+    assert _verify_prep(dw, wy, L.lumo_gdn_prep(4, 0.0, None, None)) == L.LUMO_EINVAL
+    assert _verify_prep(dw, wy, L.lumo_gdn_prep(L.LUMO_PREP_QK_NORM, -1.0, None, None)) == L.LUMO_EINVAL
+    assert _verify_prep(dw, wy, L.lumo_gdn_prep(L.LUMO_PREP_QK_NORM, float("nan"), None, None)) == L.LUMO_EINVAL
+    assert _verify_prep(dw, wy, L.lumo_gdn_prep(L.LUMO_PREP_RAW_GATES, 0.0, FAKE, None)) == L.LUMO_EINVAL
+    assert "a_log" in L.lumo_last_error()
+    assert _verify_prep(dw, wy, L.lumo_gdn_prep(L.LUMO_PREP_RAW_GATES, 0.0, FAKE + 2, FAKE)) == L.LUMO_EINVAL
+    P = ctypes.c_void_p
+    bad = L.lumo_gdn_prep(8, 0.0, None, None)
+    st = L._lib.lumo_gdn_commit_prep(ctypes.byref(_dims()), ctypes.byref(paths), ctypes.byref(bad), 4,
+                                     P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+                                     P(FAKE), 0, None, None, None)
+    assert st == L.LUMO_EINVAL
+
+
+def test_prep_empty_batch_is_a_no_op():
+    plan, blob = L.lumo_tree_plan(np.array([0], np.int32), np.zeros(0, np.int32),
+                                  np.zeros(0, np.int32), L.LUMO_POLICY_WY)
+    desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
+    d = _dims(n_req=0, h_k=1, h_v=1, d_k=128, d_v=128, op_dtype=1)
+    prep = L.lumo_gdn_prep(L.LUMO_PREP_QK_NORM | L.LUMO_PREP_RAW_GATES, 1e-6, FAKE, FAKE)
+    assert _verify_prep(d, desc, prep) == L.LUMO_OK

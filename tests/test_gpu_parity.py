@@ -563,3 +563,126 @@ def test_conv_tree_shapes(deep):
     assert gu.max_rel(got[:, rows], ref[:, rows]) <= gu.TOL_BF16
     pad = [r for r in range(wl.total_rows) if r not in set(rows.tolist())]
     assert np.all(got[:, pad] == 0)
+
+
+# ---------------------------------------------------------------- operand preparation
+
+QKN, RAWG = L.LUMO_PREP_QK_NORM, L.LUMO_PREP_RAW_GATES
+
+
+def _prep_inputs(wl, flags, seed, eps=1e-6):
+    """Raw operands for a prepared run: q and k rows rescaled by U(0.3, 3) (so the
+    normalisation matters), raw gate inputs a, b ~ N(0, 1), and per-(layer, head)
+    A_log ~ N(0, 0.5^2), dt_bias ~ N(0, 1). Returns (arrays, oracle Prep, device Prep)."""
+    rng = np.random.default_rng(seed)
+    a = dict(wl.arrays)
+    if flags & QKN:
+        for key in ("q", "k"):
+            f = ops.bf16_bits_to_f32(a[key]) * rng.uniform(0.3, 3.0, size=a[key].shape[:-1] + (1,))
+            a[key] = ops.to_bf16_bits(f.astype(np.float32))
+    if flags & RAWG:
+        a["g"] = rng.standard_normal(a["g"].shape).astype(np.float32)
+        a["beta"] = rng.standard_normal(a["beta"].shape).astype(np.float32)
+    a_log = (0.5 * rng.standard_normal((wl.n_layers, wl.h_v))).astype(np.float32)
+    dt_bias = rng.standard_normal((wl.n_layers, wl.h_v)).astype(np.float32)
+    oprep = oracle.Prep(flags, eps, a_log, dt_bias)
+    gprep = L.Prep(flags, eps, torch.from_numpy(a_log).cuda(), torch.from_numpy(dt_bias).cuda())
+    return a, oprep, gprep
+
+
+def _prep_step(wl, arrays, gprep, policy=L.LUMO_POLICY_WY):
+    return GdnTreeStep(n_req=wl.n_req, n_layers=wl.n_layers, h_k=wl.h_k, h_v=wl.h_v, d_k=wl.d_k,
+                       d_v=wl.d_v, op_dtype=wl.op_dtype, node_off=wl.node_off,
+                       parent=wl.parent_flat, n_rows=wl.n_rows,
+                       arrays={k: v for k, v in arrays.items() if k not in ("x", "hist", "w")},
+                       policy=policy, max_path=wl.max_path, accepted=wl.accepted, prep=gprep)
+
+
+def _check_prep_outputs(wl, o, arrays, oprep, inst, tol=gu.TOL_BF16):
+    worst = 0.0
+    for (r, l, h) in inst:
+        n = len(wl.parents[r])
+        if n == 0:
+            continue
+        ref = oracle.verify_nodes(wl, r, l, h, list(range(n)), arrays=arrays, prep=oprep)
+        got = o[l, gu.node_rows(wl, r), h, :]
+        assert np.all(np.isfinite(got)), (r, l, h)
+        e = gu.max_rel(got, ref)
+        worst = max(worst, e)
+        assert e <= tol, f"instance {(r, l, h)}: max rel err {e:.3e}"
+    return worst
+
+
+@pytest.mark.parametrize("flags", [QKN, RAWG, QKN | RAWG])
+def test_wy_prep_parity(flags):
+    """Operands prepared inside the WY kernel and the commit replay: outputs and the
+    published state against the oracle with the same preparation."""
+    wl = workload("layer1")
+    a, oprep, gprep = _prep_inputs(wl, flags, seed=71 + flags)
+    say(f"[gpu] wy prep flags={flags}")
+    st = _prep_step(wl, a, gprep)
+    st.verify()
+    st.commit()
+    torch.cuda.synchronize()
+    inst = [(0, 0, h) for h in range(wl.h_v)]
+    worst = _check_prep_outputs(wl, gu.to_np(st.o), a, oprep, inst)
+    say(f"  outputs worst max-rel {worst:.3e}")
+    ref_state, _, pl = oracle.commit(wl, arrays=a, prep=oprep)
+    assert np.array_equal(st.path_len.cpu().numpy(), pl)
+    ws = gu.check_states(wl, st.state.cpu().numpy(), ref_state, inst)
+    say(f"  published state worst max-rel {ws:.3e}")
+    # without the preparation the same raw operands give other outputs (the test has teeth)
+    plain = _prep_step(wl, a, None)
+    plain.verify()
+    torch.cuda.synchronize()
+    assert gu.max_rel(gu.to_np(plain.o)[0, gu.node_rows(wl, 0), 0], gu.to_np(st.o)[0, gu.node_rows(wl, 0), 0]) > 0.05
+
+
+def test_wy_prep_deep_and_groupings():
+    """Prepared operands with 17-node paths (16 path-stack registers) and one value head
+    per block (h_k = h_v)."""
+    rng = np.random.default_rng(73)
+    parents = [trees.chain(17), trees.random_tree(rng, 40, 9, trees.bmax_uniform(3)), trees.FIG1_PARENT]
+    wl = pins.make_wl(parents, d_k=128, d_v=128, h_k=4, h_v=4, op_dtype=ops.BF16,
+                      n_rows=[17, 41, 7], n_layers=2, max_path=17)
+    wl.arrays = ops.make_gdn_operands(74, n_req=3, n_layers=2, total_rows=65, h_k=4, h_v=4,
+                                      d_k=128, d_v=128, op_dtype=ops.BF16)
+    a, oprep, gprep = _prep_inputs(wl, QKN | RAWG, seed=75)
+    st = _prep_step(wl, a, gprep)
+    st.verify()
+    torch.cuda.synchronize()
+    inst = [(r, l, h) for r in range(3) for l in range(2) for h in (0, 3)]
+    _check_prep_outputs(wl, gu.to_np(st.o), a, oprep, inst)
+
+
+def test_commit_prep_on_scan_plan():
+    """The commit's preparation does not depend on the plan's policy."""
+    wl = workload("paper28")
+    a, oprep, gprep = _prep_inputs(wl, QKN | RAWG, seed=76)
+    st = _prep_step(wl, a, gprep, policy=L.LUMO_POLICY_PATHS)
+    st.commit()
+    torch.cuda.synchronize()
+    ref_state, _, _ = oracle.commit(wl, arrays=a, prep=oprep)
+    gu.check_states(wl, st.state.cpu().numpy(), ref_state,
+                    [(0, 0, h) for h in range(wl.h_v)])
+
+
+def test_verify_pending_prep():
+    """Deferred publication with prepared operands in both iterations."""
+    prev, cur = _pending_pair(2, 4, seed=77)
+    pa, poprep, gprep = _prep_inputs(prev, QKN | RAWG, seed=78)
+    # the current iteration uses the same gate parameters (same layers and heads)
+    ca, _, _ = _prep_inputs(cur, QKN | RAWG, seed=79)
+    sp = _prep_step(prev, pa, gprep, policy=L.LUMO_POLICY_PATHS)
+    sp.commit(defer=True)
+    sc = _prep_step(cur, ca, gprep)
+    sc.verify_pending(sp, state=sp.state)
+    torch.cuda.synchronize()
+    acc = prev.accepted.copy()
+    acc[3] = -1
+    ref_state, _, _ = oracle.commit(prev, accepted=acc, arrays=pa, prep=poprep)
+    inst = [(r, l, h) for r in range(5) for l in range(2) for h in range(4)]
+    gu.check_states(prev, sp.state.cpu().numpy(), ref_state, inst)
+    c2 = dict(ca)
+    c2["state0"] = ref_state.astype(np.float32)
+    _check_prep_outputs(cur, gu.to_np(sc.o), c2, poprep, inst)
