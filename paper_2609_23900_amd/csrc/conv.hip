@@ -298,7 +298,12 @@ hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.w = a.w;
     p.bias = a.bias;
     p.y = a.y;
-    if (d.op_dtype == LUMO_BF16 && pl.max_depth <= 16) {
+    // The depth-first walk reads every x row once but runs one block per (request, layer,
+    // channel block), each walking its request's nodes in sequence: it is chosen when
+    // that gives at least four blocks per CU; otherwise the run kernel's parallelism over
+    // node runs wins (measured: one request or one layer of 128-256-node trees).
+    const long dfs_blocks = (long)d.n_req * d.n_layers * p.n_cchunks;
+    if (d.op_dtype == LUMO_BF16 && pl.max_depth <= 16 && dfs_blocks >= 4 * 256) {
         ConvDfsParams q;
         q.blob = desc.blob;
         q.o_node_off = pl.o_node_off;

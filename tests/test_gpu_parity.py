@@ -534,28 +534,32 @@ def lumo_commit_into(st, bank):
 
 # ---------------------------------------------------------------- tree convolution shapes
 
-@pytest.mark.parametrize("deep", [False, True])
-def test_conv_tree_shapes(deep):
-    """Paths of 16 nodes (the depth-first kernel's limit) or 20 (the run kernel), a request
-    without nodes, a partial channel block (2056 = 2048 + 8), two layers, bias."""
+@pytest.mark.parametrize("case", ["depth_first", "runs_deep", "runs_few_blocks"])
+def test_conv_tree_shapes(case):
+    """Both conv kernels on edge shapes: paths of 16 nodes (the depth-first kernel's limit)
+    or 20 (run kernel), a request without nodes, a partial channel block, bias. The
+    depth-first kernel is used when it has at least 1024 blocks (requests x layers x
+    channel blocks): 4 x 52 x 5 here."""
     rng = np.random.default_rng(41)
+    deep = case == "runs_deep"
+    n_layers, C = (52, 8200) if case == "depth_first" else (2, 2056)
     parents = [trees.chain(20 if deep else 16), np.zeros(0, np.int32), trees.FIG1_PARENT,
                trees.random_tree(rng, 40, 8, trees.bmax_uniform(4))]
     n_rows = [len(parents[0]) + 1, 1, 7, 40]
-    wl = pins.make_wl(parents, d_k=128, d_v=128, op_dtype=ops.BF16, n_rows=n_rows, n_layers=2,
-                      max_path=24, channels=2056)
-    wl.arrays = ops.make_conv_operands(43, n_req=4, n_layers=2, total_rows=wl.total_rows,
-                                       channels=2056, op_dtype=ops.BF16)
-    bias = rng.standard_normal((2, 2056)).astype(np.float32)
-    say(f"[gpu] conv shapes deep={deep}")
+    wl = pins.make_wl(parents, d_k=128, d_v=128, op_dtype=ops.BF16, n_rows=n_rows, n_layers=n_layers,
+                      max_path=24, channels=C)
+    wl.arrays = ops.make_conv_operands(43, n_req=4, n_layers=n_layers, total_rows=wl.total_rows,
+                                       channels=C, op_dtype=ops.BF16)
+    bias = rng.standard_normal((n_layers, C)).astype(np.float32)
+    say(f"[gpu] conv shapes {case}")
     desc = L.TreeDesc.build(wl.node_off, wl.parent_flat, wl.n_rows)
-    d = L.dims(4, 2, 1, 1, 128, 128, L.LUMO_BF16)
+    d = L.dims(4, n_layers, 1, 1, 128, 128, L.LUMO_BF16)
     x = torch.from_numpy(wl.arrays["x"]).view(torch.bfloat16).cuda()
     hist = torch.from_numpy(wl.arrays["hist"]).view(torch.bfloat16).cuda()
     w = torch.from_numpy(wl.arrays["w"]).cuda()
     b = torch.from_numpy(bias).cuda()
-    y = torch.zeros((2, wl.total_rows, 2056), dtype=torch.bfloat16, device="cuda")
-    L.lumo_tree_conv_gather(d, desc, 2056, x, hist, w, b, 1, y)
+    y = torch.zeros((n_layers, wl.total_rows, C), dtype=torch.bfloat16, device="cuda")
+    L.lumo_tree_conv_gather(d, desc, C, x, hist, w, b, 1, y)
     torch.cuda.synchronize()
     got = gu.to_np(y)
     ref = oracle.conv_all(wl, bias=bias)
