@@ -74,8 +74,9 @@ def _load(path):
     L.orc_commit.argtypes = [ctypes.POINTER(Dims), P, P, P, P, I, P, P, P, P, P, P, P, P, I]
     L.orc_conv_all.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P, I, P]
     L.orc_conv_hist_publish.argtypes = [I, I, I, I, I, P, P, P, P, I, P, P, P]
+    L.orc_tree_attention.argtypes = [I, I, I, I, I, P, P, P, P, ctypes.c_double, P, P, P, P, P, P, P, I]
     for f in ("orc_verify_nodes", "orc_verify_all", "orc_commit", "orc_conv_all",
-              "orc_conv_hist_publish", "orc_max_threads"):
+              "orc_conv_hist_publish", "orc_tree_attention", "orc_max_threads"):
         getattr(L, f).restype = I
     return L
 
@@ -204,3 +205,28 @@ def conv_hist_publish(wl, path_out, path_len, *, arrays=None):
                                 _p(_op(a["x"], wl.op_dtype)), _p(_op(a["hist"], wl.op_dtype)),
                                 _p(out))
     return out
+
+
+def tree_attention(parents, row_off, total_rows, ctx_off, q, k_ctx, v_ctx, k_tree, v_tree, *,
+                   h_q, h_kv, d, op_dtype, scale=None, n_threads=None):
+    """(o [rows][h_q][d], lse [rows][h_q]) in fp64; rows without a node are NaN.
+
+    Row i of request r attends to its context tokens ctx_off[r] .. ctx_off[r+1]-1 and to
+    the tree nodes of its own root-to-node path (Sec. V-B)."""
+    node_off = np.zeros(len(parents) + 1, np.int32)
+    node_off[1:] = np.cumsum([len(p) for p in parents])
+    parent_flat = np.concatenate([np.asarray(p, np.int32) for p in parents]) if len(parents) else np.zeros(0, np.int32)
+    rows = plan.flat_rows(parents, row_off) if len(parents) else np.zeros(0, np.int32)
+    o = np.full((total_rows, h_q, d), np.nan, np.float64)
+    lse = np.full((total_rows, h_q), np.nan, np.float64)
+    sc = 1.0 / np.sqrt(d) if scale is None else float(scale)
+    nt = n_threads or lib().orc_max_threads()
+    rc = lib().orc_tree_attention(len(parents), h_q, h_kv, d, op_dtype, _p(node_off),
+                                  _p(_c(parent_flat, np.int32)), _p(_c(rows, np.int32)),
+                                  _p(_c(ctx_off, np.int32)), sc, _p(_op(q, op_dtype)),
+                                  _p(_op(k_ctx, op_dtype)), _p(_op(v_ctx, op_dtype)),
+                                  _p(_op(k_tree, op_dtype)), _p(_op(v_tree, op_dtype)), _p(o), _p(lse),
+                                  int(nt))
+    if rc:
+        raise ValueError("oracle: malformed tree")
+    return o, lse

@@ -23,6 +23,8 @@
  *     packed rows); the window is the last four entries, taps applied oldest to
  *     newest.
  *
+ *   - Sec. V-B tree attention: every query row sees the committed context and its
+ *     own ancestry (plain two-pass softmax in fp64, orc_tree_attention).
  *   - Sec. IV-B operand preparation (optional, prep_flags): verification takes raw
  *     gate inputs and normalises queries and keys itself. With ORC_PREP_QK_NORM
  *     every query and key row x is used as x / sqrt(|x|^2 + qk_eps); with
@@ -387,6 +389,78 @@ int orc_conv_hist_publish(int n_req, int n_layers, int total_rows, int channels,
             }
     }
     return 0;
+}
+
+/*
+ * Tree attention (Sec. V-B; Sec. III-A visibility): query row i of request r sees the
+ * request's committed context (tokens ctx_off[r] .. ctx_off[r+1]-1) and the tree nodes
+ * on its own root-to-node path, itself included; pad rows are invisible. For query head
+ * h (key/value head h / (h_q / h_kv)):
+ *   s_j = scale * (q_i . k_j)  over the visible keys j,
+ *   o_i = sum_j exp(s_j - lse) v_j,  lse = log sum_j exp(s_j).
+ * q [rows][h_q][d]; k_tree, v_tree [rows][h_kv][d] at the tree's physical rows;
+ * k_ctx, v_ctx [tokens][h_kv][d]. o [rows][h_q][d] and lse [rows][h_q] in fp64 (rows
+ * that hold no node are left untouched). Returns 0, or -1 on a malformed tree.
+ */
+int orc_tree_attention(int n_req, int h_q, int h_kv, int d, int op_dtype, const int* node_off,
+                       const int* parent, const int* row, const int* ctx_off, double scale,
+                       const void* q, const void* k_ctx, const void* v_ctx, const void* k_tree,
+                       const void* v_tree, double* o, double* lse, int n_threads) {
+    int bad = 0;
+    const int grp = h_q / h_kv;
+#ifdef _OPENMP
+#pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads > 0 ? n_threads : 1) reduction(| : bad)
+#endif
+    for (int r = 0; r < n_req; ++r) {
+        const int n = node_off[r + 1] - node_off[r];
+        const int* par = parent + node_off[r];
+        const int* rw = row + node_off[r];
+        const long c0 = ctx_off[r], nc = ctx_off[r + 1] - ctx_off[r];
+        int* path = (int*)malloc(sizeof(int) * (size_t)(n > 0 ? n : 1));
+        double* sc = (double*)malloc(sizeof(double) * (size_t)(nc + n + 1));
+        double* acc = (double*)malloc(sizeof(double) * (size_t)d);
+        if (!path || !sc || !acc) {
+            bad |= 1;
+        } else {
+            for (int i = 0; i < n && !bad; ++i) {
+                const int len = ancestry(par, n, i, path, n);
+                if (len < 0) {
+                    bad |= 1;
+                    break;
+                }
+                for (int h = 0; h < h_q; ++h) {
+                    const int hk = h / grp;
+                    const long qb = ((long)rw[i] * h_q + h) * d;
+                    /* scores: context first, then the path root first */
+                    double mx = -INFINITY;
+                    for (long t = 0; t < nc + len; ++t) {
+                        const void* kk = t < nc ? k_ctx : k_tree;
+                        const long kb = t < nc ? ((c0 + t) * h_kv + hk) * d : ((long)rw[path[t - nc]] * h_kv + hk) * d;
+                        double s = 0.0;
+                        for (int e = 0; e < d; ++e) s += ld_op(q, qb + e, op_dtype) * ld_op(kk, kb + e, op_dtype);
+                        sc[t] = scale * s;
+                        if (sc[t] > mx) mx = sc[t];
+                    }
+                    double sum = 0.0;
+                    for (int e = 0; e < d; ++e) acc[e] = 0.0;
+                    for (long t = 0; t < nc + len; ++t) {
+                        const double w = exp(sc[t] - mx);
+                        sum += w;
+                        const void* vv = t < nc ? v_ctx : v_tree;
+                        const long vb = t < nc ? ((c0 + t) * h_kv + hk) * d : ((long)rw[path[t - nc]] * h_kv + hk) * d;
+                        for (int e = 0; e < d; ++e) acc[e] += w * ld_op(vv, vb + e, op_dtype);
+                    }
+                    for (int e = 0; e < d; ++e) o[qb + e] = acc[e] / sum;
+                    lse[(long)rw[i] * h_q + h] = mx + log(sum);
+                }
+            }
+        }
+        free(path);
+        free(sc);
+        free(acc);
+    }
+    (void)n_threads;
+    return bad ? -1 : 0;
 }
 
 int orc_max_threads(void) {

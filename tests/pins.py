@@ -558,4 +558,111 @@ def pin_prep_commit_equals_node_state():
     np.testing.assert_array_equal(pub[0, 0, 1], st[0])
 
 
+# --------------------------------------------------------------------------- tree attention
+
+def _attn_case(rng, parents, n_ctx, h_q, h_kv, d, n_rows=None, scale_q=1.0):
+    n_rows = [len(p) for p in parents] if n_rows is None else n_rows
+    row_off = np.concatenate([[0], np.cumsum(n_rows)]).astype(np.int32)
+    total = int(row_off[-1])
+    ctx_off = np.concatenate([[0], np.cumsum(n_ctx)]).astype(np.int32)
+    a = dict(q=(scale_q * rng.standard_normal((total, h_q, d))).astype(np.float32),
+             k_tree=rng.standard_normal((total, h_kv, d)).astype(np.float32),
+             v_tree=rng.standard_normal((total, h_kv, d)).astype(np.float32),
+             k_ctx=rng.standard_normal((int(ctx_off[-1]), h_kv, d)).astype(np.float32),
+             v_ctx=rng.standard_normal((int(ctx_off[-1]), h_kv, d)).astype(np.float32))
+    return row_off, total, ctx_off, a
+
+
+def _attn(parents, row_off, total, ctx_off, a, h_q, h_kv, d, scale=None):
+    return oracle.tree_attention(parents, row_off, total, ctx_off, a["q"], a["k_ctx"], a["v_ctx"],
+                                 a["k_tree"], a["v_tree"], h_q=h_q, h_kv=h_kv, d=d, op_dtype=0,
+                                 scale=scale)
+
+
+def pin_attention_root_only():
+    """A root with no context sees only itself: o = v_root, lse = scale q.k."""
+    rng = np.random.default_rng(81)
+    row_off, total, ctx_off, a = _attn_case(rng, [np.array([-1], np.int32)], [0], 2, 1, 8)
+    o, lse = _attn([np.array([-1], np.int32)], row_off, total, ctx_off, a, 2, 1, 8, scale=0.7)
+    for h in range(2):
+        np.testing.assert_allclose(o[0, h], a["v_tree"][0, 0], rtol=1e-15)
+        want = 0.7 * float(a["q"][0, h].astype(np.float64) @ a["k_tree"][0, 0].astype(np.float64))
+        np.testing.assert_allclose(lse[0, h], want, rtol=1e-14)
+
+
+def pin_attention_uniform_scores():
+    """q = 0: every visible key weighs the same, so o is the mean of the visible values
+    (the context and the node's own path) and lse = log(number of visible keys)."""
+    rng = np.random.default_rng(82)
+    par = trees.FIG1_PARENT
+    row_off, total, ctx_off, a = _attn_case(rng, [par], [5], 2, 2, 4, scale_q=0.0)
+    rows = oracle.plan.rows_of(par, 0)
+    o, lse = _attn([par], row_off, total, ctx_off, a, 2, 2, 4)
+    for i in range(len(par)):
+        path = oracle.plan.ancestry(par, i)
+        for h in range(2):
+            vis = [a["v_ctx"][t, h] for t in range(5)] + [a["v_tree"][rows[x], h] for x in path]
+            np.testing.assert_allclose(o[rows[i], h], np.mean(np.array(vis, np.float64), 0), rtol=1e-13, atol=1e-15)
+            np.testing.assert_allclose(lse[rows[i], h], np.log(5 + len(path)), rtol=1e-14)
+
+
+def pin_attention_dense_masked_softmax():
+    """Against a dense formulation: visibility from boolean reachability powers of the
+    parent matrix, scores by matrix product, masked softmax; two requests, grouped heads."""
+    rng = np.random.default_rng(83)
+    parents = [trees.random_tree(rng, 13, 5, trees.bmax_uniform(3)), trees.FIG1_PARENT]
+    n_ctx = [6, 3]
+    h_q, h_kv, d = 4, 2, 8
+    row_off, total, ctx_off, a = _attn_case(rng, parents, n_ctx, h_q, h_kv, d, n_rows=[15, 7])
+    o, lse = _attn(parents, row_off, total, ctx_off, a, h_q, h_kv, d, scale=0.35)
+    for r, par in enumerate(parents):
+        n = len(par)
+        A = np.zeros((n, n), bool)
+        for i, p_ in enumerate(par):
+            if p_ >= 0:
+                A[i, p_] = True
+        vis = np.eye(n, dtype=bool)
+        step = np.eye(n, dtype=bool)
+        for _ in range(n):
+            step = (step.astype(int) @ A.astype(int)) > 0
+            vis |= step
+        rows = np.array(oracle.plan.rows_of(par, int(row_off[r])))
+        ctx = slice(int(ctx_off[r]), int(ctx_off[r + 1]))
+        for h in range(h_q):
+            g = h // (h_q // h_kv)
+            Q = a["q"][rows, h].astype(np.float64)
+            K = np.concatenate([a["k_ctx"][ctx, g], a["k_tree"][rows, g]]).astype(np.float64)
+            V = np.concatenate([a["v_ctx"][ctx, g], a["v_tree"][rows, g]]).astype(np.float64)
+            S = 0.35 * Q @ K.T
+            mask = np.concatenate([np.ones((n, n_ctx[r]), bool), vis], axis=1)
+            S = np.where(mask, S, -np.inf)
+            m = S.max(1, keepdims=True)
+            P = np.exp(S - m)
+            want_l = np.log(P.sum(1)) + m[:, 0]
+            want_o = (P / P.sum(1, keepdims=True)) @ V
+            np.testing.assert_allclose(o[rows, h], want_o, rtol=1e-11, atol=1e-13)
+            np.testing.assert_allclose(lse[rows, h], want_l, rtol=1e-12)
+
+
+def pin_attention_context_order_and_padding():
+    """Permuting the context tokens changes nothing; NaN in pad rows of the tree keys
+    and values is never read."""
+    rng = np.random.default_rng(84)
+    par = trees.random_tree(rng, 10, 4, trees.bmax_uniform(3))
+    row_off, total, ctx_off, a = _attn_case(rng, [par], [9], 2, 1, 6, n_rows=[12])
+    o1, l1 = _attn([par], row_off, total, ctx_off, a, 2, 1, 6)
+    perm = rng.permutation(9)
+    b = dict(a)
+    b["k_ctx"], b["v_ctx"] = a["k_ctx"][perm], a["v_ctx"][perm]
+    rows = oracle.plan.rows_of(par, 0)
+    pad = [x for x in range(12) if x not in rows]
+    for key in ("k_tree", "v_tree", "q"):
+        b[key] = b[key].copy()
+        b[key][pad] = np.nan
+    o2, l2 = _attn([par], row_off, total, ctx_off, b, 2, 1, 6)
+    np.testing.assert_allclose(o2[rows], o1[rows], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(l2[rows], l1[rows], rtol=1e-13)
+    assert np.all(np.isfinite(o2[rows]))
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]

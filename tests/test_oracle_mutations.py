@@ -46,6 +46,14 @@ MUTATIONS = {
     "query_not_normalised": ("    qk_prepare(d, qv, dk);\n", ""),
     "raw_gate_without_dt_bias": ("const double x = g_in + (double)d->dt_bias[lh];", "const double x = g_in;"),
     "raw_beta_sign": ("*beta = 1.0 / (1.0 + exp(-b_in));", "*beta = 1.0 / (1.0 + exp(b_in));"),
+    "attn_drops_last_context": ("const long c0 = ctx_off[r], nc = ctx_off[r + 1] - ctx_off[r];",
+                                "const long c0 = ctx_off[r], nc = ctx_off[r + 1] - ctx_off[r] - (ctx_off[r + 1] > ctx_off[r]);"),
+    "attn_kv_head_modulo": ("const int hk = h / grp;", "const int hk = h % h_kv;"),
+    "attn_no_scale": ("sc[t] = scale * s;", "sc[t] = s;"),
+    "attn_value_of_parent": ("const long vb = t < nc ? ((c0 + t) * h_kv + hk) * d : ((long)rw[path[t - nc]] * h_kv + hk) * d;",
+                             "const long vb = t < nc ? ((c0 + t) * h_kv + hk) * d : ((long)rw[path[t - nc > 0 ? t - nc - 1 : 0]] * h_kv + hk) * d;"),
+    "attn_excludes_self": ("for (long t = 0; t < nc + len; ++t) {\n                        const void* kk",
+                           "for (long t = 0; t < nc + len - (len > 1); ++t) {\n                        const void* kk"),
 }
 
 
