@@ -9,7 +9,8 @@
  *   lumo_tree_gdn_verify   device: every node's recurrent output from its ancestry
  *   lumo_gdn_commit        device: derive the accepted path, replay it into the
  *                          native state, publish the convolution history
- * plus a captured-graph form of the commit; lumo_tree_gdn_verify_pending, which
+ * plus lumo_tree_attention (the attention layers' tree verification), a
+ * captured-graph form of the commit; lumo_tree_gdn_verify_pending, which
  * folds the replay of one iteration into the verification of the next; and forms
  * that prepare the operands inside the kernels (lumo_gdn_prep: query/key
  * normalisation, gates from raw inputs).
@@ -115,6 +116,8 @@ typedef struct {
     /* preorder tables (chunks of 32 preorder positions per request) */
     int32_t n_chunks;    /* chunks over all requests                            */
     int32_t o_pre_row, o_pre_depth, o_pre_ci, o_chunk_off, o_chunk_stack;
+    /* attention visibility, per node in slot order */
+    int32_t o_vis;
 } lumo_plan;
 
 /* A plan whose blob has been copied to device memory. */
@@ -160,7 +163,10 @@ typedef struct {
  *   chunk of 32, else 16 + its offset in the chunk; 0xff past the node's depth),
  *   chunk_off[n_req+1],
  *   chunk_stack[n_chunks][16] (rows of the ancestors of each chunk's first node by
- *   depth, -1 beyond its depth).
+ *   depth, -1 beyond its depth),
+ *   vis[N][2] (per node in slot order, node_off[r] + slot: its preorder position and
+ *   the position one past its subtree; node a is an ancestor-or-self of node i iff
+ *   vis[a][0] <= vis[i][0] < vis[a][1]).
  * Returns LUMO_EDESC for malformed trees, LUMO_ESPACE (with out->n_words set)
  * when blob is NULL or too small, LUMO_EINVAL for bad arguments.
  */
@@ -321,6 +327,45 @@ lumo_status lumo_gdn_commit_prep(const lumo_gdn_dims* dims, const lumo_tree_desc
                                  const void* x, void* conv_hist, void* stream);
 
 /* Opaque captured commit (Sec. V-A: one fixed-shape committer graph). */
+/*
+ * Tree attention (Sec. V-B; visibility Sec. III-A): the attention layers' verification
+ * of the same candidate tree. Query row i (a tree node) attends to its request's
+ * committed context and to the tree nodes on its own root-to-node path, itself
+ * included; pad rows are invisible:
+ *   s_j = scale (q_i . k_j),  o_i = sum_j exp(s_j - lse_i) v_j,  lse_i = log sum_j exp(s_j)
+ * over those keys j. Query head h reads key/value head h / (h_q / h_kv).
+ *   lumo_attn_dims  n_req; h_q, h_kv with h_q / h_kv in {1, 2, 4, 8}; d = 128;
+ *                   op_dtype = LUMO_BF16
+ *   q           [total_rows][h_q][d] at the tree's physical rows (spine first)
+ *   k_tree, v_tree  [total_rows][h_kv][d], the tree nodes' own keys and values at the
+ *               same rows (spine-contiguous)
+ *   k_ctx, v_ctx    [tokens][h_kv][d]; request r's context is tokens
+ *               ctx_off[r] .. ctx_off[r+1]-1 (ctx_off device int32 [n_req+1])
+ *   max_ctx     host, >= every request's context length
+ *   scale       softmax scale (> 0)
+ *   o           [total_rows][h_q][d] op_dtype, written at node rows only
+ *   lse         [total_rows][h_q] fp32 natural log, written at node rows only
+ *   n_split     context partitions reduced separately and combined (split-K), >= 1;
+ *               lumo_tree_attention_splits suggests one that fills the device
+ *   workspace   >= lumo_tree_attention_workspace_bytes(dims, plan, n_split) bytes
+ * Keys are reduced context first (partition by partition), then the tree nodes in
+ * physical slot order; the reduction order is fixed for given shapes and n_split.
+ * All pointers 16-byte aligned; LUMO_EUNSUPPORTED for other shapes.
+ */
+typedef struct {
+    int32_t n_req, h_q, h_kv, d, op_dtype;
+} lumo_attn_dims;
+
+size_t lumo_tree_attention_workspace_bytes(const lumo_attn_dims* dims, const lumo_plan* plan,
+                                           int32_t n_split);
+int32_t lumo_tree_attention_splits(const lumo_attn_dims* dims, const lumo_plan* plan, int32_t max_ctx);
+lumo_status lumo_tree_attention(const lumo_attn_dims* dims, const lumo_tree_desc* desc,
+                                const int32_t* ctx_off, int32_t max_ctx, float scale,
+                                const void* q, const void* k_ctx, const void* v_ctx,
+                                const void* k_tree, const void* v_tree, void* o, float* lse,
+                                int32_t n_split, void* workspace, size_t workspace_bytes,
+                                void* stream);
+
 typedef struct lumo_commit_graph lumo_commit_graph;
 
 /*

@@ -5,7 +5,8 @@ kernels; torch tensors only provide device memory and the current HIP stream.
 The functions keep the names of the C ABI (include/lumo_tree.h):
   lumo_tree_plan, lumo_tree_gdn_workspace_bytes, lumo_tree_conv_gather,
   lumo_tree_gdn_verify, lumo_tree_gdn_verify_prep, lumo_tree_gdn_verify_pending, lumo_gdn_commit,
-  lumo_gdn_commit_prep, lumo_gdn_commit_graph_create,
+  lumo_gdn_commit_prep, lumo_tree_attention, lumo_tree_attention_workspace_bytes,
+  lumo_tree_attention_splits, lumo_gdn_commit_graph_create,
   lumo_gdn_commit_graph_launch, lumo_gdn_commit_graph_destroy, lumo_last_error,
   lumo_version.
 Device arguments are torch tensors on the GPU (or None where the ABI allows NULL);
@@ -50,7 +51,7 @@ _PLAN_FIELDS = ("n_req", "total_nodes", "total_rows", "max_nodes", "max_depth", 
                 "o_parent", "o_depth", "o_slot", "o_row", "o_conv_src", "o_path_off",
                 "o_path_leaf", "o_spine_off", "o_spine", "o_level_off", "o_seg", "o_seg_nodes",
                 "o_dfs", "o_dfs_pos", "n_chunks", "o_pre_row", "o_pre_depth",
-                "o_pre_ci", "o_chunk_off", "o_chunk_stack")
+                "o_pre_ci", "o_chunk_off", "o_chunk_stack", "o_vis")
 
 
 class lumo_plan(ctypes.Structure):
@@ -59,6 +60,10 @@ class lumo_plan(ctypes.Structure):
 
 class lumo_tree_desc(ctypes.Structure):
     _fields_ = [("blob", ctypes.c_void_p), ("host_blob", ctypes.c_void_p), ("plan", lumo_plan)]
+
+
+class lumo_attn_dims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("n_req", "h_q", "h_kv", "d", "op_dtype")]
 
 
 LUMO_PREP_QK_NORM, LUMO_PREP_RAW_GATES = 1, 2
@@ -96,6 +101,12 @@ def _load():
     L.lumo_tree_conv_gather.argtypes = [PD, PT, I32, P, P, P, P, I32, P, P]
     L.lumo_tree_gdn_verify.argtypes = [PD, PT, P, P, P, P, P, P, P, P, P, SZ, I32, P]
     PP = ctypes.POINTER(lumo_gdn_prep)
+    PA = ctypes.POINTER(lumo_attn_dims)
+    L.lumo_tree_attention_workspace_bytes.argtypes = [PA, ctypes.POINTER(lumo_plan), I32]
+    L.lumo_tree_attention_workspace_bytes.restype = SZ
+    L.lumo_tree_attention_splits.argtypes = [PA, ctypes.POINTER(lumo_plan), I32]
+    L.lumo_tree_attention_splits.restype = I32
+    L.lumo_tree_attention.argtypes = [PA, PT, P, I32, ctypes.c_float, P, P, P, P, P, P, P, I32, P, SZ, P]
     L.lumo_tree_gdn_verify_prep.argtypes = [PD, PT, PP, P, P, P, P, P, P, P, P]
     L.lumo_tree_gdn_verify_pending.argtypes = [PD, PT, PP, P, P, P, P, P, P, P, PT, I32, P, P, P, P, P, P,
                                                P]
@@ -110,7 +121,7 @@ def _load():
     L.lumo_version.restype = ctypes.c_char_p
     for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_gdn_verify",
               "lumo_tree_gdn_verify_prep", "lumo_tree_gdn_verify_pending", "lumo_gdn_commit",
-              "lumo_gdn_commit_prep", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
+              "lumo_gdn_commit_prep", "lumo_tree_attention", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -248,6 +259,27 @@ def lumo_gdn_commit_prep(d, desc: TreeDesc, prep: Prep | None, max_path, accepte
                                      _dptr(path_len), _dptr(k), _dptr(v), _dptr(g), _dptr(beta),
                                      _dptr(state), int(channels), _dptr(x), _dptr(conv_hist),
                                      _stream(stream)))
+
+
+def attn_dims(n_req, h_q, h_kv, d=128, op_dtype=LUMO_BF16) -> lumo_attn_dims:
+    return lumo_attn_dims(n_req, h_q, h_kv, d, op_dtype)
+
+
+def lumo_tree_attention_workspace_bytes(d: lumo_attn_dims, plan: lumo_plan, n_split) -> int:
+    return int(_lib.lumo_tree_attention_workspace_bytes(ctypes.byref(d), ctypes.byref(plan), int(n_split)))
+
+
+def lumo_tree_attention_splits(d: lumo_attn_dims, plan: lumo_plan, max_ctx) -> int:
+    return int(_lib.lumo_tree_attention_splits(ctypes.byref(d), ctypes.byref(plan), int(max_ctx)))
+
+
+def lumo_tree_attention(d, desc: TreeDesc, ctx_off, max_ctx, scale, q, k_ctx, v_ctx, k_tree, v_tree,
+                        o, lse, n_split, workspace, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib.lumo_tree_attention(ctypes.byref(d), ctypes.byref(desc.desc), _dptr(ctx_off),
+                                    int(max_ctx), float(scale), _dptr(q), _dptr(k_ctx), _dptr(v_ctx),
+                                    _dptr(k_tree), _dptr(v_tree), _dptr(o), _dptr(lse), int(n_split),
+                                    _dptr(workspace), ws_bytes, _stream(stream)))
 
 
 class CommitGraph:

@@ -9,6 +9,8 @@
 #include "internal.h"
 #include "launch.h"
 
+#include <algorithm>
+
 namespace lumo {
 
 namespace {
@@ -315,6 +317,74 @@ extern "C" lumo_status lumo_gdn_commit_prep(const lumo_gdn_dims* dims, const lum
     if (dims->n_req == 0) return LUMO_OK;
     CommitArgs a{max_path, accepted_node, path_out, path_len, k, v, g, beta, state, channels, x, conv_hist, pr};
     hipError_t e = launch_commit(*dims, *desc, a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
+namespace {
+lumo_status check_attn_dims(const lumo_attn_dims* d, const char* fn) {
+    if (!d) return fail(LUMO_EINVAL, "%s: dims is NULL", fn);
+    if (d->n_req < 0 || d->h_q < 1 || d->h_kv < 1) return fail(LUMO_ESHAPE, "%s: need n_req >= 0, h_q, h_kv >= 1", fn);
+    if (d->h_q % d->h_kv) return fail(LUMO_ESHAPE, "%s: h_q (%d) is not a multiple of h_kv (%d)", fn, d->h_q, d->h_kv);
+    const int grp = d->h_q / d->h_kv;
+    if (grp != 1 && grp != 2 && grp != 4 && grp != 8)
+        return fail(LUMO_EUNSUPPORTED, "%s: h_q / h_kv = %d (supported: 1, 2, 4, 8)", fn, grp);
+    if (d->d != 128 || d->op_dtype != LUMO_BF16)
+        return fail(LUMO_EUNSUPPORTED, "%s: built for bf16 with d = 128 (got d = %d, dtype %d)", fn, d->d, d->op_dtype);
+    return LUMO_OK;
+}
+}  // namespace
+
+extern "C" size_t lumo_tree_attention_workspace_bytes(const lumo_attn_dims* d, const lumo_plan* p, int32_t n_split) {
+    if (!d || !p || n_split < 1) return 0;
+    return (size_t)(n_split + 1) * p->total_rows * d->h_q * (128 + 1) * sizeof(float);
+}
+
+extern "C" int32_t lumo_tree_attention_splits(const lumo_attn_dims* d, const lumo_plan* p, int32_t max_ctx) {
+    if (!d || !p || d->h_kv < 1) return 1;
+    // about four blocks per CU of 256, partitions of at least 256 context tokens
+    const long per_split = (long)d->n_req * d->h_kv * ((p->max_nodes + 31) / 32);
+    long n = per_split > 0 ? (1024 + per_split - 1) / per_split : 1;
+    const long cap = std::max<long>(1, (max_ctx + 255) / 256);
+    n = std::min(n, cap);
+    return (int32_t)std::max<long>(1, std::min<long>(n, 4096));
+}
+
+extern "C" lumo_status lumo_tree_attention(const lumo_attn_dims* dims, const lumo_tree_desc* desc,
+                                           const int32_t* ctx_off, int32_t max_ctx, float scale, const void* q,
+                                           const void* k_ctx, const void* v_ctx, const void* k_tree,
+                                           const void* v_tree, void* o, float* lse, int32_t n_split,
+                                           void* workspace, size_t workspace_bytes, void* stream) {
+    static const char* fn = "lumo_tree_attention";
+    clear_error();
+    LUMO_TRY(check_attn_dims(dims, fn));
+    if (!desc) return fail(LUMO_EINVAL, "%s: desc is NULL", fn);
+    const lumo_plan& pl = desc->plan;
+    if (pl.n_req != dims->n_req) return fail(LUMO_EDESC, "%s: plan has %d requests, dims %d", fn, pl.n_req, dims->n_req);
+    if (!desc->blob) return fail(LUMO_EINVAL, "%s: desc blob is NULL", fn);
+    if (n_split < 1 || n_split > 4096) return fail(LUMO_EINVAL, "%s: n_split %d (1..4096)", fn, n_split);
+    if (max_ctx < 0) return fail(LUMO_EINVAL, "%s: max_ctx %d", fn, max_ctx);
+    if (!(scale > 0.f && scale < 3.0e38f)) return fail(LUMO_EINVAL, "%s: scale must be positive and finite", fn);
+    if (dims->n_req == 0 || pl.total_nodes == 0) return LUMO_OK;
+    LUMO_TRY(check_ptr(ctx_off, fn, "ctx_off"));
+    LUMO_TRY(check_ptr(q, fn, "q"));
+    LUMO_TRY(check_ptr(k_tree, fn, "k_tree"));
+    LUMO_TRY(check_ptr(v_tree, fn, "v_tree"));
+    LUMO_TRY(check_ptr(o, fn, "o"));
+    LUMO_TRY(check_ptr(lse, fn, "lse"));
+    if (max_ctx > 0) {
+        LUMO_TRY(check_ptr(k_ctx, fn, "k_ctx"));
+        LUMO_TRY(check_ptr(v_ctx, fn, "v_ctx"));
+    } else {
+        k_ctx = k_tree;  // never read: every context range is empty
+        v_ctx = v_tree;
+    }
+    const size_t need = lumo_tree_attention_workspace_bytes(dims, &pl, n_split);
+    LUMO_TRY(check_ptr(workspace, fn, "workspace"));
+    if (workspace_bytes < need) return fail(LUMO_ESPACE, "%s: workspace needs %zu bytes, got %zu", fn, need, workspace_bytes);
+    AttnArgs a{ctx_off, max_ctx, n_split, scale, q, k_ctx, v_ctx, k_tree, v_tree, o, lse, static_cast<float*>(workspace)};
+    hipError_t e = launch_attention(*dims, *desc, a, static_cast<hipStream_t>(stream));
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not available in this build", fn);
     if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return LUMO_OK;
 }

@@ -83,4 +83,22 @@ struct ConvArgs {
 
 hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const ConvArgs& a, hipStream_t s);
 
+// Tree attention: split-K partial kernel plus the merge (workspace: n_split + 1 ranges).
+struct AttnArgs {
+    const int32_t* ctx_off;
+    int32_t max_ctx;
+    int32_t n_split;
+    float scale;
+    const void* q;
+    const void* k_ctx;
+    const void* v_ctx;
+    const void* k_tree;
+    const void* v_tree;
+    void* o;
+    float* lse;
+    float* ws;
+};
+int attn_part_len(int max_ctx, int n_split);
+hipError_t launch_attention(const lumo_attn_dims& d, const lumo_tree_desc& desc, const AttnArgs& a, hipStream_t s);
+
 }  // namespace lumo

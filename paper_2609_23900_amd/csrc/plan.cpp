@@ -276,6 +276,7 @@ extern "C" lumo_status lumo_tree_plan(int32_t n_req, const int32_t* node_off, co
     p.o_pre_ci = take((int64_t)lumo::kPreCiWords * N);
     p.o_chunk_off = take(n_req + 1);
     p.o_chunk_stack = take((int64_t)lumo::kPreStack * p.n_chunks);
+    p.o_vis = take(2 * N);
     if (w > (int64_t(1) << 30)) return lumo::fail(LUMO_ESHAPE, "lumo_tree_plan: plan too large");
     p.n_words = (int32_t)w;
     *out = p;
@@ -321,6 +322,20 @@ extern "C" lumo_status lumo_tree_plan(int32_t n_req, const int32_t* node_off, co
     }
     b[p.o_path_off + n_req] = np;
     b[p.o_spine_off + n_req] = ns;
+    // attention visibility: per node (slot order) its preorder interval [pos, pos + subtree)
+    for (int r = 0; r < n_req; ++r) {
+        const ReqTree& t = tr[r];
+        const int base = node_off[r];
+        std::vector<int> size(t.n, 1);
+        for (int pos = t.n - 1; pos > 0; --pos) {
+            const int x = t.dfs[pos];
+            size[t.parent[x]] += size[x];
+        }
+        for (int x = 0; x < t.n; ++x) {
+            b[p.o_vis + 2 * (base + t.slot[x])] = t.dfs_pos[x];
+            b[p.o_vis + 2 * (base + t.slot[x]) + 1] = t.dfs_pos[x] + size[x];
+        }
+    }
     // preorder tables: per position the node's row and depth, and the Gram candidate
     // slot of every ancestor in the position's chunk of kPreChunk (one byte per depth)
     int nc = 0;

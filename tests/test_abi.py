@@ -249,3 +249,37 @@ def test_prep_empty_batch_is_a_no_op():
     d = _dims(n_req=0, h_k=1, h_v=1, d_k=128, d_v=128, op_dtype=1)
     prep = L.lumo_gdn_prep(L.LUMO_PREP_QK_NORM | L.LUMO_PREP_RAW_GATES, 1e-6, FAKE, FAKE)
     assert _verify_prep(d, desc, prep) == L.LUMO_OK
+
+
+def _attn(d, desc, n_split=2, max_ctx=100, scale=0.1, ws=1 << 30, ptrs=True):
+    P = ctypes.c_void_p
+    f = P(FAKE) if ptrs else None
+    return L._lib.lumo_tree_attention(ctypes.byref(d), ctypes.byref(desc), P(FAKE), max_ctx, scale,
+                                      f, P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+                                      n_split, P(FAKE), ws, None)
+
+
+def test_attention_rejects_bad_arguments():
+    desc, _blob = _desc()
+    ok = L.attn_dims(1, 4, 2)
+    assert _attn(L.attn_dims(1, 6, 2), desc) == L.LUMO_EUNSUPPORTED     # group of 3
+    assert _attn(L.attn_dims(1, 32, 2), desc) == L.LUMO_EUNSUPPORTED    # group of 16
+    assert _attn(L.attn_dims(1, 4, 3), desc) == L.LUMO_ESHAPE           # not a multiple
+    assert _attn(L.attn_dims(1, 4, 2, d=64), desc) == L.LUMO_EUNSUPPORTED
+    assert _attn(L.attn_dims(2, 4, 2), desc) == L.LUMO_EDESC
+    assert _attn(ok, desc, n_split=0) == L.LUMO_EINVAL
+    assert _attn(ok, desc, max_ctx=-1) == L.LUMO_EINVAL
+    assert _attn(ok, desc, scale=0.0) == L.LUMO_EINVAL
+    assert _attn(ok, desc, scale=float("inf")) == L.LUMO_EINVAL
+    assert _attn(ok, desc, ptrs=False) == L.LUMO_EINVAL
+    need = L.lumo_tree_attention_workspace_bytes(ok, desc.plan, 2)
+    assert need == 3 * 7 * 4 * 129 * 4
+    assert _attn(ok, desc, ws=need - 4) == L.LUMO_ESPACE
+    assert 1 <= L.lumo_tree_attention_splits(ok, desc.plan, 131072) <= 512
+
+
+def test_attention_empty_batch_is_a_no_op():
+    plan, blob = L.lumo_tree_plan(np.array([0], np.int32), np.zeros(0, np.int32),
+                                  np.zeros(0, np.int32), 0)
+    desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
+    assert _attn(L.attn_dims(0, 4, 2), desc, ptrs=False) == L.LUMO_OK

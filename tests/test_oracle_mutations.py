@@ -52,8 +52,8 @@ MUTATIONS = {
     "attn_no_scale": ("sc[t] = scale * s;", "sc[t] = s;"),
     "attn_value_of_parent": ("const long vb = t < nc ? ((c0 + t) * h_kv + hk) * d : ((long)rw[path[t - nc]] * h_kv + hk) * d;",
                              "const long vb = t < nc ? ((c0 + t) * h_kv + hk) * d : ((long)rw[path[t - nc > 0 ? t - nc - 1 : 0]] * h_kv + hk) * d;"),
-    "attn_excludes_self": ("for (long t = 0; t < nc + len; ++t) {\n                        const void* kk",
-                           "for (long t = 0; t < nc + len - (len > 1); ++t) {\n                        const void* kk"),
+    "attn_excludes_self": ("for (long t = 0; t < nc + len; ++t) {\n                    const void* kk",
+                           "for (long t = 0; t < nc + len - (len > 1); ++t) {\n                    const void* kk"),
 }
 
 

@@ -206,3 +206,21 @@ def test_bad_policy_rejected():
         L.lumo_tree_plan(np.array([0, 1], np.int32), np.array([-1], np.int32),
                          np.array([1], np.int32), 9)
     assert e.value.status == L.LUMO_EINVAL
+
+
+def test_visibility_intervals_match_ancestry():
+    """vis[slot] is the preorder interval of the node's subtree: a is an ancestor-or-self
+    of i exactly when i's position falls in a's interval (checked by brute force)."""
+    rng = np.random.default_rng(91)
+    parents = [trees.random_tree(rng, n, 6, trees.bmax_uniform(4)) for n in (1, 9, 40)] + [trees.FIG1_PARENT]
+    node_off = np.concatenate([[0], np.cumsum([len(p) for p in parents])]).astype(np.int32)
+    plan, blob = L.lumo_tree_plan(node_off, np.concatenate(parents), np.array([len(p) for p in parents], np.int32))
+    vis = blob[plan.o_vis:plan.o_vis + 2 * plan.total_nodes].reshape(-1, 2)
+    for r, par in enumerate(parents):
+        slot = oplan.slot_map(par)
+        base = int(node_off[r])
+        for i in range(len(par)):
+            anc = set(oplan.ancestry(par, i))
+            for a in range(len(par)):
+                lo, hi = vis[base + slot[a]]
+                assert (lo <= vis[base + slot[i]][0] < hi) == (a in anc), (r, a, i)
