@@ -16,6 +16,7 @@ durations, and the fp64 CPU oracle timed on a bounded sample of the same workloa
    path, in the same pass over the state, and the commit derives the path and the conv
    history only; eager: the commit replays the path itself; wy policy only)
   python bench.py --copy-probe     # plain 1 GiB device copy x3 (HBM counter calibration)
+  python bench.py --attention      # tree attention over a 131,072-token context (separate line)
 
 The roofline's `traffic` (measured HBM bytes per verify call) is reported from
 profiles/traffic.json only while the verify kernel's sources hash to the value the
@@ -94,6 +95,68 @@ WORKLOAD_TEXT = {
     "chainmix": "64 requests x 1 layer x 32 value heads, d=128: 32 chains of 16 + 32 trees of 128 nodes, bf16 operands, accepted lengths 0-16",
     "paper28": "1 request x 1 layer x 32 value heads, d=128, the 28-node draft geometry padded to 32 rows",
 }
+
+
+ATTN_WORKLOAD = ("tree attention: the 28-node draft geometry in 32 rows, 1 request, 131,072 context "
+                 "tokens, 16 query heads in pairs on 8 key/value heads, d=128, bf16")
+
+
+def attention_bench(args):
+    """Tree attention (lumo_tree_attention) on the evaluated geometry: HBM-bound by the
+    context keys and values; one step = one attention layer's call."""
+    import numpy as np
+    import torch
+
+    import paper_2609_23900_amd as L
+    from lumo_synth import operands as ops
+    from lumo_synth import trees
+
+    par = trees.paper_geometry_tree()
+    n_ctx, h_q, h_kv, d = 131072, 16, 8, 128
+    desc = L.TreeDesc.build(np.array([0, len(par)], np.int32), par, np.array([32], np.int32))
+    dims = L.attn_dims(1, h_q, h_kv, d)
+    rng = np.random.default_rng(9)
+
+    def bf(shape):
+        return torch.from_numpy(ops.to_bf16_bits(rng.standard_normal(shape).astype(np.float32))).cuda()
+
+    q, kt, vt = bf((32, h_q, d)), bf((32, h_kv, d)), bf((32, h_kv, d))
+    kc, vc = bf((n_ctx, h_kv, d)), bf((n_ctx, h_kv, d))
+    ctx_off = torch.tensor([0, n_ctx], dtype=torch.int32, device="cuda")
+    o = torch.zeros((32, h_q, d), dtype=torch.int16, device="cuda")
+    lse = torch.zeros((32, h_q), dtype=torch.float32, device="cuda")
+    n_split = L.lumo_tree_attention_splits(dims, desc.plan, n_ctx)
+    ws = torch.empty(L.lumo_tree_attention_workspace_bytes(dims, desc.plan, n_split) // 4 + 1,
+                     dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        L.lumo_tree_attention(dims, desc, ctx_off, n_ctx, 1.0 / np.sqrt(d), q, kc, vc, kt, vt, o, lse,
+                              n_split, ws, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    nodes = len(par)
+    alg = 2 * n_ctx * h_kv * d * 2 + 32 * (h_q + 2 * h_kv) * d * 2 + nodes * h_q * (d * 2 + 4)
+    ach = alg / (ms * 1e-3) / 1e9
+    out = {"metric": "tree attention query-head rows/sec + % of HBM roofline, 1 MI355X",
+           "value": round(nodes * h_q / (ms * 1e-3), 1), "unit": "query-head rows/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (N(0,1) queries, keys and values)",
+           "config": {"workload": ATTN_WORKLOAD, "n_split": n_split},
+           "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None, "kernel": "tree attention",
+                        "per_launch": f"{alg / 1e6:.1f} MB algorithmic (context keys and values once)"}}
+    print(json.dumps(out), flush=True)
 
 
 def log(*a):
@@ -180,6 +243,7 @@ def main():
                     help="prepare operands in the kernels (query/key normalisation, gates from raw "
                          "inputs; wy policy): g and beta are then read as raw inputs")
     ap.add_argument("--copy-probe", action="store_true", help="only run the counter-calibration copy")
+    ap.add_argument("--attention", action="store_true", help="only run the tree-attention benchmark")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     args = ap.parse_args()
@@ -190,6 +254,9 @@ def main():
 
     if args.copy_probe:
         copy_probe()
+        return
+    if args.attention:
+        attention_bench(args)
         return
 
     import numpy as np

@@ -341,13 +341,27 @@ extern "C" size_t lumo_tree_attention_workspace_bytes(const lumo_attn_dims* d, c
 }
 
 extern "C" int32_t lumo_tree_attention_splits(const lumo_attn_dims* d, const lumo_plan* p, int32_t max_ctx) {
-    if (!d || !p || d->h_kv < 1) return 1;
-    // about four blocks per CU of 256, partitions of at least 256 context tokens
-    const long per_split = (long)d->n_req * d->h_kv * ((p->max_nodes + 31) / 32);
-    long n = per_split > 0 ? (1024 + per_split - 1) / per_split : 1;
-    const long cap = std::max<long>(1, (max_ctx + 255) / 256);
-    n = std::min(n, cap);
-    return (int32_t)std::max<long>(1, std::min<long>(n, 4096));
+    if (!d || !p || d->h_kv < 1 || d->h_q < d->h_kv) return 1;
+    // Blocks of one partition: requests x kv heads x head blocks x query chunks; the
+    // device holds 512 such blocks at once (256 with 4 query heads per block). Pick the
+    // partition count that minimises (rounds of resident blocks) x (64-key tiles per
+    // block), the longest chain of tiles any block slot runs.
+    const int grp = d->h_q / d->h_kv;
+    const long per = (long)d->n_req * d->h_kv * (grp > 4 ? grp / 4 : 1) * ((p->max_nodes + 31) / 32);
+    const long slots = grp >= 4 ? 256 : 512;
+    if (per <= 0 || max_ctx <= 0) return 1;
+    const long max_n = std::min<long>(4096, std::max<long>(1, (max_ctx + 63) / 64));
+    long best = 1, best_cost = -1;
+    for (long n = 1; n <= max_n; ++n) {
+        const long rounds = ((n + 1) * per + slots - 1) / slots;
+        const long tiles = ((long)attn_part_len(max_ctx, (int)n) + 63) / 64;
+        const long cost = rounds * tiles;
+        if (best_cost < 0 || cost < best_cost) {
+            best = n;
+            best_cost = cost;
+        }
+    }
+    return (int32_t)best;
 }
 
 extern "C" lumo_status lumo_tree_attention(const lumo_attn_dims* dims, const lumo_tree_desc* desc,
