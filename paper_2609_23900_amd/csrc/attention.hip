@@ -14,9 +14,11 @@
 // online softmax needs only two lane-group swaps per reduction, and the probabilities
 // are already in the B-operand layout of O^T = V^T P^T (key slot 8 j + e of lane group
 // j is key 4 j + e of the tile's first 16-key half for e < 4, of the second for
-// e >= 4). K is staged by direct global-to-LDS copies (16-byte slots XOR-swizzled by
-// key); V is staged transposed (d-major, 8-byte units of 4 keys, swizzled by d) from
-// registers. Tiles of 64 keys, double-buffered.
+// e >= 4). K and V tiles are staged by direct global-to-LDS copies, key-major with
+// 16-byte slots XOR-swizzled by key; the V^T operand is read back with the transposing
+// LDS read (ds_read_b64_tr_b16: within 16 lanes, lane i receives element i % 4 of
+// lanes 4 e + i / 4, e = 0..3), so V never passes through registers. Tiles of 64 keys,
+// double-buffered.
 #include "device_common.h"
 #include "internal.h"
 #include "launch.h"
@@ -27,6 +29,8 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 constexpr int kAD = 128;  // head dimension
 constexpr int kAN = 32;   // query nodes per block
@@ -67,12 +71,11 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast
 template <int G>
 __global__ __launch_bounds__(128 * G, G == 1 ? 1 : 2) void attn_kernel(AttnParams p) {
     constexpr int nthr = 128 * G;
-    // key tiles: [key][16 slots]; slot c of key t holds dims 8 (c ^ (t & 15)) .. + 7
+    // key and value tiles: [key][16 slots]; slot c of key t holds dims 8 (c ^ (t & 15)) .. + 7
     __shared__ uint4 kt0[kAT * 16];
     __shared__ uint4 kt1[kAT * 16];
-    // value tiles transposed: [dim][16 units]; unit u of dim d holds keys 4 (u ^ (d & 15)) .. + 3
-    __shared__ uint2 vt0[kAD * 16];
-    __shared__ uint2 vt1[kAD * 16];
+    __shared__ uint4 vt0[kAT * 16];
+    __shared__ uint4 vt1[kAT * 16];
     const int tid = (int)threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
@@ -114,8 +117,9 @@ __global__ __launch_bounds__(128 * G, G == 1 ? 1 : 2) void attn_kernel(AttnParam
     const int qnode = tree ? p.blob[p.o_dfs + base + p.blob[p.o_vis + 2 * (base + min(qs, N - 1))]] : 0;
 
     const int ntile = (nk + kAT - 1) / kAT;
-    // key tile i into (kt, vregs): keys past the range repeat its last key (masked later)
-    auto k_issue = [&](int i, uint4* kt) {
+    // tile i of a key/value matrix into `dst`: keys past the range repeat its last key
+    // (masked later, so pad rows are never read)
+    auto tile_issue = [&](const uint16_t* mat, int i, uint4* dst) {
 #pragma unroll
         for (int j = 0; j < kAT * 16 / nthr; ++j) {
             const int slot0 = j * nthr + 64 * wave;  // uniform
@@ -123,42 +127,8 @@ __global__ __launch_bounds__(128 * G, G == 1 ? 1 : 2) void attn_kernel(AttnParam
             const int t = slot >> 4;
             const int kb = (slot & 15) ^ (t & 15);
             const int key = min(i * kAT + t, nk - 1);
-            __builtin_amdgcn_global_load_lds(kmat + ((long)(krow0 + key) * p.h_kv + g) * kAD + 8 * kb,
-                                             (lds_void*)&kt[slot0], 16, 0, 0);
-        }
-    };
-    constexpr int kPairs = (256 + nthr - 1) / nthr;  // (4-key group, 8-dim group) pairs per thread
-    uint4 vr[kPairs][4];
-    auto v_load = [&](int i) {
-#pragma unroll
-        for (int pi = 0; pi < kPairs; ++pi) {
-            const int pr = min(pi * nthr + tid, 255);
-            const int tg = pr >> 4, dg = pr & 15;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int key = min(i * kAT + 4 * tg + e, nk - 1);
-                vr[pi][e] = *reinterpret_cast<const uint4*>(vmat + ((long)(krow0 + key) * p.h_kv + g) * kAD + 8 * dg);
-            }
-        }
-    };
-    auto v_store = [&](uint2* vt) {
-#pragma unroll
-        for (int pi = 0; pi < kPairs; ++pi) {
-            const int pr = pi * nthr + tid;
-            if (pr >= 256) break;
-            const int tg = pr >> 4, dg = pr & 15;
-            const uint32_t w[4][4] = {{vr[pi][0].x, vr[pi][0].y, vr[pi][0].z, vr[pi][0].w},
-                                      {vr[pi][1].x, vr[pi][1].y, vr[pi][1].z, vr[pi][1].w},
-                                      {vr[pi][2].x, vr[pi][2].y, vr[pi][2].z, vr[pi][2].w},
-                                      {vr[pi][3].x, vr[pi][3].y, vr[pi][3].z, vr[pi][3].w}};
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int d = 8 * dg + e;
-                const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;  // upper or lower halves
-                const uint32_t lo = __builtin_amdgcn_perm(w[1][e >> 1], w[0][e >> 1], sel);
-                const uint32_t hi = __builtin_amdgcn_perm(w[3][e >> 1], w[2][e >> 1], sel);
-                vt[d * 16 + (tg ^ (d & 15))] = make_uint2(lo, hi);
-            }
+            __builtin_amdgcn_global_load_lds(mat + ((long)(krow0 + key) * p.h_kv + g) * kAD + 8 * kb,
+                                             (lds_void*)&dst[slot0], 16, 0, 0);
         }
     };
 
@@ -184,7 +154,7 @@ __global__ __launch_bounds__(128 * G, G == 1 ? 1 : 2) void attn_kernel(AttnParam
         }
         return vm;
     };
-    auto compute = [&](int i, const uint4* kt, const uint2* vt) {
+    auto compute = [&](int i, const uint4* kt, const uint4* vt) {
         const uint64_t vm = tile_mask(i);
         // S^T = K Q^T: lane (query lane%16) gets keys 16 tt + 4 (lane/16) + x
         f32x4 s[kAT / 16];
@@ -232,12 +202,21 @@ __global__ __launch_bounds__(128 * G, G == 1 ? 1 : 2) void attn_kernel(AttnParam
                                         f32x2_to_bf16x2(s[2 * kh][2], s[2 * kh][3]),
                                         f32x2_to_bf16x2(s[2 * kh + 1][0], s[2 * kh + 1][1]),
                                         f32x2_to_bf16x2(s[2 * kh + 1][2], s[2 * kh + 1][3]));
-            const int u1 = 8 * kh + (lane >> 4), u2 = u1 + 4;
+            // transposing reads: lane j of a 16-lane group reads dims 16 dt + 4 (j % 4) .. + 3
+            // of key 32 kh + 4 (lane / 16) + j / 4 (and of that key + 16), and receives dim
+            // 16 dt + j of keys 32 kh + 4 (lane / 16) + e (and + 16 + e), e = 0..3
+            const int jj = lane & 15;
+            const int t1 = 32 * kh + 4 * (lane >> 4) + (jj >> 2), t2 = t1 + 16;
+            const char* vb = reinterpret_cast<const char*>(vt);
 #pragma unroll
             for (int dt = 0; dt < kAD / 16; ++dt) {
-                const int d = 16 * dt + (lane & 15);
-                const uint2 a1 = vt[d * 16 + (u1 ^ (d & 15))];
-                const uint2 a2 = vt[d * 16 + (u2 ^ (d & 15))];
+                const int sg = 2 * dt + ((jj & 3) >> 1);  // 16-byte dim segment, then its half
+                const int hb = 8 * (jj & 1);
+                const v4i16 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_v4i16*)(vb + (t1 * 16 + (sg ^ (t1 & 15))) * 16 + hb));
+                const v4i16 r2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_v4i16*)(vb + (t2 * 16 + (sg ^ (t2 & 15))) * 16 + hb));
+                const uint2 a1 = __builtin_bit_cast(uint2, r1), a2 = __builtin_bit_cast(uint2, r2);
                 o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(make_uint4(a1.x, a1.y, a2.x, a2.y)),
                                                                 as_bf16x8(pw), o[dt], 0, 0, 0);
             }
@@ -245,32 +224,29 @@ __global__ __launch_bounds__(128 * G, G == 1 ? 1 : 2) void attn_kernel(AttnParam
     };
 
     if (ntile > 0) {
-        k_issue(0, kt0);
-        v_load(0);
+        tile_issue(kmat, 0, kt0);
+        tile_issue(vmat, 0, vt0);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        v_store(vt0);
         __syncthreads();
         for (int i = 0; i < ntile; i += 2) {
             // tile i from buffers 0 while tile i + 1 lands in buffers 1, then the reverse
             const bool n1 = i + 1 < ntile;
             if (n1) {
-                k_issue(i + 1, kt1);
-                v_load(i + 1);
+                tile_issue(kmat, i + 1, kt1);
+                tile_issue(vmat, i + 1, vt1);
             }
             compute(i, kt0, vt0);
             if (!n1) break;
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            v_store(vt1);
             __syncthreads();
             const bool n2 = i + 2 < ntile;
             if (n2) {
-                k_issue(i + 2, kt0);
-                v_load(i + 2);
+                tile_issue(kmat, i + 2, kt0);
+                tile_issue(vmat, i + 2, vt0);
             }
             compute(i + 1, kt1, vt1);
             if (!n2) break;
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            v_store(vt0);
             __syncthreads();
         }
     }
