@@ -408,51 +408,50 @@ int orc_tree_attention(int n_req, int h_q, int h_kv, int d, int op_dtype, const 
                        const void* v_tree, double* o, double* lse, int n_threads) {
     int bad = 0;
     const int grp = h_q / h_kv;
+    const long n_all = node_off[n_req];
+    /* one (request, node) per iteration; r is found by scanning node_off */
 #ifdef _OPENMP
 #pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads > 0 ? n_threads : 1) reduction(| : bad)
 #endif
-    for (int r = 0; r < n_req; ++r) {
+    for (long flat = 0; flat < n_all; ++flat) {
+        int r = 0;
+        while (node_off[r + 1] <= flat) ++r;
+        const int i = (int)(flat - node_off[r]);
         const int n = node_off[r + 1] - node_off[r];
         const int* par = parent + node_off[r];
         const int* rw = row + node_off[r];
         const long c0 = ctx_off[r], nc = ctx_off[r + 1] - ctx_off[r];
-        int* path = (int*)malloc(sizeof(int) * (size_t)(n > 0 ? n : 1));
+        int* path = (int*)malloc(sizeof(int) * (size_t)n);
         double* sc = (double*)malloc(sizeof(double) * (size_t)(nc + n + 1));
         double* acc = (double*)malloc(sizeof(double) * (size_t)d);
-        if (!path || !sc || !acc) {
+        const int len = (path && sc && acc) ? ancestry(par, n, i, path, n) : -1;
+        if (len < 0) {
             bad |= 1;
         } else {
-            for (int i = 0; i < n && !bad; ++i) {
-                const int len = ancestry(par, n, i, path, n);
-                if (len < 0) {
-                    bad |= 1;
-                    break;
+            for (int h = 0; h < h_q; ++h) {
+                const int hk = h / grp;
+                const long qb = ((long)rw[i] * h_q + h) * d;
+                /* scores: context first, then the path root first */
+                double mx = -INFINITY;
+                for (long t = 0; t < nc + len; ++t) {
+                    const void* kk = t < nc ? k_ctx : k_tree;
+                    const long kb = t < nc ? ((c0 + t) * h_kv + hk) * d : ((long)rw[path[t - nc]] * h_kv + hk) * d;
+                    double s = 0.0;
+                    for (int e = 0; e < d; ++e) s += ld_op(q, qb + e, op_dtype) * ld_op(kk, kb + e, op_dtype);
+                    sc[t] = scale * s;
+                    if (sc[t] > mx) mx = sc[t];
                 }
-                for (int h = 0; h < h_q; ++h) {
-                    const int hk = h / grp;
-                    const long qb = ((long)rw[i] * h_q + h) * d;
-                    /* scores: context first, then the path root first */
-                    double mx = -INFINITY;
-                    for (long t = 0; t < nc + len; ++t) {
-                        const void* kk = t < nc ? k_ctx : k_tree;
-                        const long kb = t < nc ? ((c0 + t) * h_kv + hk) * d : ((long)rw[path[t - nc]] * h_kv + hk) * d;
-                        double s = 0.0;
-                        for (int e = 0; e < d; ++e) s += ld_op(q, qb + e, op_dtype) * ld_op(kk, kb + e, op_dtype);
-                        sc[t] = scale * s;
-                        if (sc[t] > mx) mx = sc[t];
-                    }
-                    double sum = 0.0;
-                    for (int e = 0; e < d; ++e) acc[e] = 0.0;
-                    for (long t = 0; t < nc + len; ++t) {
-                        const double w = exp(sc[t] - mx);
-                        sum += w;
-                        const void* vv = t < nc ? v_ctx : v_tree;
-                        const long vb = t < nc ? ((c0 + t) * h_kv + hk) * d : ((long)rw[path[t - nc]] * h_kv + hk) * d;
-                        for (int e = 0; e < d; ++e) acc[e] += w * ld_op(vv, vb + e, op_dtype);
-                    }
-                    for (int e = 0; e < d; ++e) o[qb + e] = acc[e] / sum;
-                    lse[(long)rw[i] * h_q + h] = mx + log(sum);
+                double sum = 0.0;
+                for (int e = 0; e < d; ++e) acc[e] = 0.0;
+                for (long t = 0; t < nc + len; ++t) {
+                    const double w = exp(sc[t] - mx);
+                    sum += w;
+                    const void* vv = t < nc ? v_ctx : v_tree;
+                    const long vb = t < nc ? ((c0 + t) * h_kv + hk) * d : ((long)rw[path[t - nc]] * h_kv + hk) * d;
+                    for (int e = 0; e < d; ++e) acc[e] += w * ld_op(vv, vb + e, op_dtype);
                 }
+                for (int e = 0; e < d; ++e) o[qb + e] = acc[e] / sum;
+                lse[(long)rw[i] * h_q + h] = mx + log(sum);
             }
         }
         free(path);

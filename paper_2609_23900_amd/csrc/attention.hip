@@ -261,7 +261,9 @@ __global__ __launch_bounds__(128 * G, G == 1 ? 1 : 2) void attn_kernel(AttnParam
     if (lane < 16) p.ws_lse[wi] = lsum > 0.f ? m + __log2f(lsum) : -INFINITY;
 }
 
-// Merge of the key ranges of one (query row, head): weights 2^(lse_s - max).
+// Merge of the key ranges of one (query row, head): weights 2^(lse_s - max). Lane s
+// holds range s's log-sum-exp (64 ranges at a time); every lane then accumulates two
+// of the d values over the ranges, eight independent loads in flight.
 __global__ __launch_bounds__(64) void attn_combine_kernel(AttnParams p, uint16_t* __restrict__ o,
                                                           float* __restrict__ lse) {
     int blk = blockIdx.x;
@@ -274,18 +276,44 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnParams p, uint16_t
     const int row = p.blob[p.o_row_off + r] + s;
     const int lane = (int)threadIdx.x;
     const int ns = p.n_split + 1;
+    const long rs = (long)p.total_rows * p.h_q;  // stride between ranges
+    const long ri = (long)row * p.h_q + h;
     float mx = -INFINITY;
-    for (int sp = 0; sp < ns; ++sp) mx = fmaxf(mx, p.ws_lse[((long)sp * p.total_rows + row) * p.h_q + h]);
+    for (int c = 0; c < ns; c += 64) {
+        const int sp = c + lane;
+        if (sp < ns) mx = fmaxf(mx, p.ws_lse[sp * rs + ri]);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
     float wsum = 0.f, a0 = 0.f, a1 = 0.f;
-    for (int sp = 0; sp < ns; ++sp) {
-        const long wi = ((long)sp * p.total_rows + row) * p.h_q + h;
-        const float ls = p.ws_lse[wi];
-        if (ls == -INFINITY) continue;
-        const float w = __builtin_amdgcn_exp2f(ls - mx);
-        const float2 v = *reinterpret_cast<const float2*>(p.ws_o + wi * kAD + 2 * lane);
-        wsum += w;
-        a0 = __builtin_fmaf(w, v.x, a0);
-        a1 = __builtin_fmaf(w, v.y, a1);
+    for (int c = 0; c < ns; c += 64) {
+        const int sp = c + lane;
+        const float ls = sp < ns ? p.ws_lse[sp * rs + ri] : -INFINITY;
+        const float w = ls == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ls - mx);
+        float ws = w;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) ws += __shfl_xor(ws, off);
+        wsum += ws;
+        const int nr = min(64, ns - c);
+        int k = 0;
+        for (; k + 8 <= nr; k += 8) {
+            float2 v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                v[u] = *reinterpret_cast<const float2*>(p.ws_o + ((c + k + u) * rs + ri) * kAD + 2 * lane);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k + u));
+                a0 = __builtin_fmaf(wu, v[u].x, a0);
+                a1 = __builtin_fmaf(wu, v[u].y, a1);
+            }
+        }
+        for (; k < nr; ++k) {
+            const float2 v = *reinterpret_cast<const float2*>(p.ws_o + ((c + k) * rs + ri) * kAD + 2 * lane);
+            const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k));
+            a0 = __builtin_fmaf(wu, v.x, a0);
+            a1 = __builtin_fmaf(wu, v.y, a1);
+        }
     }
     const float inv = 1.f / wsum;  // every node sees at least itself
     reinterpret_cast<uint32_t*>(o + ((long)row * p.h_q + h) * kAD)[lane] = f32x2_to_bf16x2(a0 * inv, a1 * inv);
