@@ -7,15 +7,17 @@ form a serving loop: each verify reads the state the previous commit published.
 
 Prints one JSON line: head-node updates per second (tree nodes x layers x value
 heads, each node counted once), the roofline of the dominant kernel (verify) with
-its duration measured by HIP events on the launch stream, the other kernels'
-durations, and the fp64 CPU oracle timed on a bounded sample of the same workload.
+its duration measured by HIP events on the launch stream and set against the published
+peak and against a plain device copy timed in the same run, the other kernels'
+durations, per-step percentiles, and the fp64 CPU oracle timed on a bounded sample of
+the same workload (all host cores, and one thread).
 
   python bench.py [--steps K] [--warmup W] [--config batched] [--policy wy]
                   [--commit deferred|eager]
   (deferred: each step's verification also publishes the previous step's accepted
    path, in the same pass over the state, and the commit derives the path and the conv
    history only; eager: the commit replays the path itself; wy policy only)
-  python bench.py --copy-probe     # plain 1 GiB device copy x3 (HBM counter calibration)
+  python bench.py --copy-probe     # plain 1 GiB device copy (HBM counter calibration)
   python bench.py --attention      # tree attention over a 131,072-token context (separate line)
 
 The roofline's `traffic` (measured HBM bytes per verify call) is reported from
@@ -42,7 +44,9 @@ TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "traffic.json")
 VERIFY_SOURCES = {
     "wy": ["verify_wy.hip", "device_common.h", "internal.h", "launch.h"],
     "paths": ["verify_scan.hip", "device_common.h", "internal.h", "launch.h"],
+    "attention": ["attention.hip", "device_common.h", "internal.h", "launch.h"],
 }
+ATTN_CONFIG = "paper28_ctx131072"
 
 
 def verify_source_hash(policy):
@@ -68,24 +72,51 @@ def recorded_traffic(policy, config, commit="eager"):
     return None
 
 
-def copy_probe():
-    """A plain device copy of known size (1 GiB read + 1 GiB written, three times): the
-    calibration of the HBM byte counters, and the practical read+write rate."""
+def copy_rate(reps=3):
+    """Milliseconds per plain device copy of 1 GiB (read) into 1 GiB (written), and the
+    read + write rate in GB/s: the practical HBM ceiling a kernel is compared with."""
     import torch
     n = 256 * 1024 * 1024
     a = torch.ones(n, device="cuda")
     b = torch.empty_like(a)
+    b.copy_(a)
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record()
-    for _ in range(3):
+    for _ in range(reps):
         b.copy_(a)
     e1.record()
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / 3
-    print(json.dumps({"copy_probe_bytes": n * 4, "copies": 3, "ms_per_copy": round(ms, 4),
-                      "read_plus_write_GBps": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}), flush=True)
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    return ms, 2 * n * 4 / (ms * 1e-3) / 1e9
+
+
+def copy_probe():
+    """A plain device copy of known size (1 GiB read + 1 GiB written, four times with the
+    first as warm-up): the calibration of the HBM byte counters."""
+    ms, gbs = copy_rate()
+    print(json.dumps({"copy_probe_bytes": 256 * 1024 * 1024 * 4, "copies": 4, "ms_per_copy": round(ms, 4),
+                      "read_plus_write_GBps": round(gbs, 1)}), flush=True)
+
+
+def pct(xs):
+    """10th, 50th and 90th percentiles (nearest rank) of a list of times."""
+    ys = sorted(xs)
+    return [round(ys[min(len(ys) - 1, int(q * len(ys)))], 4) for q in (0.1, 0.5, 0.9)]
+
+
+def host_cpu():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
 
 WORKLOAD_TEXT = {
     "tiny": "Fig. 1 tree, 1 request, 1 head, d=16, fp32 operands",
@@ -154,8 +185,18 @@ def attention_bench(args):
            "data": "synthetic (N(0,1) queries, keys and values)",
            "config": {"workload": ATTN_WORKLOAD, "n_split": n_split},
            "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                        "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None, "kernel": "tree attention",
+                        "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                        "kernel": "tree attention call (partition kernel + merge kernel)",
                         "per_launch": f"{alg / 1e6:.1f} MB algorithmic (context keys and values once)"}}
+    tr = recorded_traffic("attention", ATTN_CONFIG, "n/a")
+    if tr is not None:
+        out["roofline"]["traffic"] = {"fetch_bytes": tr["fetch_bytes"], "write_bytes": tr["write_bytes"],
+                                      "total_bytes": tr["fetch_bytes"] + tr["write_bytes"],
+                                      "unit": "B per attention call", "source": "profiles/traffic.json"}
+    if not args.no_copy:
+        _, cgbs = copy_rate()
+        out["roofline"]["practical"] = {"copy_GBps": round(cgbs, 1), "frac_of_copy": round(ach / cgbs, 4),
+                                        "what": "plain 1 GiB device copy (read + write) timed in this run"}
     print(json.dumps(out), flush=True)
 
 
@@ -181,7 +222,10 @@ def alg_bytes_flops(wl):
     # publication folded into the next verification: the state is read there anyway, so
     # what it adds is the state written back and the path's operand rows
     pub_bytes = c_bytes - active * wl.n_layers * wl.h_v * mat
-    conv_bytes = wl.total_nodes * wl.n_layers * wl.channels * opb * 2 + wl.n_layers * wl.channels * 16
+    # x read and y written per (layer, node), the committed history read per (request,
+    # layer), four fp32 taps per (layer, channel)
+    conv_bytes = (wl.total_nodes * wl.n_layers * wl.channels * opb * 2
+                  + wl.n_req * wl.n_layers * 3 * wl.channels * opb + wl.n_layers * wl.channels * 16)
     return dict(verify_bytes=v_bytes, verify_flops=v_flops, commit_bytes=c_bytes, pub_bytes=pub_bytes,
                 commit_flops=c_flops, conv_bytes=conv_bytes, commit_updates=c_upd)
 
@@ -198,7 +242,8 @@ def oracle_depth(parent, a):
 
 def cpu_baseline(wl, budget_s=12.0):
     """fp64 oracle (conv + verify + commit) on the first k layers of the workload, k chosen
-    so that the run takes about budget_s seconds; scaled to head-node updates/s."""
+    so that the run takes about budget_s seconds, with OpenMP over the host cores; scaled
+    to head-node updates/s. Also the same oracle on one thread over one layer."""
     import numpy as np
 
     import oracle
@@ -213,29 +258,32 @@ def cpu_baseline(wl, budget_s=12.0):
                "x": a["x"][:k], "hist": np.ascontiguousarray(a["hist"][:, :k]), "w": a["w"][:k]}
         return configs.Workload(**{**wl.__dict__, "n_layers": k, "arrays": arr})
 
-    def run(k):
+    def run(k, nt):
         w = sub(k)
         t0 = time.perf_counter()
         oracle.conv_all(w)
-        oracle.verify_all(w, n_threads=threads)
-        oracle.commit(w, n_threads=threads)
+        oracle.verify_all(w, n_threads=nt)
+        oracle.commit(w, n_threads=nt)
         return time.perf_counter() - t0, w.head_node_updates
 
-    t1, hn1 = run(1)
+    t1, hn1 = run(1, threads)
     k = 1
     if t1 < budget_s and wl.n_layers > 1:
         k = int(min(wl.n_layers, max(1, budget_s // max(t1, 1e-3))))
-        t1, hn1 = run(k) if k > 1 else (t1, hn1)
+        t1, hn1 = run(k, threads) if k > 1 else (t1, hn1)
+    ts, hns = run(1, 1)
     return {"value": hn1 / t1, "unit": "head-node updates/s", "cores": threads, "kind": "oracle",
             "sample": f"conv + verify + commit of {k} of {wl.n_layers} layers "
-                      f"({hn1} head-node updates), all requests and heads, {t1:.1f} s"}
+                      f"({hn1} head-node updates), all requests and heads, {t1:.1f} s",
+            "one_thread": {"value": hns / ts, "sample": f"1 layer ({hns} head-node updates), {ts:.1f} s"},
+            "host": host_cpu()}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="batched")
     ap.add_argument("--policy", default="wy")
     ap.add_argument("--commit", choices=("deferred", "eager"), default="deferred")
@@ -246,6 +294,7 @@ def main():
     ap.add_argument("--attention", action="store_true", help="only run the tree-attention benchmark")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--no-copy", action="store_true", help="skip the device-copy reference rate")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the step shards "
@@ -316,6 +365,8 @@ def main():
     ver_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
     com_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
     ms_step = total_ms / args.steps
+    step_dist = pct([e[0].elapsed_time(e[3]) for e in evs])
+    ver_dist = pct([e[1].elapsed_time(e[2]) for e in evs])
     log(f"[bench] step {ms_step:.3f} ms (conv {conv_ms:.3f}, verify {ver_ms:.3f}, commit {com_ms:.3f})")
     assert torch.isfinite(st.state).all().item(), "non-finite state"
 
@@ -345,6 +396,8 @@ def main():
         "conv_hbm_frac": round(ab["conv_bytes"] / (conv_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         "verify_ms": round(ver_ms, 4),
         "commit_ms": round(com_ms, 4),
+        "step_ms_p10_p50_p90": step_dist,
+        "verify_ms_p10_p50_p90": ver_dist,
     }
     if not deferred:
         kernels["commit_hbm_frac"] = round(ab["commit_bytes"] / (com_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
@@ -359,6 +412,11 @@ def main():
                    "operands": "bf16" if wl.op_dtype == 1 else "f32"},
         "roofline": roof, "kernels": kernels,
     }
+    if not args.no_copy:
+        cms, cgbs = copy_rate()
+        roof["practical"] = {"copy_GBps": round(cgbs, 1), "frac_of_copy": round(roof["achieved"] / cgbs, 4)
+                             if roof["unit"] == "GB/s" else None,
+                             "what": "plain 1 GiB device copy (read + write) timed in this run"}
     if not args.no_cpu:
         log("[bench] CPU oracle leg")
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)

@@ -261,63 +261,70 @@ __global__ __launch_bounds__(128 * G, G == 1 ? 1 : 2) void attn_kernel(AttnParam
     if (lane < 16) p.ws_lse[wi] = lsum > 0.f ? m + __log2f(lsum) : -INFINITY;
 }
 
-// Merge of the key ranges of one (query row, head): weights 2^(lse_s - max). Lane s
-// holds range s's log-sum-exp (64 ranges at a time); every lane then accumulates two
-// of the d values over the ranges, eight independent loads in flight.
-__global__ __launch_bounds__(64) void attn_combine_kernel(AttnParams p, uint16_t* __restrict__ o,
-                                                          float* __restrict__ lse) {
+// Merge of the key ranges of one (query row, head): weights 2^(lse_s - max). Four waves
+// take every fourth range, eight ranges' loads in flight per wave, each lane two of the
+// d values; the waves' sums are added in a fixed order, so the result does not depend
+// on timing.
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p, uint16_t* __restrict__ o,
+                                                           float* __restrict__ lse) {
+    __shared__ float red[4];
+    __shared__ float2 part[4][64];
     int blk = blockIdx.x;
     const int h = blk % p.h_q;
     blk /= p.h_q;
     const int s = blk % p.max_nodes;
     const int r = blk / p.max_nodes;
     const int N = p.blob[p.o_node_off + r + 1] - p.blob[p.o_node_off + r];
-    if (s >= N) return;
+    if (s >= N) return;  // uniform over the block
     const int row = p.blob[p.o_row_off + r] + s;
-    const int lane = (int)threadIdx.x;
+    const int t = (int)threadIdx.x, lane = t & 63, wv = t >> 6;
     const int ns = p.n_split + 1;
     const long rs = (long)p.total_rows * p.h_q;  // stride between ranges
     const long ri = (long)row * p.h_q + h;
     float mx = -INFINITY;
-    for (int c = 0; c < ns; c += 64) {
-        const int sp = c + lane;
-        if (sp < ns) mx = fmaxf(mx, p.ws_lse[sp * rs + ri]);
-    }
+    for (int sp = t; sp < ns; sp += 256) mx = fmaxf(mx, p.ws_lse[sp * rs + ri]);
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    if (lane == 0) red[wv] = mx;
+    __syncthreads();
+    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));  // finite: every node sees itself
     float wsum = 0.f, a0 = 0.f, a1 = 0.f;
-    for (int c = 0; c < ns; c += 64) {
-        const int sp = c + lane;
-        const float ls = sp < ns ? p.ws_lse[sp * rs + ri] : -INFINITY;
-        const float w = ls == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ls - mx);
-        float ws = w;
+    auto weight = [&](float ls) { return ls == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ls - mx); };
+    int sp = wv;
+    for (; sp + 28 < ns; sp += 32) {
+        float ls[8];
+        float2 v[8];
 #pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) ws += __shfl_xor(ws, off);
-        wsum += ws;
-        const int nr = min(64, ns - c);
-        int k = 0;
-        for (; k + 8 <= nr; k += 8) {
-            float2 v[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-                v[u] = *reinterpret_cast<const float2*>(p.ws_o + ((c + k + u) * rs + ri) * kAD + 2 * lane);
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k + u));
-                a0 = __builtin_fmaf(wu, v[u].x, a0);
-                a1 = __builtin_fmaf(wu, v[u].y, a1);
-            }
+        for (int u = 0; u < 8; ++u) {
+            ls[u] = p.ws_lse[(sp + 4 * u) * rs + ri];
+            v[u] = *reinterpret_cast<const float2*>(p.ws_o + ((sp + 4 * u) * rs + ri) * kAD + 2 * lane);
         }
-        for (; k < nr; ++k) {
-            const float2 v = *reinterpret_cast<const float2*>(p.ws_o + ((c + k) * rs + ri) * kAD + 2 * lane);
-            const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), k));
-            a0 = __builtin_fmaf(wu, v.x, a0);
-            a1 = __builtin_fmaf(wu, v.y, a1);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const float w = weight(ls[u]);
+            wsum += w;
+            a0 = __builtin_fmaf(w, v[u].x, a0);
+            a1 = __builtin_fmaf(w, v[u].y, a1);
         }
     }
-    const float inv = 1.f / wsum;  // every node sees at least itself
-    reinterpret_cast<uint32_t*>(o + ((long)row * p.h_q + h) * kAD)[lane] = f32x2_to_bf16x2(a0 * inv, a1 * inv);
-    if (lane == 0) lse[(long)row * p.h_q + h] = (mx + __log2f(wsum)) * 0.69314718055994531f;
+    for (; sp < ns; sp += 4) {
+        const float w = weight(p.ws_lse[sp * rs + ri]);
+        const float2 v = *reinterpret_cast<const float2*>(p.ws_o + (sp * rs + ri) * kAD + 2 * lane);
+        wsum += w;
+        a0 = __builtin_fmaf(w, v.x, a0);
+        a1 = __builtin_fmaf(w, v.y, a1);
+    }
+    part[wv][lane] = make_float2(a0, a1);
+    __syncthreads();  // also orders red[] (read above) before its reuse below
+    if (lane == 0) red[wv] = wsum;
+    __syncthreads();
+    if (wv != 0) return;
+    const float2 q0 = part[0][lane], q1 = part[1][lane], q2 = part[2][lane], q3 = part[3][lane];
+    const float ws = ((red[0] + red[1]) + red[2]) + red[3];
+    const float inv = 1.f / ws;
+    const float b0 = ((q0.x + q1.x) + q2.x) + q3.x, b1 = ((q0.y + q1.y) + q2.y) + q3.y;
+    reinterpret_cast<uint32_t*>(o + ((long)row * p.h_q + h) * kAD)[lane] = f32x2_to_bf16x2(b0 * inv, b1 * inv);
+    if (lane == 0) lse[(long)row * p.h_q + h] = (mx + __log2f(ws)) * 0.69314718055994531f;
 }
 
 }  // namespace
@@ -368,7 +375,7 @@ hipError_t launch_attention(const lumo_attn_dims& d, const lumo_tree_desc& desc,
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const long cb = (long)d.n_req * pl.max_nodes * d.h_q;
-    hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)cb), dim3(64), 0, s, p, static_cast<uint16_t*>(a.o), a.lse);
+    hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)cb), dim3(256), 0, s, p, static_cast<uint16_t*>(a.o), a.lse);
     return hipGetLastError();
 }
 
