@@ -14,9 +14,10 @@ the same workload (all host cores, and one thread).
 
   python bench.py [--steps K] [--warmup W] [--config batched] [--policy wy]
                   [--commit deferred|eager]
-  (deferred: each step's verification also publishes the previous step's accepted
-   path, in the same pass over the state, and the commit derives the path and the conv
-   history only; eager: the commit replays the path itself; wy policy only)
+  (deferred: each step's conv first publishes the previous step's accepted path into
+   the conv history, its verification publishes that path into the state in the same
+   pass over the state, and the commit only derives the path; eager: the commit
+   publishes the history and replays the path itself; wy policy only)
   python bench.py --copy-probe     # plain 1 GiB device copy (HBM counter calibration)
   python bench.py --attention      # tree attention over a 131,072-token context (separate line)
 
@@ -222,12 +223,16 @@ def alg_bytes_flops(wl):
     # publication folded into the next verification: the state is read there anyway, so
     # what it adds is the state written back and the path's operand rows
     pub_bytes = c_bytes - active * wl.n_layers * wl.h_v * mat
+    # conv history publication (up to three x rows of the path read, three entries
+    # written per request and layer), in the commit or deferred into the next conv
+    hist_pub_bytes = active * wl.n_layers * 3 * wl.channels * opb * 2
     # x read and y written per (layer, node), the committed history read per (request,
     # layer), four fp32 taps per (layer, channel)
     conv_bytes = (wl.total_nodes * wl.n_layers * wl.channels * opb * 2
                   + wl.n_req * wl.n_layers * 3 * wl.channels * opb + wl.n_layers * wl.channels * 16)
     return dict(verify_bytes=v_bytes, verify_flops=v_flops, commit_bytes=c_bytes, pub_bytes=pub_bytes,
-                commit_flops=c_flops, conv_bytes=conv_bytes, commit_updates=c_upd)
+                commit_flops=c_flops, conv_bytes=conv_bytes, commit_updates=c_upd,
+                hist_pub_bytes=hist_pub_bytes)
 
 
 def oracle_depth(parent, a):
@@ -334,7 +339,10 @@ def main():
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        st.conv(stream)
+        if deferred:
+            st.conv_pending(st, stream)  # publishes the previous step's history, then the conv
+        else:
+            st.conv(stream)
         if ev is not None:
             ev[1].record(stream)
         if deferred:
@@ -343,7 +351,7 @@ def main():
             st.verify(stream)
         if ev is not None:
             ev[2].record(stream)
-        st.commit(stream, defer=deferred)
+        st.commit(stream, defer=deferred, with_conv=not deferred)
         if ev is not None:
             ev[3].record(stream)
 
@@ -393,7 +401,8 @@ def main():
                           f"algorithmic per verify call")
     kernels = {
         "conv_gather_ms": round(conv_ms, 4),
-        "conv_hbm_frac": round(ab["conv_bytes"] / (conv_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "conv_hbm_frac": round((ab["conv_bytes"] + (ab["hist_pub_bytes"] if deferred else 0))
+                               / (conv_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         "verify_ms": round(ver_ms, 4),
         "commit_ms": round(com_ms, 4),
         "step_ms_p10_p50_p90": step_dist,

@@ -10,8 +10,9 @@
  *   lumo_gdn_commit        device: derive the accepted path, replay it into the
  *                          native state, publish the convolution history
  * plus lumo_tree_attention (the attention layers' tree verification), a
- * captured-graph form of the commit; lumo_tree_gdn_verify_pending, which
- * folds the replay of one iteration into the verification of the next; and forms
+ * captured-graph form of the commit; lumo_tree_gdn_verify_pending and
+ * lumo_tree_conv_gather_pending, which fold the publication of one iteration (state
+ * replay, conv history) into the verification and convolution of the next; and forms
  * that prepare the operands inside the kernels (lumo_gdn_prep: query/key
  * normalisation, gates from raw inputs).
  *
@@ -199,6 +200,34 @@ lumo_status lumo_tree_conv_gather(const lumo_gdn_dims* dims, const lumo_tree_des
                                   void* stream);
 
 /*
+ * lumo_tree_conv_gather_pending - publish the previous iteration's accepted path into
+ * the conv history, then the tree convolution of this iteration from the published
+ * history (Alg. 1: publication of iteration t-1 precedes iteration t; Sec. V-C). For
+ * every request r and layer l with a valid pending path of length L (1 <= L <=
+ * max_path; the previous tree had nodes):
+ *   conv_hist[r][l] <- the last three entries of (conv_hist[r][l], x_prev rows of the
+ *                      path), in place, exactly as lumo_gdn_commit would publish them;
+ *   y               <- lumo_tree_conv_gather from that history.
+ * A pending length <= 0 (none, or invalid: -1) or > max_path leaves conv_hist as it is.
+ * Requests with no nodes in this iteration are still published. The result equals
+ * lumo_gdn_commit's history publication followed by lumo_tree_conv_gather, bit for bit;
+ * the commit of the previous iteration is then called with a NULL conv_hist (and NULL
+ * x), so that it only derives path_out and path_len.
+ *   desc, x, w, bias, act, y   this iteration, as lumo_tree_conv_gather
+ *   conv_hist                  in/out [n_req][layers][3][channels]
+ *   pend_desc                  the previous iteration's descriptor (same n_req)
+ *   max_path, path_out, path_len   as written by that iteration's lumo_gdn_commit
+ *   x_prev                     the previous iteration's x, [layers][its rows][channels]
+ *                              (nullable when the previous tree had no nodes)
+ */
+lumo_status lumo_tree_conv_gather_pending(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                          int32_t channels, const void* x, void* conv_hist,
+                                          const float* w, const float* bias, int32_t act, void* y,
+                                          const lumo_tree_desc* pend_desc, int32_t max_path,
+                                          const int32_t* path_out, const int32_t* path_len,
+                                          const void* x_prev, void* stream);
+
+/*
  * lumo_gdn_prep - operand preparation inside the kernels (Sec. IV-B: verification
  * takes raw gate inputs and normalises queries and keys itself). Applies to every
  * node of the call (tree nodes, path nodes replayed, pending path nodes).
@@ -306,7 +335,9 @@ lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, const lumo_t
  *                  (k, v, g, beta may then be NULL too): only path_out, path_len and
  *                  the conv history are written
  *   x, conv_hist   nullable pair: when given, conv_hist[r][l] becomes the last
- *                  three entries of (conv_hist[r][l], x rows of the path), in place
+ *                  three entries of (conv_hist[r][l], x rows of the path), in place;
+ *                  NULL leaves that publication to the next
+ *                  lumo_tree_conv_gather_pending
  */
 lumo_status lumo_gdn_commit(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
                             int32_t max_path, const int32_t* accepted_node, int32_t* path_out,

@@ -4,7 +4,7 @@ kernels; torch tensors only provide device memory and the current HIP stream.
 
 The functions keep the names of the C ABI (include/lumo_tree.h):
   lumo_tree_plan, lumo_tree_gdn_workspace_bytes, lumo_tree_conv_gather,
-  lumo_tree_gdn_verify, lumo_tree_gdn_verify_prep, lumo_tree_gdn_verify_pending, lumo_gdn_commit,
+  lumo_tree_conv_gather_pending, lumo_tree_gdn_verify, lumo_tree_gdn_verify_prep, lumo_tree_gdn_verify_pending, lumo_gdn_commit,
   lumo_gdn_commit_prep, lumo_tree_attention, lumo_tree_attention_workspace_bytes,
   lumo_tree_attention_splits, lumo_gdn_commit_graph_create,
   lumo_gdn_commit_graph_launch, lumo_gdn_commit_graph_destroy, lumo_last_error,
@@ -99,6 +99,7 @@ def _load():
     L.lumo_tree_gdn_workspace_bytes.argtypes = [PD, ctypes.POINTER(lumo_plan)]
     L.lumo_tree_gdn_workspace_bytes.restype = SZ
     L.lumo_tree_conv_gather.argtypes = [PD, PT, I32, P, P, P, P, I32, P, P]
+    L.lumo_tree_conv_gather_pending.argtypes = [PD, PT, I32, P, P, P, P, I32, P, PT, I32, P, P, P, P]
     L.lumo_tree_gdn_verify.argtypes = [PD, PT, P, P, P, P, P, P, P, P, P, SZ, I32, P]
     PP = ctypes.POINTER(lumo_gdn_prep)
     PA = ctypes.POINTER(lumo_attn_dims)
@@ -119,7 +120,7 @@ def _load():
     L.lumo_gdn_commit_graph_destroy.restype = None
     L.lumo_last_error.restype = ctypes.c_char_p
     L.lumo_version.restype = ctypes.c_char_p
-    for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_gdn_verify",
+    for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_conv_gather_pending", "lumo_tree_gdn_verify",
               "lumo_tree_gdn_verify_prep", "lumo_tree_gdn_verify_pending", "lumo_gdn_commit",
               "lumo_gdn_commit_prep", "lumo_tree_attention", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
         getattr(L, f).restype = ctypes.c_int
@@ -215,6 +216,15 @@ def lumo_tree_conv_gather(d, desc: TreeDesc, channels, x, conv_hist, w, bias, ac
     _check(_lib.lumo_tree_conv_gather(ctypes.byref(d), ctypes.byref(desc.desc), int(channels),
                                       _dptr(x), _dptr(conv_hist), _dptr(w), _dptr(bias), int(act),
                                       _dptr(y), _stream(stream)))
+
+
+def lumo_tree_conv_gather_pending(d, desc: TreeDesc, channels, x, conv_hist, w, bias, act, y,
+                                  pend_desc: TreeDesc, max_path, path_out, path_len, x_prev,
+                                  stream=None):
+    _check(_lib.lumo_tree_conv_gather_pending(
+        ctypes.byref(d), ctypes.byref(desc.desc), int(channels), _dptr(x), _dptr(conv_hist), _dptr(w),
+        _dptr(bias), int(act), _dptr(y), ctypes.byref(pend_desc.desc), int(max_path), _dptr(path_out),
+        _dptr(path_len), _dptr(x_prev), _stream(stream)))
 
 
 def lumo_tree_gdn_verify(d, desc: TreeDesc, q, k, v, g, beta, state0, o, node_states=None,

@@ -142,6 +142,39 @@ extern "C" lumo_status lumo_tree_conv_gather(const lumo_gdn_dims* dims, const lu
     return LUMO_OK;
 }
 
+extern "C" lumo_status lumo_tree_conv_gather_pending(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                                     int32_t channels, const void* x, void* conv_hist,
+                                                     const float* w, const float* bias, int32_t act, void* y,
+                                                     const lumo_tree_desc* pend_desc, int32_t max_path,
+                                                     const int32_t* path_out, const int32_t* path_len,
+                                                     const void* x_prev, void* stream) {
+    static const char* fn = "lumo_tree_conv_gather_pending";
+    clear_error();
+    LUMO_TRY(check_dims(dims, fn));
+    LUMO_TRY(check_desc(dims, desc, fn));
+    if (!pend_desc) return fail(LUMO_EINVAL, "%s: pend_desc is NULL", fn);
+    LUMO_TRY(check_desc(dims, pend_desc, fn));
+    if (channels <= 0 || channels % 8) return fail(LUMO_ESHAPE, "%s: channels %d must be a positive multiple of 8", fn, channels);
+    if (act != 0 && act != 1) return fail(LUMO_EINVAL, "%s: act %d (0 identity, 1 SiLU)", fn, act);
+    if (max_path < 1 || max_path > 4096) return fail(LUMO_EINVAL, "%s: max_path %d (1..4096)", fn, max_path);
+    if (dims->n_req == 0) return LUMO_OK;
+    LUMO_TRY(check_ptr(conv_hist, fn, "conv_hist"));
+    LUMO_TRY(check_ptr(path_out, fn, "path_out"));
+    LUMO_TRY(check_ptr(path_len, fn, "path_len"));
+    if (pend_desc->plan.total_nodes > 0) LUMO_TRY(check_ptr(x_prev, fn, "x_prev"));
+    if (desc->plan.total_nodes > 0) {
+        LUMO_TRY(check_ptr(x, fn, "x"));
+        LUMO_TRY(check_ptr(w, fn, "w"));
+        LUMO_TRY(check_ptr(bias, fn, "bias", true));
+        LUMO_TRY(check_ptr(y, fn, "y"));
+    }
+    ConvArgs a{channels, x, conv_hist, w, bias, act, y};
+    ConvPendArgs pa{pend_desc, max_path, path_out, path_len, x_prev};
+    hipError_t e = launch_conv(*dims, *desc, a, static_cast<hipStream_t>(stream), &pa);
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
 extern "C" lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lumo_tree_desc* desc, const void* q,
                                             const void* k, const void* v, const float* g, const float* beta,
                                             const float* state0, void* o, float* node_states, void* workspace,

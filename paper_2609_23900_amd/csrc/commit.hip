@@ -280,20 +280,23 @@ __global__ __launch_bounds__(256) void path_hist_kernel(PathParams pp, HistParam
     node[2] = a;
     node[1] = len >= 2 ? pp.blob[pp.o_parent + base + a] : -1;
     node[0] = len >= 3 ? pp.blob[pp.o_parent + base + node[1]] : -1;
-    constexpr int W = 16 / sizeof(T) >= 8 ? 1 : 2;  // uint4 loads per 8 channels
-    uint4 val[3][W];
+    const T* src[3];
 #pragma unroll
     for (int e = 0; e < 3; ++e) {
         const int pos = len + e;
-        const T* src = pos < 3 ? hist + (long)pos * p.channels + c
-                               : x + ((long)l * p.total_rows + p.blob[p.o_row + base + node[e]]) * p.channels + c;
-#pragma unroll
-        for (int w = 0; w < W; ++w) val[e][w] = reinterpret_cast<const uint4*>(src)[w];
+        src[e] = pos < 3 ? hist + (long)pos * p.channels + c
+                         : x + ((long)l * p.total_rows + p.blob[p.o_row + base + node[e]]) * p.channels + c;
     }
+    constexpr int W = 16 / sizeof(T) >= 8 ? 1 : 2;  // 16-byte pieces per 8 channels
 #pragma unroll
-    for (int e = 0; e < 3; ++e)
-#pragma unroll
-        for (int w = 0; w < W; ++w) reinterpret_cast<uint4*>(hist + (long)e * p.channels + c)[w] = val[e][w];
+    for (int w = 0; w < W; ++w) {  // each piece read whole before it is overwritten
+        const uint4 v0 = reinterpret_cast<const uint4*>(src[0])[w];
+        const uint4 v1 = reinterpret_cast<const uint4*>(src[1])[w];
+        const uint4 v2 = reinterpret_cast<const uint4*>(src[2])[w];
+        reinterpret_cast<uint4*>(hist + c)[w] = v0;
+        reinterpret_cast<uint4*>(hist + (long)p.channels + c)[w] = v1;
+        reinterpret_cast<uint4*>(hist + 2L * p.channels + c)[w] = v2;
+    }
 }
 
 template <int DK, int OPT>

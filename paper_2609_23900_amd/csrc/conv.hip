@@ -60,6 +60,69 @@ template <> struct Vec8<1> {
     }
 };
 
+// Publication of the previous iteration's accepted path into the conv history, deferred
+// into this iteration's conv (Alg. 1: iteration t-1's path is published before
+// iteration t reads the history). The history of (request r, layer l) becomes the last
+// three entries of (history, rows of the previous x along the pending path), in place,
+// before the windows read it. A pending length <= 0 or > max_path, or a previous tree
+// without nodes, leaves the history as it is.
+struct HistPend {
+    const int32_t* blob;  // previous iteration's plan
+    int32_t o_node_off, o_row, total_rows, max_path;
+    const int32_t* path_out;  // [n_req][max_path], root first
+    const int32_t* path_len;  // [n_req]
+    const void* x_prev;       // previous iteration's x, [layers][its rows][channels]
+    void* hist;               // the history, written in place
+};
+
+__device__ __forceinline__ int pend_hist_len(const HistPend& q, int r) {
+    const int len = q.path_len[r];
+    return (len > q.max_path || q.blob[q.o_node_off + r + 1] <= q.blob[q.o_node_off + r]) ? 0 : len;
+}
+
+// Source of entry e (0..2) of the published history at channel c, len >= 1: entry
+// len + e of (history, previous x rows of the path). Path entries are clamped to the
+// previous tree's nodes.
+template <class T>
+__device__ __forceinline__ const T* pend_hist_src(const HistPend& q, const T* hist_rl, int r, int l, int len,
+                                                  int e, int channels, int c) {
+    const int pos = len + e;
+    if (pos < 3) return hist_rl + (long)pos * channels + c;
+    const int base = q.blob[q.o_node_off + r];
+    const int pn = q.blob[q.o_node_off + r + 1] - base;
+    const int node = min(max(q.path_out[(long)r * q.max_path + pos - 3], 0), pn - 1);
+    const int row = q.blob[q.o_row + base + node];
+    return static_cast<const T*>(q.x_prev) + ((long)l * q.total_rows + row) * channels + c;
+}
+
+// Standalone publication, ahead of the run kernel: one block per (request, layer,
+// 2048 channels), 8 channels per thread.
+template <int OPT>
+__global__ __launch_bounds__(256) void hist_pend_kernel(HistPend q, int n_layers, int channels, int n_cchunks) {
+    using T = typename Op<OPT>::T;
+    const int cc = blockIdx.x % n_cchunks;
+    const int l = (blockIdx.x / n_cchunks) % n_layers;
+    const int r = blockIdx.x / (n_cchunks * n_layers);
+    const int len = pend_hist_len(q, r);
+    if (len <= 0) return;
+    const int c = (cc * 256 + (int)threadIdx.x) * 8;
+    if (c >= channels) return;
+    T* h = static_cast<T*>(q.hist) + (((long)r * n_layers + l) * 3) * channels;
+    const T* s0 = pend_hist_src<T>(q, h, r, l, len, 0, channels, c);
+    const T* s1 = pend_hist_src<T>(q, h, r, l, len, 1, channels, c);
+    const T* s2 = pend_hist_src<T>(q, h, r, l, len, 2, channels, c);
+    constexpr int W = 16 / sizeof(T) >= 8 ? 1 : 2;  // 16-byte pieces per 8 channels
+#pragma unroll
+    for (int w = 0; w < W; ++w) {  // each piece read whole before it is overwritten
+        const uint4 v0 = reinterpret_cast<const uint4*>(s0)[w];
+        const uint4 v1 = reinterpret_cast<const uint4*>(s1)[w];
+        const uint4 v2 = reinterpret_cast<const uint4*>(s2)[w];
+        reinterpret_cast<uint4*>(h + c)[w] = v0;
+        reinterpret_cast<uint4*>(h + (long)channels + c)[w] = v1;
+        reinterpret_cast<uint4*>(h + 2L * channels + c)[w] = v2;
+    }
+}
+
 // One block: one layer, 2048 channels (8 per thread), a run of kNodesPerBlock nodes.
 // The taps and bias of the thread's channels stay in registers across the run; the
 // window rows of consecutive nodes (parents, grandparents) are mostly L2 hits.
@@ -146,7 +209,10 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
 // channels, the x entries of the current root path (after the three history entries)
 // in registers, so every x row is read from memory exactly once. A node at depth d has
 // the window (ext[d], ext[d+1], ext[d+2], x_node) with ext = (history, path by depth);
-// taps, accumulation order, activation and cast are those of conv_kernel.
+// taps, accumulation order, activation and cast are those of conv_kernel. With PH the
+// block first publishes the pending path into its slice of the history (which no other
+// block reads) and takes the three entries from registers; requests without nodes in
+// this iteration only publish.
 constexpr int kDfsWin = 512;  // preorder positions staged in LDS at a time
 constexpr int kDfsGroup = 4;  // nodes whose rows are loaded one group ahead
 
@@ -188,8 +254,8 @@ __device__ __forceinline__ void dfs_taps(int d, uint4 (&ext)[DD + 3], const uint
     asm volatile("" ::"n"(D) : "memory");
 }
 
-template <int DD>
-__global__ __launch_bounds__(256) void conv_dfs_kernel(ConvDfsParams p) {
+template <int DD, bool PH>
+__global__ __launch_bounds__(256) void conv_dfs_kernel(ConvDfsParams p, HistPend hp) {
     int t = xcd_remap(blockIdx.x, gridDim.x);
     const int cc = t % p.n_cchunks;
     t /= p.n_cchunks;
@@ -197,11 +263,28 @@ __global__ __launch_bounds__(256) void conv_dfs_kernel(ConvDfsParams p) {
     const int l = t / p.n_req;
     const int base = p.blob[p.o_node_off + r];
     const int N = p.blob[p.o_node_off + r + 1] - base;
-    if (N <= 0) return;  // uniform over the block
     const int tid = (int)threadIdx.x;
     const int c0ch = (cc * 256 + tid) * 8;
     const bool has_c = c0ch < p.channels;
     const int c = has_c ? c0ch : p.channels - 8;
+    uint4 ext[DD + 3];
+    const uint16_t* hr = p.hist + ((long)r * p.n_layers + l) * 3 * p.channels + c;
+    const int plen = PH ? pend_hist_len(hp, r) : 0;  // uniform
+    if (plen > 0) {
+        const uint16_t* hrl = p.hist + ((long)r * p.n_layers + l) * 3 * p.channels;
+#pragma unroll
+        for (int e = 0; e < 3; ++e)
+            ext[e] = *reinterpret_cast<const uint4*>(pend_hist_src<uint16_t>(hp, hrl, r, l, plen, e, p.channels, c));
+        if (has_c) {
+            uint16_t* hw = static_cast<uint16_t*>(hp.hist) + ((long)r * p.n_layers + l) * 3 * p.channels + c;
+#pragma unroll
+            for (int e = 0; e < 3; ++e) *reinterpret_cast<uint4*>(hw + (long)e * p.channels) = ext[e];
+        }
+    } else if (N > 0) {
+#pragma unroll
+        for (int e = 0; e < 3; ++e) ext[e] = *reinterpret_cast<const uint4*>(hr + (long)e * p.channels);
+    }
+    if (N <= 0) return;  // uniform over the block
     float wt[32];
     const float4* wp = reinterpret_cast<const float4*>(p.w + ((long)l * p.channels + c) * 4);
 #pragma unroll
@@ -212,10 +295,6 @@ __global__ __launch_bounds__(256) void conv_dfs_kernel(ConvDfsParams p) {
     float b0[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) b0[e] = p.bias ? p.bias[(long)l * p.channels + c + e] : 0.f;
-    uint4 ext[DD + 3];
-    const uint16_t* hr = p.hist + ((long)r * p.n_layers + l) * 3 * p.channels + c;
-#pragma unroll
-    for (int e = 0; e < 3; ++e) ext[e] = *reinterpret_cast<const uint4*>(hr + (long)e * p.channels);
 #pragma unroll
     for (int e = 3; e < DD + 3; ++e) ext[e] = make_uint4(0, 0, 0, 0);  // written before read in preorder
     const uint16_t* xl = p.x + (long)l * p.total_rows * p.channels + c;
@@ -279,8 +358,71 @@ __global__ __launch_bounds__(256) void conv_dfs_kernel(ConvDfsParams p) {
 
 }  // namespace
 
-hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const ConvArgs& a, hipStream_t s) {
+hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const ConvArgs& a, hipStream_t s,
+                       const ConvPendArgs* pend) {
     const lumo_plan& pl = desc.plan;
+    const int n_cchunks = (a.channels + 2047) / 2048;
+    HistPend hq{};
+    if (pend) {
+        const lumo_plan& pp = pend->desc->plan;
+        hq.blob = pend->desc->blob;
+        hq.o_node_off = pp.o_node_off;
+        hq.o_row = pp.o_row;
+        hq.total_rows = pp.total_rows;
+        hq.max_path = pend->max_path;
+        hq.path_out = pend->path_out;
+        hq.path_len = pend->path_len;
+        hq.x_prev = pend->x_prev;
+        hq.hist = const_cast<void*>(a.hist);
+    }
+    // The depth-first walk reads every x row once but runs one block per (request, layer,
+    // channel block), each walking its request's nodes in sequence: it is chosen when
+    // that gives at least four blocks per CU; otherwise the run kernel's parallelism over
+    // node runs wins (measured: one request or one layer of 128-256-node trees).
+    const long dfs_blocks = (long)d.n_req * d.n_layers * n_cchunks;
+    const bool dfs = d.op_dtype == LUMO_BF16 && pl.max_depth <= 16 && dfs_blocks >= 4 * 256;
+    if (pend && !dfs) {  // publish first, then the run kernel reads the history
+        const long hb = (long)d.n_req * d.n_layers * n_cchunks;
+        if (d.op_dtype == LUMO_BF16)
+            hipLaunchKernelGGL(hist_pend_kernel<1>, dim3((unsigned)hb), dim3(256), 0, s, hq, d.n_layers, a.channels,
+                               n_cchunks);
+        else
+            hipLaunchKernelGGL(hist_pend_kernel<0>, dim3((unsigned)hb), dim3(256), 0, s, hq, d.n_layers, a.channels,
+                               n_cchunks);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (dfs && (pl.total_nodes > 0 || pend)) {  // with pend, requests without nodes still publish
+        ConvDfsParams q;
+        q.blob = desc.blob;
+        q.o_node_off = pl.o_node_off;
+        q.o_pre_row = pl.o_pre_row;
+        q.o_pre_depth = pl.o_pre_depth;
+        q.n_req = d.n_req;
+        q.total_rows = pl.total_rows;
+        q.n_layers = d.n_layers;
+        q.channels = a.channels;
+        q.n_cchunks = n_cchunks;
+        q.act = a.act;
+        q.x = static_cast<const uint16_t*>(a.x);
+        q.hist = static_cast<const uint16_t*>(a.hist);
+        q.w = a.w;
+        q.bias = a.bias;
+        q.y = static_cast<uint16_t*>(a.y);
+        const dim3 grid((unsigned)dfs_blocks);
+        if (pl.max_depth <= 8) {
+            if (pend)
+                hipLaunchKernelGGL((conv_dfs_kernel<8, true>), grid, dim3(256), 0, s, q, hq);
+            else
+                hipLaunchKernelGGL((conv_dfs_kernel<8, false>), grid, dim3(256), 0, s, q, hq);
+        } else {
+            if (pend)
+                hipLaunchKernelGGL((conv_dfs_kernel<16, true>), grid, dim3(256), 0, s, q, hq);
+            else
+                hipLaunchKernelGGL((conv_dfs_kernel<16, false>), grid, dim3(256), 0, s, q, hq);
+        }
+        return hipGetLastError();
+    }
     if (pl.total_nodes == 0) return hipSuccess;
     ConvParams p;
     p.blob = desc.blob;
@@ -291,43 +433,14 @@ hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.total_rows = pl.total_rows;
     p.n_layers = d.n_layers;
     p.channels = a.channels;
-    p.n_cchunks = (a.channels + 2047) / 2048;
+    p.n_cchunks = n_cchunks;
     p.act = a.act;
     p.x = a.x;
     p.hist = a.hist;
     p.w = a.w;
     p.bias = a.bias;
     p.y = a.y;
-    // The depth-first walk reads every x row once but runs one block per (request, layer,
-    // channel block), each walking its request's nodes in sequence: it is chosen when
-    // that gives at least four blocks per CU; otherwise the run kernel's parallelism over
-    // node runs wins (measured: one request or one layer of 128-256-node trees).
-    const long dfs_blocks = (long)d.n_req * d.n_layers * p.n_cchunks;
-    if (d.op_dtype == LUMO_BF16 && pl.max_depth <= 16 && dfs_blocks >= 4 * 256) {
-        ConvDfsParams q;
-        q.blob = desc.blob;
-        q.o_node_off = pl.o_node_off;
-        q.o_pre_row = pl.o_pre_row;
-        q.o_pre_depth = pl.o_pre_depth;
-        q.n_req = d.n_req;
-        q.total_rows = pl.total_rows;
-        q.n_layers = d.n_layers;
-        q.channels = a.channels;
-        q.n_cchunks = p.n_cchunks;
-        q.act = a.act;
-        q.x = static_cast<const uint16_t*>(a.x);
-        q.hist = static_cast<const uint16_t*>(a.hist);
-        q.w = a.w;
-        q.bias = a.bias;
-        q.y = static_cast<uint16_t*>(a.y);
-        const long nb = (long)d.n_layers * d.n_req * q.n_cchunks;
-        if (pl.max_depth <= 8)
-            hipLaunchKernelGGL(conv_dfs_kernel<8>, dim3((unsigned)nb), dim3(256), 0, s, q);
-        else
-            hipLaunchKernelGGL(conv_dfs_kernel<16>, dim3((unsigned)nb), dim3(256), 0, s, q);
-        return hipGetLastError();
-    }
-    const long blocks = (long)d.n_layers * p.n_cchunks * ((pl.total_nodes + kNodesPerBlock - 1) / kNodesPerBlock);
+    const long blocks = (long)d.n_layers * n_cchunks * ((pl.total_nodes + kNodesPerBlock - 1) / kNodesPerBlock);
     if (d.op_dtype == LUMO_BF16)
         hipLaunchKernelGGL(conv_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, s, p);
     else

@@ -81,7 +81,18 @@ struct ConvArgs {
     void* y;
 };
 
-hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const ConvArgs& a, hipStream_t s);
+// The previous iteration's accepted path, published into the conv history by the conv
+// of this iteration (lumo_tree_conv_gather_pending).
+struct ConvPendArgs {
+    const lumo_tree_desc* desc;  // previous iteration's descriptor
+    int32_t max_path;
+    const int32_t* path_out;
+    const int32_t* path_len;
+    const void* x_prev;
+};
+
+hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const ConvArgs& a, hipStream_t s,
+                       const ConvPendArgs* pend = nullptr);
 
 // Tree attention: split-K partial kernel plus the merge (workspace: n_split + 1 ranges).
 struct AttnArgs {

@@ -11,7 +11,8 @@ import numpy as np
 import torch
 
 from . import (LUMO_BF16, LumoError, TreeDesc, dims, lumo_gdn_commit_graph_create,
-               lumo_gdn_commit_prep, lumo_tree_conv_gather, lumo_tree_gdn_verify,
+               lumo_gdn_commit_prep, lumo_tree_conv_gather, lumo_tree_conv_gather_pending,
+               lumo_tree_gdn_verify,
                lumo_tree_gdn_verify_pending, lumo_tree_gdn_verify_prep,
                lumo_tree_gdn_workspace_bytes)
 
@@ -77,6 +78,16 @@ class GdnTreeStep:
         lumo_tree_conv_gather(self.dims, self.desc, self.channels, self.x, self.hist, self.w,
                               self.bias, self.act, self.y, stream)
 
+    def conv_pending(self, prev: "GdnTreeStep", stream=None):
+        """Publish prev's accepted path (written by prev.commit(defer=True, with_conv=False))
+        into the conv history, then the tree conv of this step from it, in one launch."""
+        if not self.has_conv:
+            raise LumoError(1, "no conv operands")
+        lumo_tree_conv_gather_pending(self.dims, self.desc, self.channels, self.x, self.hist, self.w,
+                                      self.bias, self.act, self.y, prev.desc, prev.max_path,
+                                      prev.path_out, prev.path_len, prev.x if prev.has_conv else None,
+                                      stream)
+
     def verify(self, stream=None, state0=None):
         s0 = self.state if state0 is None else state0
         if self.prep is not None:
@@ -98,7 +109,8 @@ class GdnTreeStep:
                                      prev.t["v"], prev.t["g"], prev.t["beta"], stream, self.prep)
 
     def commit(self, stream=None, with_conv=True, defer=False):
-        """Accepted path, conv history and (unless defer) the replay into self.state."""
+        """Accepted path, conv history (unless with_conv is False: then the next
+        conv_pending publishes it) and (unless defer) the replay into self.state."""
         use_conv = with_conv and self.has_conv
         lumo_gdn_commit_prep(self.dims, self.desc, self.prep, self.max_path, self.accepted,
                              self.path_out, self.path_len, self.t["k"], self.t["v"], self.t["g"],

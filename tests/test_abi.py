@@ -144,6 +144,38 @@ def test_conv_rejects_bad_arguments():
              P(FAKE), None) == L.LUMO_EINVAL
 
 
+def _conv_pending(d, desc, pdesc, *, channels=16, act=1, max_path=4, hist=FAKE, x_prev=FAKE, path=FAKE,
+                  pend_desc=True):
+    P = ctypes.c_void_p
+    return L._lib.lumo_tree_conv_gather_pending(
+        ctypes.byref(d), ctypes.byref(desc), channels, P(FAKE), P(hist) if hist else None, P(FAKE), None, act,
+        P(FAKE), ctypes.byref(pdesc) if pend_desc else None, max_path, P(path) if path else None, P(FAKE),
+        P(x_prev) if x_prev else None, None)
+
+
+def test_conv_pending_rejects_bad_arguments():
+    desc, _b1 = _desc()
+    two, _b2 = _desc(n_req=2)
+    d = _dims()
+    assert _conv_pending(d, desc, desc, channels=12) == L.LUMO_ESHAPE
+    assert _conv_pending(d, desc, desc, act=2) == L.LUMO_EINVAL
+    assert _conv_pending(d, desc, desc, max_path=0) == L.LUMO_EINVAL
+    assert _conv_pending(d, desc, two) == L.LUMO_EDESC            # request counts differ
+    assert _conv_pending(d, desc, desc, pend_desc=False) == L.LUMO_EINVAL
+    assert _conv_pending(d, desc, desc, hist=0) == L.LUMO_EINVAL
+    assert "conv_hist" in L.lumo_last_error()
+    assert _conv_pending(d, desc, desc, path=0) == L.LUMO_EINVAL
+    assert _conv_pending(d, desc, desc, x_prev=0) == L.LUMO_EINVAL  # the previous tree has nodes
+    assert "x_prev" in L.lumo_last_error()
+    assert _conv_pending(d, desc, desc, x_prev=FAKE + 2) == L.LUMO_EINVAL
+
+
+def test_conv_pending_empty_batch_is_a_no_op():
+    plan, blob = L.lumo_tree_plan(np.array([0], np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32), 0)
+    desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
+    assert _conv_pending(_dims(n_req=0), desc, desc, hist=0, path=0, x_prev=0) == L.LUMO_OK
+
+
 def test_graph_create_rejects_and_null_launch():
     desc, _blob = _desc()
     h = ctypes.c_void_p()

@@ -39,6 +39,8 @@ def test_algorithmic_work_batched():
     assert ab["commit_updates"] == upd
     assert ab["commit_bytes"] == inst * 2 * 65536 + upd * (128 + 256 + 8)
     assert ab["pub_bytes"] == ab["commit_bytes"] - inst * 65536
+    # history publication: three x rows read and three entries written per (request, layer)
+    assert ab["hist_pub_bytes"] == 8 * 48 * 3 * 8192 * 2 * 2
     # x read + y written and the history read (824.2 MB), plus the taps (6.3 MB)
     assert ab["conv_bytes"] == 512 * 48 * 8192 * 4 + 8 * 48 * 3 * 8192 * 2 + 48 * 8192 * 16
     assert abs(ab["conv_bytes"] / 1e6 - 830.5) < 0.1

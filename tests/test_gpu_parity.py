@@ -569,6 +569,98 @@ def test_conv_tree_shapes(case):
     assert np.all(got[:, pad] == 0)
 
 
+def _conv_wl(parents, n_rows, n_layers, C, op_dtype, seed, max_path=24):
+    wl = pins.make_wl(parents, d_k=128, d_v=128, op_dtype=op_dtype, n_rows=n_rows, n_layers=n_layers,
+                      max_path=max_path, channels=C)
+    wl.arrays = ops.make_conv_operands(seed, n_req=len(parents), n_layers=n_layers, total_rows=wl.total_rows,
+                                       channels=C, op_dtype=op_dtype)
+    return wl
+
+
+def _dev(a, bf):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    return (t.view(torch.bfloat16) if bf else t).cuda()
+
+
+@pytest.mark.parametrize("case", ["depth_first", "runs", "f32"])
+def test_conv_pending_history(case):
+    """lumo_tree_conv_gather_pending publishes the previous iteration's accepted paths
+    into the history, then convolves this iteration's tree from it. The history and y
+    must equal the commit's publication followed by the plain conv, bit for bit, and the
+    oracle's publication (exactly) and conv (to tolerance). The previous iteration has a
+    path of more than three nodes (only x entries), one of two nodes (history and x),
+    none (accepted -1), and an invalid one (accepted out of range: nothing published);
+    this iteration has a request without nodes, which is still published. depth_first:
+    4 requests x 64 layers x 4 channel blocks (the depth-first kernel publishes in
+    place); runs: 3 layers, 2056 channels (a separate publication, then the run kernel);
+    f32: the same with fp32 operands."""
+    rng = np.random.default_rng(47)
+    bf = case != "f32"
+    opd = ops.BF16 if bf else ops.F32
+    n_layers, C = (64, 8192) if case == "depth_first" else (3, 2056)
+    prev_par = [trees.random_tree(rng, 30, 8, trees.bmax_uniform(3)), trees.chain(5), trees.FIG1_PARENT,
+                trees.random_tree(rng, 12, 6, trees.bmax_uniform(3))]
+    deep = int(np.argmax(trees.depths(prev_par[0])))
+    prev_acc = np.array([deep, 1, -1, 99], np.int32)
+    cur_par = [trees.random_tree(rng, 20, 8, trees.bmax_uniform(3)), np.zeros(0, np.int32), trees.chain(16),
+               trees.FIG1_PARENT]
+    prev = _conv_wl(prev_par, [31, 5, 7, 14], n_layers, C, opd, 51)
+    cur = _conv_wl(cur_par, [20, 2, 16, 9], n_layers, C, opd, 52)
+    cur.arrays["hist"] = prev.arrays["hist"]
+    bias = rng.standard_normal((n_layers, C)).astype(np.float32) if case == "depth_first" else None
+    say(f"[gpu] conv pending {case}")
+    dt = L.LUMO_BF16 if bf else L.LUMO_F32
+    d = L.dims(4, n_layers, 1, 1, 128, 128, dt)
+    pdesc = L.TreeDesc.build(prev.node_off, prev.parent_flat, prev.n_rows)
+    cdesc = L.TreeDesc.build(cur.node_off, cur.parent_flat, cur.n_rows)
+    max_path = prev.max_path
+    acc = torch.from_numpy(prev_acc).cuda()
+    po = torch.full((4, max_path), -7, dtype=torch.int32, device="cuda")
+    pl = torch.full((4,), -7, dtype=torch.int32, device="cuda")
+    xp, xc = _dev(prev.arrays["x"], bf), _dev(cur.arrays["x"], bf)
+    w = torch.from_numpy(cur.arrays["w"]).cuda()
+    b = torch.from_numpy(bias).cuda() if bias is not None else None
+    odt = torch.bfloat16 if bf else torch.float32
+    # reference order: the commit publishes the history, then the plain conv
+    hist_ref = _dev(prev.arrays["hist"], bf)
+    y_ref = torch.zeros((n_layers, cur.total_rows, C), dtype=odt, device="cuda")
+    L.lumo_gdn_commit(d, pdesc, max_path, acc, po, pl, None, None, None, None, None, C, xp, hist_ref)
+    L.lumo_tree_conv_gather(d, cdesc, C, xc, hist_ref, w, b, 1, y_ref)
+    # deferred: the commit derives the path only; the next conv publishes
+    po2 = torch.full((4, max_path), -7, dtype=torch.int32, device="cuda")
+    pl2 = torch.full((4,), -7, dtype=torch.int32, device="cuda")
+    hist = _dev(prev.arrays["hist"], bf)
+    y = torch.zeros((n_layers, cur.total_rows, C), dtype=odt, device="cuda")
+    L.lumo_gdn_commit(d, pdesc, max_path, acc, po2, pl2, None, None, None, None, None, 0, None, None)
+    L.lumo_tree_conv_gather_pending(d, cdesc, C, xc, hist, w, b, 1, y, pdesc, max_path, po2, pl2, xp)
+    torch.cuda.synchronize()
+    assert pl2.cpu().numpy().tolist() == [int(trees.depths(prev_par[0])[deep]) + 1, 2, 0, -1]
+    assert torch.equal(hist.view(torch.int16 if bf else torch.int32), hist_ref.view(torch.int16 if bf else torch.int32))
+    assert torch.equal(y.view(torch.int16 if bf else torch.int32), y_ref.view(torch.int16 if bf else torch.int32))
+    # the oracle: paths from the parents (the invalid request publishes nothing: length 0)
+    opo = np.full((4, max_path), -1, np.int32)
+    opl = np.zeros(4, np.int32)
+    for r in range(3):
+        path, ln = oracle.plan.accepted_path(prev_par[r], int(prev_acc[r]), max_path)
+        opo[r], opl[r] = path, ln
+    href = oracle.conv_hist_publish(prev, opo, opl)
+    assert np.array_equal(gu.to_np(hist).astype(np.float64), href)
+    cur.arrays["hist"] = href.astype(np.float32) if not bf else ops.to_bf16_bits(href.astype(np.float32))
+    yref = oracle.conv_all(cur, bias=bias)
+    rows = oracle.plan.flat_rows(cur.parents, cur.row_off)
+    assert gu.max_rel(gu.to_np(y)[:, rows], yref[:, rows]) <= (gu.TOL_BF16 if bf else gu.TOL_F32)
+    pad = [r for r in range(cur.total_rows) if r not in set(rows.tolist())]
+    assert np.all(gu.to_np(y)[:, pad] == 0)
+    if case == "runs":
+        # a batch without nodes in this iteration still publishes
+        empty = L.TreeDesc.build(np.zeros(5, np.int32), np.zeros(0, np.int32), np.ones(4, np.int32))
+        hist_e = _dev(prev.arrays["hist"], bf)
+        L.lumo_tree_conv_gather_pending(d, empty, C, None, hist_e, None, None, 1, None, pdesc, max_path, po2,
+                                        pl2, xp)
+        torch.cuda.synchronize()
+        assert torch.equal(hist_e.view(torch.int16), hist_ref.view(torch.int16))
+
+
 # ---------------------------------------------------------------- operand preparation
 
 QKN, RAWG = L.LUMO_PREP_QK_NORM, L.LUMO_PREP_RAW_GATES
