@@ -75,8 +75,9 @@ def _load(path):
     L.orc_conv_all.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P, I, P]
     L.orc_conv_hist_publish.argtypes = [I, I, I, I, I, P, P, P, P, I, P, P, P]
     L.orc_tree_attention.argtypes = [I, I, I, I, I, P, P, P, P, ctypes.c_double, P, P, P, P, P, P, P, I]
+    L.orc_draft_select.argtypes = [I, I, I, I, I, P, P, P, I]
     for f in ("orc_verify_nodes", "orc_verify_all", "orc_commit", "orc_conv_all",
-              "orc_conv_hist_publish", "orc_tree_attention", "orc_max_threads"):
+              "orc_conv_hist_publish", "orc_tree_attention", "orc_draft_select", "orc_max_threads"):
         getattr(L, f).restype = I
     return L
 
@@ -230,3 +231,20 @@ def tree_attention(parents, row_off, total_rows, ctx_off, q, k_ctx, v_ctx, k_tre
     if rc:
         raise ValueError("oracle: malformed tree")
     return o, lse
+
+
+def draft_select(logits, *, k, op_dtype, ties=0, n_threads=None):
+    """(spine [rows], cand [rows][k]) int32 of a logits array [rows][vocab] (Sec. V-D):
+    spine = lowest index among each row's maximal logits; cand = the k indices ranked
+    first by logit, descending, ties by index ascending (ties=0) or descending (ties=1).
+    NaN ranks above every number."""
+    x = _op(logits, op_dtype)
+    if x.ndim != 2:
+        raise ValueError("logits must be [rows][vocab]")
+    rows, vocab = x.shape
+    spine = np.empty(rows, np.int32)
+    cand = np.empty((rows, k), np.int32)
+    nt = n_threads if n_threads is not None else lib().orc_max_threads()
+    if lib().orc_draft_select(rows, vocab, int(k), int(op_dtype), int(ties), _p(x), _p(spine), _p(cand), int(nt)):
+        raise ValueError("oracle: k must be in 1..vocab and ties 0 or 1")
+    return spine, cand

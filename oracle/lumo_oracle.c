@@ -25,6 +25,8 @@
  *
  *   - Sec. V-B tree attention: every query row sees the committed context and its
  *     own ancestry (plain two-pass softmax in fp64, orc_tree_attention).
+ *   - Sec. V-D draft selection: the argmax (spine) token and the ordered top-k
+ *     candidates of a logits row, with their two tie conventions (orc_draft_select).
  *   - Sec. IV-B operand preparation (optional, prep_flags): verification takes raw
  *     gate inputs and normalises queries and keys itself. With ORC_PREP_QK_NORM
  *     every query and key row x is used as x / sqrt(|x|^2 + qk_eps); with
@@ -460,6 +462,60 @@ int orc_tree_attention(int n_req, int h_q, int h_kv, int d, int op_dtype, const 
     }
     (void)n_threads;
     return bad ? -1 : 0;
+}
+
+/*
+ * Fused draft selection (Sec. V-D): from one full-vocabulary logits row the principal
+ * (spine) token and k ordered sibling candidates, two outputs whose reference
+ * operations break ties differently:
+ *   spine[r]      = the lowest index among the maximal logits of row r (argmax);
+ *   cand[r][0..k) = the k indices ranked first by logit, descending, and among equal
+ *                   logits by index: ascending (ties = 0) or descending (ties = 1)
+ *                   (top-k). The spine token may appear among the candidates.
+ * A NaN logit ranks above every number (NaNs equal among themselves); -0 equals +0.
+ * Plain definition: one scan for the spine, then k selection passes over the row,
+ * each taking the best index not yet taken.
+ * logits [rows][vocab], float32 (dtype 0) or bfloat16 bit patterns (dtype 1).
+ */
+static int sel_greater(double a, double b) { /* a ranks strictly above b by value */
+    if (isnan(a)) return !isnan(b);
+    if (isnan(b)) return 0;
+    return a > b;
+}
+
+static int sel_before(double a, int ia, double b, int ib, int ties) {
+    if (sel_greater(a, b)) return 1;
+    if (sel_greater(b, a)) return 0;
+    return ties == 0 ? ia < ib : ia > ib;
+}
+
+int orc_draft_select(int rows, int vocab, int k, int op_dtype, int ties, const void* logits, int* spine,
+                     int* cand, int n_threads) {
+    if (k < 1 || k > vocab || (ties != 0 && ties != 1)) return 1;
+#ifdef _OPENMP
+#pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads > 0 ? n_threads : 1)
+#endif
+    for (int r = 0; r < rows; ++r) {
+        const long base = (long)r * vocab;
+        int best = 0;
+        for (int i = 1; i < vocab; ++i)
+            if (sel_greater(ld_op(logits, base + i, op_dtype), ld_op(logits, base + best, op_dtype))) best = i;
+        spine[r] = best;
+        for (int j = 0; j < k; ++j) {
+            int pick = -1;
+            for (int i = 0; i < vocab; ++i) {
+                int taken = 0;
+                for (int m = 0; m < j; ++m)
+                    if (cand[(long)r * k + m] == i) taken = 1;
+                if (taken) continue;
+                if (pick < 0 || sel_before(ld_op(logits, base + i, op_dtype), i,
+                                           ld_op(logits, base + pick, op_dtype), pick, ties))
+                    pick = i;
+            }
+            cand[(long)r * k + j] = pick;
+        }
+    }
+    return 0;
 }
 
 int orc_max_threads(void) {

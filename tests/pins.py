@@ -25,6 +25,7 @@ import numpy as np
 
 import oracle
 from lumo_synth import configs, trees
+from lumo_synth import operands as ops
 from lumo_synth.configs import Workload
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
@@ -663,6 +664,95 @@ def pin_attention_context_order_and_padding():
     np.testing.assert_allclose(o2[rows], o1[rows], rtol=1e-12, atol=1e-14)
     np.testing.assert_allclose(l2[rows], l1[rows], rtol=1e-13)
     assert np.all(np.isfinite(o2[rows]))
+
+
+def _tied_logits(rng, rows, vocab, levels):
+    """Logits drawn from a few levels, so that ties are common; some -inf entries."""
+    x = rng.integers(0, levels, size=(rows, vocab)).astype(np.float32) * 0.25 - 1.0
+    x[rng.random((rows, vocab)) < 0.05] = -np.inf
+    return x
+
+
+def pin_select_spine_is_numpy_argmax():
+    """The spine is numpy's argmax (first occurrence of the maximum; a NaN, if any, is
+    the maximum), also with ties, -inf, -0 against +0, and NaN entries."""
+    rng = np.random.default_rng(91)
+    x = _tied_logits(rng, 40, 300, 6)
+    x[3, 17] = np.nan
+    x[3, 5] = np.nan
+    x[4] = -np.inf
+    x[5] = 0.0
+    x[5, 2] = -0.0
+    x[6, :] = -0.0
+    x[6, 9] = 0.0
+    spine, _ = oracle.draft_select(x, k=3, op_dtype=0)
+    assert spine.tolist() == np.argmax(x.astype(np.float64), axis=1).tolist()
+
+
+def pin_select_distinct_is_argsort():
+    """With distinct logits the candidates are numpy's descending argsort, for both tie
+    conventions, and the spine is the first candidate."""
+    rng = np.random.default_rng(92)
+    x = np.stack([rng.permutation(500).astype(np.float32) - 250.0 for _ in range(12)])
+    for ties in (0, 1):
+        spine, cand = oracle.draft_select(x, k=5, op_dtype=0, ties=ties)
+        assert cand.tolist() == np.argsort(-x, axis=1)[:, :5].tolist()
+        assert spine.tolist() == cand[:, 0].tolist()
+
+
+def pin_select_brute_force():
+    """Tiny rows with heavy ties, NaN and infinities: the candidates are the first k of
+    all indices sorted by (NaN first, then value descending, then index in the tie
+    direction)."""
+    rng = np.random.default_rng(93)
+    vals = np.array([np.nan, np.inf, -np.inf, 1.5, 1.5, -0.0, 0.0, 2.0], np.float32)
+    for case in range(60):
+        vocab = int(rng.integers(3, 12))
+        row = vals[rng.integers(0, len(vals), size=vocab)][None, :]
+        k = int(rng.integers(1, vocab + 1))
+        for ties in (0, 1):
+            spine, cand = oracle.draft_select(row, k=k, op_dtype=0, ties=ties)
+
+            def key(i):
+                v = float(row[0, i])
+                tie = -i if ties == 0 else i
+                return (1, 0.0, tie) if np.isnan(v) else (0, v, tie)
+            want = sorted(range(vocab), key=key, reverse=True)[:k]
+            assert cand[0].tolist() == want, (case, ties, row, cand)
+            top = [i for i in range(vocab) if key(i)[:2] == key(want[0])[:2]]
+            assert spine[0] == min(top)
+
+
+def pin_select_all_equal():
+    """A row of equal logits: spine 0; candidates 0, 1, 2 (ties ascending) or the last
+    three indices, last first (descending)."""
+    x = np.full((2, 1000), 0.5, np.float32)
+    s0, c0 = oracle.draft_select(x, k=3, op_dtype=0, ties=0)
+    s1, c1 = oracle.draft_select(x, k=3, op_dtype=0, ties=1)
+    assert s0.tolist() == [0, 0] and s1.tolist() == [0, 0]
+    assert c0.tolist() == [[0, 1, 2]] * 2 and c1.tolist() == [[999, 998, 997]] * 2
+
+
+def pin_select_tie_conventions_differ():
+    """The maximum at indices 3 and 7: the spine is 3 under either tie convention,
+    while the first candidate is 3 (ascending) or 7 (descending); the spine token is
+    duplicated among the candidates."""
+    x = np.array([[0.1, 0.2, 0.0, 0.9, 0.5, 0.9 - 0.4, 0.3, 0.9, 0.7]], np.float32)
+    s0, c0 = oracle.draft_select(x, k=3, op_dtype=0, ties=0)
+    s1, c1 = oracle.draft_select(x, k=3, op_dtype=0, ties=1)
+    assert s0[0] == 3 and s1[0] == 3
+    assert c0[0].tolist() == [3, 7, 8] and c1[0].tolist() == [7, 3, 8]
+
+
+def pin_select_bf16_equals_decoded_f32():
+    """bf16 bit patterns give the same selection as their exact fp32 values."""
+    rng = np.random.default_rng(94)
+    bits = ops.to_bf16_bits((rng.standard_normal((8, 777)) * 3).astype(np.float32))
+    f = ops.bf16_bits_to_f32(bits)
+    for ties in (0, 1):
+        a = oracle.draft_select(bits, k=4, op_dtype=1, ties=ties)
+        b = oracle.draft_select(f, k=4, op_dtype=0, ties=ties)
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]

@@ -54,6 +54,13 @@ MUTATIONS = {
                              "const long vb = t < nc ? ((c0 + t) * h_kv + hk) * d : ((long)rw[path[t - nc > 0 ? t - nc - 1 : 0]] * h_kv + hk) * d;"),
     "attn_excludes_self": ("for (long t = 0; t < nc + len; ++t) {\n                    const void* kk",
                            "for (long t = 0; t < nc + len - (len > 1); ++t) {\n                    const void* kk"),
+    "select_tie_reversed": ("return ties == 0 ? ia < ib : ia > ib;", "return ties == 0 ? ia > ib : ia < ib;"),
+    "select_nan_lowest": ("if (isnan(a)) return !isnan(b);", "if (isnan(a)) return 0;"),
+    "select_spine_last_maximum": ("if (sel_greater(ld_op(logits, base + i, op_dtype), ld_op(logits, base + best, op_dtype))) best = i;",
+                                  "if (!sel_greater(ld_op(logits, base + best, op_dtype), ld_op(logits, base + i, op_dtype))) best = i;"),
+    "select_repeats_candidates": ("                if (taken) continue;\n", ""),
+    "select_spine_skips_index_1": ("for (int i = 1; i < vocab; ++i)\n            if (sel_greater(",
+                                   "for (int i = 2; i < vocab; ++i)\n            if (sel_greater("),
 }
 
 
