@@ -20,6 +20,7 @@ the same workload (all host cores, and one thread).
    publishes the history and replays the path itself; wy policy only)
   python bench.py --copy-probe     # plain 1 GiB device copy (HBM counter calibration)
   python bench.py --attention      # tree attention over a 131,072-token context (separate line)
+  python bench.py --select         # fused draft selection over 248,320-logit rows (separate line)
 
 The roofline's `traffic` (measured HBM bytes per verify call) is reported from
 profiles/traffic.json only while the verify kernel's sources hash to the value the
@@ -46,6 +47,7 @@ VERIFY_SOURCES = {
     "wy": ["verify_wy.hip", "device_common.h", "internal.h", "launch.h"],
     "paths": ["verify_scan.hip", "device_common.h", "internal.h", "launch.h"],
     "attention": ["attention.hip", "device_common.h", "internal.h", "launch.h"],
+    "select": ["select.hip", "select.h", "device_common.h"],
 }
 ATTN_CONFIG = "paper28_ctx131072"
 
@@ -201,6 +203,118 @@ def attention_bench(args):
     print(json.dumps(out), flush=True)
 
 
+SEL_VOCAB = 248320
+SEL_ROTATE_BYTES = 508e6  # logits cycled per replay: twice the 256 MB Infinity Cache
+
+
+def select_bench(args):
+    """Fused draft selection (lumo_draft_select): one call per drafting depth ranks one
+    full-vocabulary logits row per request (k = 3 candidates plus the spine token).
+    HBM-bound: every logit is read once. Calls are captured in a graph, one call per
+    logits buffer, and the graph is replayed, so the time is the device's (Python's
+    launch cost excluded) and, with about 508 MB of logits cycled, the reads come from
+    HBM rather than the Infinity Cache; `resident` repeats one buffer instead. Two batch
+    sizes: 8 rows (the batched workload's requests; a few microseconds, so launch
+    latency weighs in) and 64 rows."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2609_23900_amd as L
+    from lumo_synth import operands as ops
+
+    rng = np.random.default_rng(3)
+    k, ties = 3, 1
+    res = {}
+    host8 = None
+    for rows, dt, name in ((8, ops.F32, "rows8_f32"), (64, ops.BF16, "rows64_bf16")):
+        esz = 2 if dt == ops.BF16 else 4
+        nbuf = max(2, int(SEL_ROTATE_BYTES // (rows * SEL_VOCAB * esz)))
+        x = (rng.standard_normal((rows, SEL_VOCAB)) * 3).astype(np.float32)
+        if dt == ops.BF16:
+            t0 = torch.from_numpy(ops.to_bf16_bits(x).view(np.int16)).cuda().view(torch.bfloat16)
+        else:
+            t0 = torch.from_numpy(x).cuda()
+            host8 = x
+        bufs = [t0] + [t0[:, torch.randperm(SEL_VOCAB, device="cuda")].contiguous() for _ in range(nbuf - 1)]
+        n_split = L.lumo_draft_select_splits(rows, SEL_VOCAB, dt)
+        ws = torch.zeros(max(16, L.lumo_draft_select_workspace_bytes(rows, k, n_split)), dtype=torch.uint8,
+                         device="cuda")
+        spine = torch.zeros(rows, dtype=torch.int32, device="cuda")
+        cand = torch.zeros((rows, k), dtype=torch.int32, device="cuda")
+        out = {}
+        for mode in ("rotating", "resident"):
+            seq = bufs if mode == "rotating" else [t0] * len(bufs)
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):  # eager warm-up on the capture's stream
+                for b in seq:
+                    L.lumo_draft_select(b, k, ties, spine, cand, n_split, ws)
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for b in seq:
+                    L.lumo_draft_select(b, k, ties, spine, cand, n_split, ws)
+            stream = torch.cuda.current_stream()
+            reps = max(1, -(-args.steps // len(seq)))
+            for _ in range(max(1, args.warmup // len(seq))):
+                g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            out[mode] = e0.elapsed_time(e1) / (reps * len(seq))
+            out[mode + "_calls"] = reps * len(seq)
+            del g
+        want = oracle.draft_select(x if dt == ops.F32 else ops.to_bf16_bits(x), k=k, op_dtype=dt, ties=ties)
+        L.lumo_draft_select(t0, k, ties, spine, cand, n_split, ws)
+        assert np.array_equal(spine.cpu().numpy(), want[0]) and np.array_equal(cand.cpu().numpy(), want[1])
+        ms = out["rotating"]
+        nbytes = rows * SEL_VOCAB * esz + rows * (k + 1) * 4
+        ach = nbytes / (ms * 1e-3) / 1e9
+        res[name] = {"rows": rows, "dtype": "bf16" if dt == ops.BF16 else "f32", "n_split": n_split,
+                     "us_per_call": round(ms * 1e3, 3), "rows_per_s": round(rows / (ms * 1e-3), 1),
+                     "alg_bytes": nbytes, "achieved_GBps": round(ach, 1), "frac": round(ach / PEAK_HBM_GBS, 4),
+                     "calls_timed": out["rotating_calls"], "buffers_cycled": len(bufs),
+                     "resident_us_per_call": round(out["resident"] * 1e3, 3)}
+        del bufs, t0
+    main = res["rows8_f32"]
+    out = {"metric": "draft selection logits rows/sec + % of HBM roofline, 1 MI355X",
+           "value": main["rows_per_s"], "unit": "logits rows/s", "n_gpus": 1, "steps": main["calls_timed"],
+           "warmup": args.warmup, "ms_per_step": round(main["us_per_call"] / 1e3, 6),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic (N(0, 9) logits)",
+           "config": {"workload": f"draft selection: 8 rows x {SEL_VOCAB:,} float32 logits, argmax + ordered "
+                                  "top-3 (ties: higher index first), graph-replayed, 508 MB of logits cycled",
+                      "n_split": main["n_split"]},
+           "roofline": {"bound": "hbm", "achieved": main["achieved_GBps"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": main["frac"], "traffic": None,
+                        "kernel": "selection call (part kernel + merge kernel)",
+                        "per_launch": f"{main['alg_bytes'] / 1e6:.2f} MB algorithmic (every logit once)"},
+           "batches": res}
+    tr = recorded_traffic("select", "rows8_f32", "n/a")
+    if tr is not None:
+        out["roofline"]["traffic"] = {"fetch_bytes": tr["fetch_bytes"], "write_bytes": tr["write_bytes"],
+                                      "total_bytes": tr["fetch_bytes"] + tr["write_bytes"],
+                                      "unit": "B per selection call", "source": "profiles/traffic.json"}
+    if not args.no_cpu:
+        import time
+        oracle.draft_select(host8[:1], k=k, op_dtype=ops.F32, ties=ties)
+        reps, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < min(args.cpu_budget, 5.0) or reps == 0:
+            oracle.draft_select(host8, k=k, op_dtype=ops.F32, ties=ties, n_threads=1)
+            reps += 1
+        dt_s = (time.perf_counter() - t0) / reps
+        out["cpu_baseline"] = {"value": round(8 / dt_s, 1), "unit": "logits rows/s", "cores": 1, "kind": "oracle",
+                               "sample": f"the same 8 rows, {reps} repetitions, one thread",
+                               "host": host_cpu()}
+    print(json.dumps(out), flush=True)
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -297,6 +411,7 @@ def main():
                          "inputs; wy policy): g and beta are then read as raw inputs")
     ap.add_argument("--copy-probe", action="store_true", help="only run the counter-calibration copy")
     ap.add_argument("--attention", action="store_true", help="only run the tree-attention benchmark")
+    ap.add_argument("--select", action="store_true", help="only run the draft-selection benchmark")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-copy", action="store_true", help="skip the device-copy reference rate")
@@ -308,6 +423,9 @@ def main():
 
     if args.copy_probe:
         copy_probe()
+        return
+    if args.select:
+        select_bench(args)
         return
     if args.attention:
         attention_bench(args)

@@ -9,7 +9,8 @@
  *   lumo_tree_gdn_verify   device: every node's recurrent output from its ancestry
  *   lumo_gdn_commit        device: derive the accepted path, replay it into the
  *                          native state, publish the convolution history
- * plus lumo_tree_attention (the attention layers' tree verification), a
+ * plus lumo_tree_attention (the attention layers' tree verification),
+ * lumo_draft_select (the drafter's fused argmax / top-k selection), a
  * captured-graph form of the commit; lumo_tree_gdn_verify_pending and
  * lumo_tree_conv_gather_pending, which fold the publication of one iteration (state
  * replay, conv history) into the verification and convolution of the next; and forms
@@ -396,6 +397,38 @@ lumo_status lumo_tree_attention(const lumo_attn_dims* dims, const lumo_tree_desc
                                 const void* k_tree, const void* v_tree, void* o, float* lse,
                                 int32_t n_split, void* workspace, size_t workspace_bytes,
                                 void* stream);
+
+/*
+ * Fused draft selection (Sec. V-D): from one full-vocabulary logits row per drafting
+ * position, the principal (spine) token and k ordered sibling candidates in one pass.
+ * The two reference operations break ties differently, and both are reproduced:
+ *   spine[r]       the lowest index among the maximal logits of row r (argmax)
+ *   cand[r][0..k)  the k indices ranked first: logit descending; among equal logits
+ *                  index ascending (ties = 0) or descending (ties = 1) (top-k). The
+ *                  spine token may also appear among the candidates.
+ * A NaN logit (any payload) ranks above every number, NaNs equal among themselves;
+ * -0 equals +0. The result is exact (an ordering of the stored values), independent of
+ * n_split.
+ *   logits      device, row r at element r * ld, `vocab` logits each; float32
+ *               (dtype LUMO_F32) or bfloat16 bit patterns (LUMO_BF16); 16-byte aligned.
+ *               Elements between rows (ld > vocab) are never used.
+ *   rows >= 0, vocab >= 1, ld >= vocab, 1 <= k <= min(8, vocab), ties 0 or 1
+ *   spine       device int32 [rows];  cand  device int32 [rows][k]
+ *   n_split     parts each row is cut into (1..4096); lumo_draft_select_splits
+ *               suggests one for the row count and vocabulary. With n_split > 1 the
+ *               parts are reduced separately and merged by a second kernel.
+ *   workspace   device, >= lumo_draft_select_workspace_bytes(rows, k, n_split)
+ *               bytes, 16-byte aligned (0 and NULL allowed when n_split = 1). No
+ *               initial contents are needed; calls that share a workspace must not
+ *               overlap in time.
+ * LUMO_EUNSUPPORTED for k > 8.
+ */
+size_t lumo_draft_select_workspace_bytes(int32_t rows, int32_t k, int32_t n_split);
+int32_t lumo_draft_select_splits(int32_t rows, int32_t vocab, int32_t dtype);
+lumo_status lumo_draft_select(int32_t rows, int32_t vocab, int64_t ld, int32_t dtype, int32_t k,
+                              int32_t ties, const void* logits, int32_t* spine, int32_t* cand,
+                              int32_t n_split, void* workspace, size_t workspace_bytes,
+                              void* stream);
 
 typedef struct lumo_commit_graph lumo_commit_graph;
 

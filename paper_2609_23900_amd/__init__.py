@@ -6,7 +6,8 @@ The functions keep the names of the C ABI (include/lumo_tree.h):
   lumo_tree_plan, lumo_tree_gdn_workspace_bytes, lumo_tree_conv_gather,
   lumo_tree_conv_gather_pending, lumo_tree_gdn_verify, lumo_tree_gdn_verify_prep, lumo_tree_gdn_verify_pending, lumo_gdn_commit,
   lumo_gdn_commit_prep, lumo_tree_attention, lumo_tree_attention_workspace_bytes,
-  lumo_tree_attention_splits, lumo_gdn_commit_graph_create,
+  lumo_tree_attention_splits, lumo_draft_select, lumo_draft_select_workspace_bytes,
+  lumo_draft_select_splits, lumo_gdn_commit_graph_create,
   lumo_gdn_commit_graph_launch, lumo_gdn_commit_graph_destroy, lumo_last_error,
   lumo_version.
 Device arguments are torch tensors on the GPU (or None where the ABI allows NULL);
@@ -108,6 +109,11 @@ def _load():
     L.lumo_tree_attention_splits.argtypes = [PA, ctypes.POINTER(lumo_plan), I32]
     L.lumo_tree_attention_splits.restype = I32
     L.lumo_tree_attention.argtypes = [PA, PT, P, I32, ctypes.c_float, P, P, P, P, P, P, P, I32, P, SZ, P]
+    L.lumo_draft_select_workspace_bytes.argtypes = [I32, I32, I32]
+    L.lumo_draft_select_workspace_bytes.restype = SZ
+    L.lumo_draft_select_splits.argtypes = [I32, I32, I32]
+    L.lumo_draft_select_splits.restype = I32
+    L.lumo_draft_select.argtypes = [I32, I32, I64, I32, I32, I32, P, P, P, I32, P, SZ, P]
     L.lumo_tree_gdn_verify_prep.argtypes = [PD, PT, PP, P, P, P, P, P, P, P, P]
     L.lumo_tree_gdn_verify_pending.argtypes = [PD, PT, PP, P, P, P, P, P, P, P, PT, I32, P, P, P, P, P, P,
                                                P]
@@ -122,7 +128,7 @@ def _load():
     L.lumo_version.restype = ctypes.c_char_p
     for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_conv_gather_pending", "lumo_tree_gdn_verify",
               "lumo_tree_gdn_verify_prep", "lumo_tree_gdn_verify_pending", "lumo_gdn_commit",
-              "lumo_gdn_commit_prep", "lumo_tree_attention", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
+              "lumo_gdn_commit_prep", "lumo_tree_attention", "lumo_draft_select", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -290,6 +296,34 @@ def lumo_tree_attention(d, desc: TreeDesc, ctx_off, max_ctx, scale, q, k_ctx, v_
                                     int(max_ctx), float(scale), _dptr(q), _dptr(k_ctx), _dptr(v_ctx),
                                     _dptr(k_tree), _dptr(v_tree), _dptr(o), _dptr(lse), int(n_split),
                                     _dptr(workspace), ws_bytes, _stream(stream)))
+
+
+def _logits_dtype(t):
+    if t.dtype == torch.float32:
+        return LUMO_F32
+    if t.dtype == torch.bfloat16:
+        return LUMO_BF16
+    raise TypeError("logits must be float32 or bfloat16")
+
+
+def lumo_draft_select_workspace_bytes(rows, k, n_split) -> int:
+    return int(_lib.lumo_draft_select_workspace_bytes(int(rows), int(k), int(n_split)))
+
+
+def lumo_draft_select_splits(rows, vocab, dtype) -> int:
+    return int(_lib.lumo_draft_select_splits(int(rows), int(vocab), int(dtype)))
+
+
+def lumo_draft_select(logits, k, ties, spine, cand, n_split, workspace, stream=None, vocab=None):
+    """logits: contiguous [rows][ld] float32 or bfloat16 tensor; the first `vocab`
+    (default ld) entries of each row are ranked. spine int32 [rows], cand int32 [rows][k]."""
+    if logits.dim() != 2:
+        raise ValueError("logits must be [rows][ld]")
+    rows, ld = logits.shape
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib.lumo_draft_select(int(rows), int(ld if vocab is None else vocab), int(ld), _logits_dtype(logits),
+                                  int(k), int(ties), _dptr(logits), _dptr(spine), _dptr(cand), int(n_split),
+                                  _dptr(workspace), ws_bytes, _stream(stream)))
 
 
 class CommitGraph:

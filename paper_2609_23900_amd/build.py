@@ -19,7 +19,7 @@ LIB = os.path.join(PKG, "liblumo_tree.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
 SOURCES = ["capi.hip", "plan.cpp", "verify_scan.hip", "verify_wy.hip", "commit.hip", "conv.hip",
-           "attention.hip"]
+           "attention.hip", "select.hip"]
 ARCH = "gfx950"
 
 

@@ -8,6 +8,7 @@
 
 #include "internal.h"
 #include "launch.h"
+#include "select.h"
 
 #include <algorithm>
 
@@ -431,6 +432,58 @@ extern "C" lumo_status lumo_tree_attention(const lumo_attn_dims* dims, const lum
     if (workspace_bytes < need) return fail(LUMO_ESPACE, "%s: workspace needs %zu bytes, got %zu", fn, need, workspace_bytes);
     AttnArgs a{ctx_off, max_ctx, n_split, scale, q, k_ctx, v_ctx, k_tree, v_tree, o, lse, static_cast<float*>(workspace)};
     hipError_t e = launch_attention(*dims, *desc, a, static_cast<hipStream_t>(stream));
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not available in this build", fn);
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
+extern "C" size_t lumo_draft_select_workspace_bytes(int32_t rows, int32_t k, int32_t n_split) {
+    if (rows < 0 || k < 1 || n_split <= 1) return 0;
+    return (size_t)rows * n_split * (k + 1) * sizeof(uint64_t);
+}
+
+extern "C" int32_t lumo_draft_select_splits(int32_t rows, int32_t vocab, int32_t dtype) {
+    // Parts of at least 2048 16-byte vectors (one batch of eight per thread), and at
+    // most 1024 blocks in all.
+    if (rows < 1 || vocab < 1) return 1;
+    const long per_vec = dtype == LUMO_BF16 ? 8 : 4;
+    const long nvec = (long)vocab / per_vec;
+    const long want = nvec / 2048;
+    const long cap = std::max<long>(1, 1024 / rows);
+    return (int32_t)std::max<long>(1, std::min<long>({want, cap, 4096}));
+}
+
+extern "C" lumo_status lumo_draft_select(int32_t rows, int32_t vocab, int64_t ld, int32_t dtype, int32_t k,
+                                         int32_t ties, const void* logits, int32_t* spine, int32_t* cand,
+                                         int32_t n_split, void* workspace, size_t workspace_bytes, void* stream) {
+    static const char* fn = "lumo_draft_select";
+    clear_error();
+    if (rows < 0) return fail(LUMO_EINVAL, "%s: rows %d", fn, rows);
+    if (vocab < 1) return fail(LUMO_EINVAL, "%s: vocab %d", fn, vocab);
+    if (ld < vocab) return fail(LUMO_EINVAL, "%s: ld %lld < vocab %d", fn, (long long)ld, vocab);
+    if (dtype != LUMO_F32 && dtype != LUMO_BF16) return fail(LUMO_EUNSUPPORTED, "%s: dtype %d", fn, dtype);
+    if (ties != 0 && ties != 1) return fail(LUMO_EINVAL, "%s: ties %d (0 or 1)", fn, ties);
+    if (k < 1 || k > vocab) return fail(LUMO_EINVAL, "%s: k %d (1..vocab %d)", fn, k, vocab);
+    if (k > 8) return fail(LUMO_EUNSUPPORTED, "%s: k %d (at most 8)", fn, k);
+    if (n_split < 1 || n_split > 4096) return fail(LUMO_EINVAL, "%s: n_split %d (1..4096)", fn, n_split);
+    // element offsets and the grid stay within their index types
+    if ((long long)rows * n_split > 0x7fffffffLL) return fail(LUMO_EINVAL, "%s: rows x n_split too large", fn);
+    if (rows > 0 && (ld > (1LL << 40) || (long long)(rows - 1) * ld + vocab > (1LL << 40)))
+        return fail(LUMO_EINVAL, "%s: logits span too large", fn);
+    if (rows == 0) return LUMO_OK;
+    LUMO_TRY(check_ptr(logits, fn, "logits"));
+    LUMO_TRY(check_ptr(spine, fn, "spine"));
+    LUMO_TRY(check_ptr(cand, fn, "cand"));
+    uint64_t* parts = nullptr;
+    if (n_split > 1) {
+        const size_t need = lumo_draft_select_workspace_bytes(rows, k, n_split);
+        LUMO_TRY(check_ptr(workspace, fn, "workspace"));
+        if (workspace_bytes < need)
+            return fail(LUMO_ESPACE, "%s: workspace needs %zu bytes, got %zu", fn, need, workspace_bytes);
+        parts = static_cast<uint64_t*>(workspace);
+    }
+    SelectArgs a{logits, rows, vocab, (long)ld, dtype, k, ties, n_split, spine, cand, parts};
+    hipError_t e = launch_select(a, static_cast<hipStream_t>(stream));
     if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not available in this build", fn);
     if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return LUMO_OK;

@@ -315,3 +315,42 @@ def test_attention_empty_batch_is_a_no_op():
                                   np.zeros(0, np.int32), 0)
     desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
     assert _attn(L.attn_dims(0, 4, 2), desc, ptrs=False) == L.LUMO_OK
+
+
+def _select(rows=2, vocab=100, ld=None, dtype=0, k=3, ties=0, logits=FAKE, spine=FAKE, cand=FAKE,
+            n_split=2, ws=FAKE, ws_bytes=None):
+    P = ctypes.c_void_p
+    if ws_bytes is None:
+        ws_bytes = L.lumo_draft_select_workspace_bytes(rows, k, n_split)
+    return L._lib.lumo_draft_select(rows, vocab, vocab if ld is None else ld, dtype, k, ties,
+                                    P(logits) if logits else None, P(spine) if spine else None,
+                                    P(cand) if cand else None, n_split, P(ws) if ws else None, ws_bytes, None)
+
+
+def test_draft_select_rejects_bad_arguments():
+    assert _select(rows=-1) == L.LUMO_EINVAL
+    assert _select(vocab=0) == L.LUMO_EINVAL
+    assert _select(ld=99) == L.LUMO_EINVAL
+    assert _select(dtype=2) == L.LUMO_EUNSUPPORTED
+    assert _select(ties=2) == L.LUMO_EINVAL
+    assert _select(k=0) == L.LUMO_EINVAL
+    assert _select(vocab=2, k=3) == L.LUMO_EINVAL
+    assert _select(k=9) == L.LUMO_EUNSUPPORTED
+    assert _select(n_split=0) == L.LUMO_EINVAL
+    assert _select(n_split=4097) == L.LUMO_EINVAL
+    assert _select(logits=None) == L.LUMO_EINVAL
+    assert _select(logits=FAKE + 4) == L.LUMO_EINVAL
+    assert _select(spine=None) == L.LUMO_EINVAL
+    assert _select(cand=FAKE + 8) == L.LUMO_EINVAL
+    assert _select(ws=None) == L.LUMO_EINVAL
+    need = L.lumo_draft_select_workspace_bytes(2, 3, 2)
+    assert need == 2 * 2 * 4 * 8
+    assert _select(ws_bytes=need - 8) == L.LUMO_ESPACE
+    assert "workspace" in L.lumo_last_error()
+
+
+def test_draft_select_empty_and_single_part_need_no_workspace():
+    assert _select(rows=0, logits=None, spine=None, cand=None, ws=None) == L.LUMO_OK
+    assert L.lumo_draft_select_workspace_bytes(8, 3, 1) == 0
+    assert L.lumo_draft_select_splits(8, 248320, 0) * 8 <= 1024
+    assert L.lumo_draft_select_splits(1, 10, 1) == 1
