@@ -415,6 +415,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-copy", action="store_true", help="skip the device-copy reference rate")
+    ap.add_argument("--graph", action="store_true",
+                    help="also replay the step from a captured graph (ten steps per graph): the device "
+                         "time without Python's launch cost, for the small configs")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the step shards "
@@ -454,22 +457,22 @@ def main():
     st = GdnTreeStep.from_workload(wl, policy=policy, keep_state0=False, prep=prep)
     stream = torch.cuda.current_stream()
 
-    def step(ev=None):
+    def step(ev=None, s=stream):  # s=None: the current stream (a graph's capture stream)
         if ev is not None:
             ev[0].record(stream)
         if deferred:
-            st.conv_pending(st, stream)  # publishes the previous step's history, then the conv
+            st.conv_pending(st, s)  # publishes the previous step's history, then the conv
         else:
-            st.conv(stream)
+            st.conv(s)
         if ev is not None:
             ev[1].record(stream)
         if deferred:
-            st.verify_pending(st, stream)  # publishes the previous step's path, then verifies
+            st.verify_pending(st, s)  # publishes the previous step's path, then verifies
         else:
-            st.verify(stream)
+            st.verify(s)
         if ev is not None:
             ev[2].record(stream)
-        st.commit(stream, defer=deferred, with_conv=not deferred)
+        st.commit(s, defer=deferred, with_conv=not deferred)
         if ev is not None:
             ev[3].record(stream)
 
@@ -494,6 +497,31 @@ def main():
     step_dist = pct([e[0].elapsed_time(e[3]) for e in evs])
     ver_dist = pct([e[1].elapsed_time(e[2]) for e in evs])
     log(f"[bench] step {ms_step:.3f} ms (conv {conv_ms:.3f}, verify {ver_ms:.3f}, commit {com_ms:.3f})")
+    graph_ms = None
+    if args.graph:
+        per = 10
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step(s=None)  # one eager step on the capture's stream
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(per):
+                step(s=None)
+        g.replay()
+        torch.cuda.synchronize()
+        reps = max(1, args.steps // per)
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(reps):
+            g.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        graph_ms = g0.elapsed_time(g1) / (reps * per)
+        log(f"[bench] graph-replayed step {graph_ms:.4f} ms")
+        del g
     assert torch.isfinite(st.state).all().item(), "non-finite state"
 
     ab = alg_bytes_flops(wl)
@@ -526,6 +554,8 @@ def main():
         "step_ms_p10_p50_p90": step_dist,
         "verify_ms_p10_p50_p90": ver_dist,
     }
+    if graph_ms is not None:
+        kernels["graph_step_ms"] = round(graph_ms, 4)
     if not deferred:
         kernels["commit_hbm_frac"] = round(ab["commit_bytes"] / (com_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
     out = {

@@ -416,7 +416,8 @@ lumo_status lumo_tree_attention(const lumo_attn_dims* dims, const lumo_tree_desc
  *   spine       device int32 [rows];  cand  device int32 [rows][k]
  *   n_split     parts each row is cut into (1..4096); lumo_draft_select_splits
  *               suggests one for the row count and vocabulary. With n_split > 1 the
- *               parts are reduced separately and merged by a second kernel.
+ *               parts are reduced separately (each by four wavefronts) and merged by a
+ *               second kernel.
  *   workspace   device, >= lumo_draft_select_workspace_bytes(rows, k, n_split)
  *               bytes, 16-byte aligned (0 and NULL allowed when n_split = 1). No
  *               initial contents are needed; calls that share a workspace must not

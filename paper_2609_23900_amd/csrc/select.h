@@ -7,8 +7,9 @@
 
 namespace lumo {
 
-// Fused draft selection: rows x n_split blocks; with n_split > 1 the parts go to
-// `parts` ([rows][n_split][k + 1] words) and a merge kernel writes the outputs.
+// Fused draft selection: rows x n_split blocks of four wavefronts; with n_split > 1 each
+// wavefront's words go to `parts` ([rows][n_split][4][k + 1] words) and a merge kernel
+// writes the outputs.
 struct SelectArgs {
     const void* logits;
     int32_t rows;

@@ -15,12 +15,14 @@
 // insertion: per batch the wave splits into G lane groups, takes each group's float
 // maximum, and the k-th largest of those G maxima is a value that at least k logits
 // seen by the wave reach; a logit strictly below it (float compare; NaN always passes,
-// -0 equals +0) has k logits ranked above it and is skipped. The block then selects its
-// k best words by k rounds of block-wide maximum over the threads' list heads (the
-// winning thread pops its head) and one more round for the spine word.
-// With one part per row that block writes the outputs. Otherwise each part's words go
-// to the workspace and a second kernel, one wavefront per row, merges them the same
-// way; the kernel boundary orders the two, so nothing needs clearing between calls.
+// -0 equals +0) has k logits ranked above it and is skipped. Each wavefront then selects
+// its k best words by k rounds of wave-wide maximum over the lanes' list heads (the
+// winning lane pops its head; words are unique) and one more round for the spine word,
+// and, when the block has the whole row, wave 0 does the same over the block's waves and
+// writes the outputs. The cross-lane maxima use DPP moves and lane-row swaps, no LDS.
+// When a row has several parts, each wavefront's words go to the workspace and a second
+// kernel, one wavefront per row, merges them the same way; the kernel boundary orders
+// the two, so nothing needs clearing between calls.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -53,13 +55,43 @@ __device__ __forceinline__ void topk_insert(uint64_t (&t)[K], uint64_t x) {
     }
 }
 
+// Cross-lane moves without LDS: DPP within 16-lane rows, then the row-pair and
+// half-wave swaps. DPP controls: quad permutations [1,0,3,2] and [2,3,0,1], mirror
+// within 8-lane halves, mirror within the row.
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppRowMirror = 0x140;
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, CTRL, 0xF, 0xF, false);
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t max_dpp(uint64_t x) {
+    const uint64_t o = ((uint64_t)dpp<CTRL>((uint32_t)(x >> 32)) << 32) | dpp<CTRL>((uint32_t)x);
+    return x > o ? x : o;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float fmax_dpp(float x) {
+    return fmaxf(x, __uint_as_float(dpp<CTRL>(__float_as_uint(x))));
+}
+
+// Largest word of the wavefront, in every lane.
 __device__ __forceinline__ uint64_t wave_max(uint64_t x) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const uint64_t o = __shfl_xor(x, off, 64);
-        x = x > o ? x : o;
-    }
-    return x;
+    x = max_dpp<kDppXor1>(x);
+    x = max_dpp<kDppXor2>(x);
+    x = max_dpp<kDppHalfMirror>(x);
+    x = max_dpp<kDppRowMirror>(x);  // uniform within each 16-lane row
+    const uint32_t lo = (uint32_t)x, hi = (uint32_t)(x >> 32);
+    const auto l16 = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+    const auto h16 = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    const uint64_t a = ((uint64_t)h16[0] << 32) | l16[0], b = ((uint64_t)h16[1] << 32) | l16[1];
+    x = a > b ? a : b;  // rows 0-1 and rows 2-3
+    const uint32_t lo2 = (uint32_t)x, hi2 = (uint32_t)(x >> 32);
+    const auto l32 = __builtin_amdgcn_permlane32_swap(lo2, lo2, false, false);
+    const auto h32 = __builtin_amdgcn_permlane32_swap(hi2, hi2, false, false);
+    const uint64_t c = ((uint64_t)h32[0] << 32) | l32[0], d = ((uint64_t)h32[1] << 32) | l32[1];
+    return c > d ? c : d;
 }
 
 // Pop the head of t if it is the round's winner (words are unique, so one thread does).
@@ -72,26 +104,41 @@ __device__ __forceinline__ void pop_if(uint64_t (&t)[K], uint64_t win) {
     }
 }
 
-// The block's k best words (out, descending) and its spine word, valid in every thread.
+// The wavefront's k best words (out, descending; the lists are consumed) and its
+// largest spine word, in every lane.
+template <int K>
+__device__ __forceinline__ void wave_select(uint64_t (&t)[K], uint64_t sp, uint64_t (&out)[K], uint64_t& spo) {
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        out[j] = wave_max(t[0]);
+        pop_if<K>(t, out[j]);
+    }
+    spo = wave_max(sp);
+}
+
+// The block's k best words and spine word, valid in the lanes of wave 0.
 template <int K>
 __device__ __forceinline__ void block_select(uint64_t (&t)[K], uint64_t sp, uint64_t (&out)[K], uint64_t& spo,
-                                             uint64_t (*red)[kWaves]) {
+                                             uint64_t (*red)[K + 1]) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint64_t w[K], wsp;
+    wave_select<K>(t, sp, w, wsp);
+    if (lane == 0) {
 #pragma unroll
-    for (int j = 0; j <= K; ++j) {
-        const uint64_t m = wave_max(j < K ? t[0] : sp);
-        if (lane == 0) red[j & 1][wave] = m;
-        __syncthreads();  // red[j & 1] is rewritten two rounds later, after this barrier's successor
-        uint64_t b = red[j & 1][0];
-#pragma unroll
-        for (int w = 1; w < kWaves; ++w) b = b > red[j & 1][w] ? b : red[j & 1][w];
-        if (j < K) {
-            out[j] = b;
-            pop_if<K>(t, b);
-        } else {
-            spo = b;
-        }
+        for (int j = 0; j < K; ++j) red[wave][j] = w[j];
+        red[wave][K] = wsp;
     }
+    __syncthreads();
+    if (wave != 0) return;
+    // lane l < kWaves k holds word l % k of wave l / k; the rest hold nothing
+    uint64_t c[1] = {lane < kWaves * K ? red[lane / K][lane % K] : 0};
+    const uint64_t cs = lane < kWaves ? red[lane][K] : 0;
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        out[j] = wave_max(c[0]);
+        pop_if<1>(c, out[j]);
+    }
+    spo = wave_max(cs);
 }
 
 template <int K>
@@ -153,7 +200,7 @@ __global__ __launch_bounds__(kThreads) void select_part_kernel(const void* __res
     constexpr uint32_t tmask = TIES_HIGH ? 0u : 0xffffffffu;
     constexpr int G = K <= 4 ? 4 : 8;  // lane groups of the batch threshold
     constexpr int GL = 64 / G;
-    __shared__ uint64_t red[2][kWaves];
+    __shared__ uint64_t red[kWaves][K + 1];
 
     const long r = blockIdx.x / n_split;
     const int s = blockIdx.x % n_split;
@@ -185,14 +232,16 @@ __global__ __launch_bounds__(kThreads) void select_part_kernel(const void* __res
         for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
             for (int i = 0; i < N; ++i) m = fmaxf(m, __uint_as_float(V::bits(w[u], i)));
-#pragma unroll
-        for (int off = 1; off < GL; off <<= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+        m = fmax_dpp<kDppXor1>(m);
+        m = fmax_dpp<kDppXor2>(m);
+        m = fmax_dpp<kDppHalfMirror>(m);  // uniform within 8-lane groups
+        if (G == 4) m = fmax_dpp<kDppRowMirror>(m);  // within 16-lane groups
         float top[K];
 #pragma unroll
         for (int j = 0; j < K; ++j) top[j] = -__builtin_inff();
 #pragma unroll
         for (int q = 0; q < G; ++q) {
-            float x = __shfl(m, q * GL, 64);
+            float x = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(m), q * GL));
 #pragma unroll
             for (int j = 0; j < K; ++j) {
                 const float hi = fmaxf(top[j], x);
@@ -219,21 +268,23 @@ __global__ __launch_bounds__(kThreads) void select_part_kernel(const void* __res
     }
 
     uint64_t best[K], bsp;
-    block_select<K>(t, sp, best, bsp, red);
-    if (threadIdx.x != 0) return;
-    if (n_split == 1) {
-        write_result<K>(best, bsp, tmask, r, spine, cand);
+    if (n_split == 1) {  // the block has the whole row
+        block_select<K>(t, sp, best, bsp, red);  // wave 0 holds the result
+        if (threadIdx.x == 0) write_result<K>(best, bsp, tmask, r, spine, cand);
         return;
     }
-    uint64_t* pp = parts + (long)blockIdx.x * (K + 1);
+    // each wavefront's words are one part of the row for the merge kernel
+    wave_select<K>(t, sp, best, bsp);
+    if ((threadIdx.x & 63) != 0) return;
+    uint64_t* pp = parts + ((long)blockIdx.x * kWaves + (threadIdx.x >> 6)) * (K + 1);
 #pragma unroll
     for (int j = 0; j < K; ++j) pp[j] = best[j];
     pp[K] = bsp;
 }
 
-// One wavefront per row: merge the row's n_split parts ([K words, spine word] each).
+// One wavefront per row: merge the row's n_parts parts ([K words, spine word] each).
 template <int K, bool TIES_HIGH>
-__global__ __launch_bounds__(64) void select_merge_kernel(int32_t n_split, const uint64_t* __restrict__ parts,
+__global__ __launch_bounds__(64) void select_merge_kernel(int32_t n_parts, const uint64_t* __restrict__ parts,
                                                           int32_t* __restrict__ spine, int32_t* __restrict__ cand) {
     constexpr uint32_t tmask = TIES_HIGH ? 0u : 0xffffffffu;
     const long r = blockIdx.x;
@@ -241,20 +292,15 @@ __global__ __launch_bounds__(64) void select_merge_kernel(int32_t n_split, const
 #pragma unroll
     for (int j = 0; j < K; ++j) t[j] = 0;
     uint64_t sp = 0;
-    const uint64_t* rp = parts + r * n_split * (K + 1);
-    for (int p = threadIdx.x; p < n_split; p += 64) {
+    const uint64_t* rp = parts + r * n_parts * (K + 1);
+    for (int p = threadIdx.x; p < n_parts; p += 64) {
         const uint64_t* pp = rp + (long)p * (K + 1);
 #pragma unroll
         for (int j = 0; j < K; ++j) topk_insert<K>(t, pp[j]);
         sp = sp > pp[K] ? sp : pp[K];
     }
     uint64_t best[K];
-#pragma unroll
-    for (int j = 0; j < K; ++j) {
-        best[j] = wave_max(t[0]);
-        pop_if<K>(t, best[j]);
-    }
-    sp = wave_max(sp);
+    wave_select<K>(t, sp, best, sp);
     if (threadIdx.x == 0) write_result<K>(best, sp, tmask, r, spine, cand);
 }
 
@@ -265,8 +311,8 @@ hipError_t launch_kt(const SelectArgs& a, hipStream_t s) {
                        a.cand, a.parts);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.n_split == 1) return e;
-    hipLaunchKernelGGL((select_merge_kernel<K, TH>), dim3((unsigned)a.rows), dim3(64), 0, s, a.n_split, a.parts,
-                       a.spine, a.cand);
+    hipLaunchKernelGGL((select_merge_kernel<K, TH>), dim3((unsigned)a.rows), dim3(64), 0, s, a.n_split * kWaves,
+                       a.parts, a.spine, a.cand);
     return hipGetLastError();
 }
 

@@ -344,7 +344,7 @@ def test_draft_select_rejects_bad_arguments():
     assert _select(cand=FAKE + 8) == L.LUMO_EINVAL
     assert _select(ws=None) == L.LUMO_EINVAL
     need = L.lumo_draft_select_workspace_bytes(2, 3, 2)
-    assert need == 2 * 2 * 4 * 8
+    assert need == 2 * 2 * 4 * 4 * 8
     assert _select(ws_bytes=need - 8) == L.LUMO_ESPACE
     assert "workspace" in L.lumo_last_error()
 
@@ -352,5 +352,6 @@ def test_draft_select_rejects_bad_arguments():
 def test_draft_select_empty_and_single_part_need_no_workspace():
     assert _select(rows=0, logits=None, spine=None, cand=None, ws=None) == L.LUMO_OK
     assert L.lumo_draft_select_workspace_bytes(8, 3, 1) == 0
-    assert L.lumo_draft_select_splits(8, 248320, 0) * 8 <= 1024
+    assert L.lumo_draft_select_splits(8, 248320, 0) == 30
+    assert L.lumo_draft_select_splits(64, 248320, 1) == 15
     assert L.lumo_draft_select_splits(1, 10, 1) == 1

@@ -106,7 +106,7 @@ def splits_for(L, rows, vocab, dtype):
 def test_select_cases_exact(lib):
     L = lib
     rng = np.random.default_rng(2609)
-    ws = torch.zeros(4 << 20, dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(8 << 20, dtype=torch.uint8, device="cuda")
     n_cases = n_runs = 0
     for dtype in (ops.F32, ops.BF16):
         for vocab in VOCABS:
