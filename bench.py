@@ -398,6 +398,58 @@ def cpu_baseline(wl, budget_s=12.0):
             "host": host_cpu()}
 
 
+def per_layer_graph_ms(args, st, stream):
+    """The step as the paper's per-layer structure runs it: for every layer its own conv
+    and verify calls (n_layers = 1), each layer with its own state bank
+    [req][1][h_v][d_k][d_v] and conv history [req][1][3][C], the per-node tensors sliced
+    by layer, and one path derivation shared by all layers; ten steps captured in one
+    graph and replayed. Returns ms per step."""
+    import torch
+
+    import paper_2609_23900_amd as L
+
+    d = st.dims
+    nl = d.n_layers
+    d1 = L.dims(d.n_req, 1, d.h_k, d.h_v, d.d_k, d.d_v, d.op_dtype)
+    states = [st.state[:, l:l + 1].contiguous() for l in range(nl)]
+    hists = [st.hist[:, l:l + 1].contiguous() for l in range(nl)]
+
+    def one_step():
+        for l in range(nl):
+            x, y, w = st.x[l], st.y[l], st.w[l]
+            L.lumo_tree_conv_gather_pending(d1, st.desc, st.channels, x, hists[l], w, None, st.act, y, st.desc,
+                                            st.max_path, st.path_out, st.path_len, x, None)
+            q, k, v, g, b = (st.t[key][l] for key in ("q", "k", "v", "g", "beta"))
+            L.lumo_tree_gdn_verify_pending(d1, st.desc, q, k, v, g, b, states[l], st.o[l], st.desc, st.max_path,
+                                           st.path_out, st.path_len, k, v, g, b, None, st.prep)
+        st.commit(None, defer=True, with_conv=False)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        one_step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    per = 10
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(per):
+            one_step()
+    g.replay()
+    torch.cuda.synchronize()
+    reps = max(1, args.steps // per)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / (reps * per)
+    log(f"[bench] per-layer graph-replayed step {ms:.4f} ms ({2 * nl + 1} launches per step)")
+    del g
+    return ms
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -415,6 +467,10 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-copy", action="store_true", help="skip the device-copy reference rate")
+    ap.add_argument("--per-layer", action="store_true",
+                    help="also time the step as one call per layer (conv and verify of each layer "
+                         "with its own state and history bank, one path derivation), all captured in "
+                         "one graph (wy policy, deferred commit)")
     ap.add_argument("--graph", action="store_true",
                     help="also replay the step from a captured graph (ten steps per graph): the device "
                          "time without Python's launch cost, for the small configs")
@@ -556,6 +612,12 @@ def main():
     }
     if graph_ms is not None:
         kernels["graph_step_ms"] = round(graph_ms, 4)
+    if args.per_layer:
+        if not deferred:
+            sys.exit("--per-layer needs the wy policy and the deferred commit")
+        pl_ms = per_layer_graph_ms(args, st, stream)
+        kernels["per_layer_graph_step_ms"] = round(pl_ms, 4)
+        kernels["per_layer_launches_per_step"] = 2 * wl.n_layers + 1
     if not deferred:
         kernels["commit_hbm_frac"] = round(ab["commit_bytes"] / (com_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
     out = {

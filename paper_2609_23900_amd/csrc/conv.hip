@@ -19,6 +19,7 @@ struct ConvParams {
     const int32_t* blob;
     int32_t o_req, o_row, o_conv_src;
     int32_t total_nodes, total_rows, n_layers, channels, n_cchunks, act;
+    int32_t run;  // nodes per block (1..kNodesPerBlock)
     const void* x;
     const void* hist;
     const float* w;
@@ -123,7 +124,8 @@ __global__ __launch_bounds__(256) void hist_pend_kernel(HistPend q, int n_layers
     }
 }
 
-// One block: one layer, 2048 channels (8 per thread), a run of kNodesPerBlock nodes.
+// One block: one layer, 2048 channels (8 per thread), a run of up to kNodesPerBlock
+// nodes (shorter runs when the grid would otherwise leave CUs idle).
 // The taps and bias of the thread's channels stay in registers across the run; the
 // window rows of consecutive nodes (parents, grandparents) are mostly L2 hits.
 constexpr int kNodesPerBlock = 32;
@@ -132,7 +134,7 @@ template <int OPT>
 __global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
     using T = typename Op<OPT>::T;
     int t = xcd_remap(blockIdx.x, gridDim.x);
-    const int ng = (p.total_nodes + kNodesPerBlock - 1) / kNodesPerBlock;
+    const int ng = (p.total_nodes + p.run - 1) / p.run;
     const int grp = t % ng;
     t /= ng;
     const int cc = t % p.n_cchunks;
@@ -154,8 +156,8 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
     float b0[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) b0[e] = p.bias ? p.bias[(long)l * p.channels + c + e] : 0.f;
-    const int n0 = grp * kNodesPerBlock;
-    const int nn = min(p.total_nodes, n0 + kNodesPerBlock) - n0;
+    const int n0 = grp * p.run;
+    const int nn = min(p.total_nodes, n0 + p.run) - n0;
     // node info of the run, one node per lane (lanes 0..31 of every wave), broadcast
     // per node with readlane so the window loads depend on nothing but registers
     const int li = (int)threadIdx.x & (kNodesPerBlock - 1);
@@ -440,7 +442,13 @@ hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.w = a.w;
     p.bias = a.bias;
     p.y = a.y;
-    const long blocks = (long)d.n_layers * n_cchunks * ((pl.total_nodes + kNodesPerBlock - 1) / kNodesPerBlock);
+    // runs of 32 nodes, halved (down to 4) while the grid has fewer than four blocks per
+    // CU: a block's node batches are loaded one after the other, so small grids (one
+    // layer of a batch) finish sooner with more, shorter runs
+    int run = kNodesPerBlock;
+    while (run > 4 && (long)d.n_layers * n_cchunks * ((pl.total_nodes + run - 1) / run) < 4 * 256) run /= 2;
+    p.run = run;
+    const long blocks = (long)d.n_layers * n_cchunks * ((pl.total_nodes + run - 1) / run);
     if (d.op_dtype == LUMO_BF16)
         hipLaunchKernelGGL(conv_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, s, p);
     else

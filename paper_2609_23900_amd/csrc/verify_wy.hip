@@ -730,9 +730,13 @@ hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.a_log = a.prep.a_log;
     p.dt_bias = a.prep.dt_bias;
     // one block per (request, layer, key head, pair of value heads): the pair's waves
-    // share the staged key and query rows and the Gram
+    // share the staged key and query rows and the Gram. Grids of fewer pair blocks than
+    // CUs (one layer of a batch, few requests) take one value head per block instead:
+    // twice the blocks, each with half the work on its critical path, at the cost of a
+    // Gram per head.
     const bool qkn = (a.prep.flags & LUMO_PREP_QK_NORM) != 0;
-    if (p.group % 2 == 0)
+    const long pair_blocks = (long)d.n_req * d.n_layers * d.h_k * (p.group / 2);
+    if (p.group % 2 == 0 && pair_blocks >= 256)
         return qkn ? launch_wy_kernel<D, 2, PEND, true>(d, p, a, s, pp) : launch_wy_kernel<D, 2, PEND, false>(d, p, a, s, pp);
     return qkn ? launch_wy_kernel<D, 1, PEND, true>(d, p, a, s, pp) : launch_wy_kernel<D, 1, PEND, false>(d, p, a, s, pp);
 }
