@@ -344,9 +344,13 @@ def alg_bytes_flops(wl):
     # layer), four fp32 taps per (layer, channel)
     conv_bytes = (wl.total_nodes * wl.n_layers * wl.channels * opb * 2
                   + wl.n_req * wl.n_layers * 3 * wl.channels * opb + wl.n_layers * wl.channels * 16)
+    # conv fused into the verification (deferred): the verify bytes (its q, k, v read as
+    # x channels), the publication, the history read and written, the taps; no y
+    fused_bytes = (v_bytes + pub_bytes + wl.n_req * wl.n_layers * 3 * wl.channels * opb
+                   + active * wl.n_layers * 3 * wl.channels * opb + wl.n_layers * wl.channels * 16)
     return dict(verify_bytes=v_bytes, verify_flops=v_flops, commit_bytes=c_bytes, pub_bytes=pub_bytes,
                 commit_flops=c_flops, conv_bytes=conv_bytes, commit_updates=c_upd,
-                hist_pub_bytes=hist_pub_bytes)
+                hist_pub_bytes=hist_pub_bytes, fused_bytes=fused_bytes)
 
 
 def oracle_depth(parent, a):
@@ -467,6 +471,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-copy", action="store_true", help="skip the device-copy reference rate")
+    ap.add_argument("--fused", action="store_true",
+                    help="the conv fused into the verification (one kernel per step besides the path "
+                         "derivation; wy policy, deferred commit)")
     ap.add_argument("--per-layer", action="store_true",
                     help="also time the step as one call per layer (conv and verify of each layer "
                          "with its own state and history bank, one path derivation), all captured in "
@@ -499,6 +506,12 @@ def main():
 
     policy = L.POLICIES[args.policy]
     deferred = args.commit == "deferred" and policy == L.LUMO_POLICY_WY
+    if args.fused and not deferred:
+        sys.exit("--fused needs the wy policy and the deferred commit")
+    if args.fused and not args.prep:
+        # conv outputs are not unit-norm keys: as in the model, the queries and keys are
+        # normalised after the conv (in the kernel), else the replays diverge
+        sys.exit("--fused needs --prep (query/key normalisation of the conv outputs)")
     log(f"[bench] generating {args.config}")
     wl = configs.build(args.config)
     log(f"[bench] uploading; policy {args.policy}")
@@ -516,13 +529,17 @@ def main():
     def step(ev=None, s=stream):  # s=None: the current stream (a graph's capture stream)
         if ev is not None:
             ev[0].record(stream)
-        if deferred:
+        if args.fused:
+            pass  # the conv runs inside the verification
+        elif deferred:
             st.conv_pending(st, s)  # publishes the previous step's history, then the conv
         else:
             st.conv(s)
         if ev is not None:
             ev[1].record(stream)
-        if deferred:
+        if args.fused:
+            st.verify_conv_pending(st, s)  # publishes history and path, conv, verification
+        elif deferred:
             st.verify_pending(st, s)  # publishes the previous step's path, then verifies
         else:
             st.verify(s)
@@ -583,7 +600,7 @@ def main():
     ab = alg_bytes_flops(wl)
     hn = wl.head_node_updates
     if policy == L.LUMO_POLICY_WY:
-        vb = ab["verify_bytes"] + (ab["pub_bytes"] if deferred else 0)
+        vb = ab["fused_bytes"] if args.fused else ab["verify_bytes"] + (ab["pub_bytes"] if deferred else 0)
         ach = vb / (ver_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
@@ -592,19 +609,18 @@ def main():
         roof = {"bound": "alu", "achieved": round(ach, 2), "peak": PEAK_VALU_F32_TFS,
                 "unit": "TFLOP/s", "frac": round(ach / PEAK_VALU_F32_TFS, 4), "traffic": None}
     mode = "deferred" if deferred else "eager"
-    tr = recorded_traffic(args.policy, args.config, mode)
+    tr = recorded_traffic(args.policy, args.config, "fused" if args.fused else mode)
     if tr is not None:
         roof["traffic"] = {"fetch_bytes": tr["fetch_bytes"], "write_bytes": tr["write_bytes"],
                            "total_bytes": tr["fetch_bytes"] + tr["write_bytes"], "unit": "B per verify call",
                            "source": "profiles/traffic.json"}
-    roof["kernel"] = "verify + publication of the previous path" if deferred else "verify"
-    roof["per_launch"] = (f"{ab['verify_flops'] / 1e9:.2f} GFLOP, "
-                          f"{(ab['verify_bytes'] + (ab['pub_bytes'] if deferred else 0)) / 1e6:.1f} MB "
-                          f"algorithmic per verify call")
+    roof["kernel"] = ("tree conv + verify + publication of the previous path (one kernel)" if args.fused
+                      else "verify + publication of the previous path" if deferred else "verify")
+    roof["per_launch"] = (f"{ab['verify_flops'] / 1e9:.2f} GFLOP, {vb / 1e6:.1f} MB algorithmic per verify call")
     kernels = {
         "conv_gather_ms": round(conv_ms, 4),
-        "conv_hbm_frac": round((ab["conv_bytes"] + (ab["hist_pub_bytes"] if deferred else 0))
-                               / (conv_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "conv_hbm_frac": None if args.fused else round((ab["conv_bytes"] + (ab["hist_pub_bytes"] if deferred else 0))
+                                                       / (conv_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         "verify_ms": round(ver_ms, 4),
         "commit_ms": round(com_ms, 4),
         "step_ms_p10_p50_p90": step_dist,
@@ -626,7 +642,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded trees and operands shaped like the paper's workloads)",
         "config": {"workload": f"{args.config}: {WORKLOAD_TEXT[args.config]}",
-                   "policy": args.policy, "commit": mode, "head_node_updates_per_step": hn,
+                   "policy": args.policy, "commit": mode, "conv": "fused into verify" if args.fused else "separate",
+                   "head_node_updates_per_step": hn,
                    "operand_prep": "qk_norm+raw_gates" if args.prep else "none",
                    "operands": "bf16" if wl.op_dtype == 1 else "f32"},
         "roofline": roof, "kernels": kernels,

@@ -13,7 +13,9 @@
  * lumo_draft_select (the drafter's fused argmax / top-k selection), a
  * captured-graph form of the commit; lumo_tree_gdn_verify_pending and
  * lumo_tree_conv_gather_pending, which fold the publication of one iteration (state
- * replay, conv history) into the verification and convolution of the next; and forms
+ * replay, conv history) into the verification and convolution of the next, and
+ * lumo_tree_gdn_verify_conv_pending, which does both in one pass with the conv outputs
+ * never stored; and forms
  * that prepare the operands inside the kernels (lumo_gdn_prep: query/key
  * normalisation, gates from raw inputs).
  *
@@ -318,6 +320,46 @@ lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, const lumo_t
                                          const int32_t* path_out, const int32_t* path_len,
                                          const void* pend_k, const void* pend_v,
                                          const float* pend_g, const float* pend_beta, void* stream);
+
+/*
+ * lumo_tree_gdn_verify_conv_pending - lumo_tree_conv_gather_pending and
+ * lumo_tree_gdn_verify_pending in one pass, with the conv outputs never stored (Sec.
+ * V-C: windows gathered from the history and the candidate inputs, the tap computation
+ * fused, tap order and cast points kept; each output is rounded to bf16 where the
+ * separate conv stores it, then used as the verification's operand): the tree causal
+ * conv of x (channels q | k | v, window = the node's three nearest
+ * ancestors after the history, taps and activation as lumo_tree_conv_gather) gives
+ * each node's query, key and value rows; the pending path's keys and values are the
+ * same conv of x_prev along the path (from the history before its publication); the
+ * history is published from the pending path; the state bank receives the pending
+ * path's replay and the tree is verified from it, as lumo_tree_gdn_verify_pending.
+ * Results equal the two calls in sequence with y split into q, k, v (bit for bit).
+ *   channels   2 h_k d_k + h_v d_v; x channel 0 .. h_k d_k - 1 are the queries (key
+ *              head hk at hk d_k), then the keys, then the values (value head h at
+ *              2 h_k d_k + h d_v)
+ *   x          [n_layers][total_rows][channels] bf16, this iteration's rows
+ *   conv_hist  [n_req][n_layers][3][channels] bf16, read, and written in place where a
+ *              path is pending
+ *   w, bias, act   as lumo_tree_conv_gather (bias nullable); the layer's weights, so
+ *              the pending path's keys and values are convolved with them as well
+ *   g, beta, state, o, prep   as lumo_tree_gdn_verify_pending
+ *   pend_desc, max_path, path_out, path_len, pend_g, pend_beta   as
+ *              lumo_tree_gdn_verify_pending; x_prev is the previous iteration's x
+ *              ([n_layers][its total_rows][channels])
+ * Needs h_v = 2 h_k and the plan and dims of lumo_tree_gdn_verify_pending, else
+ * LUMO_EUNSUPPORTED; LUMO_ESHAPE for another channel count. Every request's history
+ * slice and state tile are read and written by one block, so calls must not overlap
+ * with other users of conv_hist or state.
+ */
+lumo_status lumo_tree_gdn_verify_conv_pending(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                              const lumo_gdn_prep* prep, int32_t channels, const void* x,
+                                              void* conv_hist, const float* w, const float* bias,
+                                              int32_t act, const float* g, const float* beta, float* state,
+                                              void* o, const lumo_tree_desc* pend_desc, int32_t max_path,
+                                              const int32_t* path_out, const int32_t* path_len,
+                                              const void* x_prev, const float* pend_g,
+                                              const float* pend_beta, void* stream);
+
 
 /*
  * lumo_gdn_commit - publish the accepted path (Alg. 1 publication; Alg. 2 replay;

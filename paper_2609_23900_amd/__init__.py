@@ -4,7 +4,8 @@ kernels; torch tensors only provide device memory and the current HIP stream.
 
 The functions keep the names of the C ABI (include/lumo_tree.h):
   lumo_tree_plan, lumo_tree_gdn_workspace_bytes, lumo_tree_conv_gather,
-  lumo_tree_conv_gather_pending, lumo_tree_gdn_verify, lumo_tree_gdn_verify_prep, lumo_tree_gdn_verify_pending, lumo_gdn_commit,
+  lumo_tree_conv_gather_pending, lumo_tree_gdn_verify, lumo_tree_gdn_verify_prep, lumo_tree_gdn_verify_pending,
+  lumo_tree_gdn_verify_conv_pending, lumo_gdn_commit,
   lumo_gdn_commit_prep, lumo_tree_attention, lumo_tree_attention_workspace_bytes,
   lumo_tree_attention_splits, lumo_draft_select, lumo_draft_select_workspace_bytes,
   lumo_draft_select_splits, lumo_gdn_commit_graph_create,
@@ -117,6 +118,8 @@ def _load():
     L.lumo_tree_gdn_verify_prep.argtypes = [PD, PT, PP, P, P, P, P, P, P, P, P]
     L.lumo_tree_gdn_verify_pending.argtypes = [PD, PT, PP, P, P, P, P, P, P, P, PT, I32, P, P, P, P, P, P,
                                                P]
+    L.lumo_tree_gdn_verify_conv_pending.argtypes = [PD, PT, PP, I32, P, P, P, P, I32, P, P, P, P, PT, I32, P, P,
+                                                    P, P, P, P]
     L.lumo_gdn_commit_prep.argtypes = [PD, PT, PP, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
     L.lumo_gdn_commit.argtypes = [PD, PT, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
     L.lumo_gdn_commit_graph_create.argtypes = [PD, PT, I32, P, P, P, P, P, P, P, P, I32, P, P,
@@ -127,7 +130,7 @@ def _load():
     L.lumo_last_error.restype = ctypes.c_char_p
     L.lumo_version.restype = ctypes.c_char_p
     for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_conv_gather_pending", "lumo_tree_gdn_verify",
-              "lumo_tree_gdn_verify_prep", "lumo_tree_gdn_verify_pending", "lumo_gdn_commit",
+              "lumo_tree_gdn_verify_prep", "lumo_tree_gdn_verify_pending", "lumo_tree_gdn_verify_conv_pending", "lumo_gdn_commit",
               "lumo_gdn_commit_prep", "lumo_tree_attention", "lumo_draft_select", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
         getattr(L, f).restype = ctypes.c_int
     return L
@@ -257,6 +260,16 @@ def lumo_tree_gdn_verify_pending(d, desc: TreeDesc, q, k, v, g, beta, state, o, 
         _dptr(beta), _dptr(state), _dptr(o), ctypes.byref(pend_desc.desc), int(max_path),
         _dptr(path_out), _dptr(path_len), _dptr(pend_k), _dptr(pend_v), _dptr(pend_g),
         _dptr(pend_beta), _stream(stream)))
+
+
+def lumo_tree_gdn_verify_conv_pending(d, desc: TreeDesc, channels, x, conv_hist, w, bias, act, g, beta, state, o,
+                                      pend_desc: TreeDesc, max_path, path_out, path_len, x_prev, pend_g,
+                                      pend_beta, stream=None, prep: Prep | None = None):
+    _check(_lib.lumo_tree_gdn_verify_conv_pending(
+        ctypes.byref(d), ctypes.byref(desc.desc), _prep_ptr(prep), int(channels), _dptr(x), _dptr(conv_hist),
+        _dptr(w), _dptr(bias), int(act), _dptr(g), _dptr(beta), _dptr(state), _dptr(o),
+        ctypes.byref(pend_desc.desc), int(max_path), _dptr(path_out), _dptr(path_len), _dptr(x_prev),
+        _dptr(pend_g), _dptr(pend_beta), _stream(stream)))
 
 
 def lumo_gdn_commit(d, desc: TreeDesc, max_path, accepted_node, path_out, path_len, k, v, g, beta,

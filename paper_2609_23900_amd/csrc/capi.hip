@@ -288,6 +288,54 @@ extern "C" lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, c
     return LUMO_OK;
 }
 
+extern "C" lumo_status lumo_tree_gdn_verify_conv_pending(
+    const lumo_gdn_dims* dims, const lumo_tree_desc* desc, const lumo_gdn_prep* prep, int32_t channels, const void* x,
+    void* conv_hist, const float* w, const float* bias, int32_t act, const float* g, const float* beta, float* state,
+    void* o, const lumo_tree_desc* pend_desc, int32_t max_path, const int32_t* path_out, const int32_t* path_len,
+    const void* x_prev, const float* pend_g, const float* pend_beta, void* stream) {
+    static const char* fn = "lumo_tree_gdn_verify_conv_pending";
+    clear_error();
+    LUMO_TRY(check_dims(dims, fn));
+    LUMO_TRY(check_desc(dims, desc, fn));
+    if (!pend_desc) return fail(LUMO_EINVAL, "%s: pend_desc is NULL", fn);
+    LUMO_TRY(check_desc(dims, pend_desc, fn));
+    LUMO_TRY(check_wy(dims, desc, fn));
+    PrepArgs pr;
+    LUMO_TRY(check_prep(prep, fn, pr));
+    if (dims->h_v != 2 * dims->h_k)
+        return fail(LUMO_EUNSUPPORTED, "%s: h_v / h_k = 2 only (got %d / %d)", fn, dims->h_v, dims->h_k);
+    if (channels != 2 * dims->h_k * dims->d_k + dims->h_v * dims->d_v)
+        return fail(LUMO_ESHAPE, "%s: channels %d, expected 2 h_k d_k + h_v d_v = %d", fn, channels,
+                    2 * dims->h_k * dims->d_k + dims->h_v * dims->d_v);
+    if (act != 0 && act != 1) return fail(LUMO_EINVAL, "%s: act %d (0 or 1)", fn, act);
+    if (max_path < 1 || max_path > 4096) return fail(LUMO_EINVAL, "%s: max_path %d (1..4096)", fn, max_path);
+    if (dims->n_req == 0) return LUMO_OK;
+    LUMO_TRY(check_ptr(state, fn, "state"));
+    LUMO_TRY(check_ptr(conv_hist, fn, "conv_hist"));
+    LUMO_TRY(check_ptr(w, fn, "w"));
+    LUMO_TRY(check_ptr(bias, fn, "bias", true));
+    LUMO_TRY(check_ptr(path_out, fn, "path_out"));
+    LUMO_TRY(check_ptr(path_len, fn, "path_len"));
+    if (pend_desc->plan.total_nodes > 0) {
+        LUMO_TRY(check_ptr(x_prev, fn, "x_prev"));
+        LUMO_TRY(check_ptr(pend_g, fn, "pend_g"));
+        LUMO_TRY(check_ptr(pend_beta, fn, "pend_beta"));
+    }
+    if (desc->plan.total_nodes > 0) {
+        LUMO_TRY(check_ptr(x, fn, "x"));
+        LUMO_TRY(check_ptr(g, fn, "g"));
+        LUMO_TRY(check_ptr(beta, fn, "beta"));
+        LUMO_TRY(check_ptr(o, fn, "o"));
+    }
+    GdnArgs a{nullptr, nullptr, nullptr, g, beta, state, o, nullptr, nullptr, pr};
+    PendArgs pa{pend_desc, max_path, path_out, path_len, nullptr, nullptr, pend_g, pend_beta, state};
+    ConvFuseArgs cf{channels, x, conv_hist, w, bias, act, x_prev};
+    hipError_t e = launch_wy_conv(*dims, *desc, a, static_cast<hipStream_t>(stream), pa, cf);
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not available for this shape", fn);
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
 namespace {
 
 lumo_status check_commit(const lumo_gdn_dims* dims, const lumo_tree_desc* desc, int32_t max_path,

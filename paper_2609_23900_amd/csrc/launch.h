@@ -51,6 +51,22 @@ struct PendArgs {
 // in `desc` are still published.
 hipError_t launch_wy(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s,
                      const PendArgs* pend = nullptr);
+
+// The tree conv fused into the WY verification: q, k and v are the conv outputs of x
+// (channels q | k | v), computed in the kernel and never stored; the history is
+// published from the pending path (when one is pending) and read from hist. With this,
+// GdnArgs q, k, v and PendArgs k, v are unused.
+struct ConvFuseArgs {
+    int32_t channels;
+    const void* x;        // [layers][rows][channels]
+    void* hist;           // [req][layers][3][channels], published in place
+    const float* w;       // [layers][channels][4]
+    const float* bias;    // [layers][channels] or NULL
+    int32_t act;
+    const void* x_prev;   // the pending path's x rows: [layers][previous rows][channels]
+};
+hipError_t launch_wy_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s,
+                          const PendArgs& pend, const ConvFuseArgs& cf);
 constexpr int kWyMaxDepth = 17;  // nodes on a root-to-leaf path
 
 struct CommitArgs {

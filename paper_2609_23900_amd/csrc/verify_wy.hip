@@ -33,6 +33,16 @@
 // This replaces sequential scans; the arithmetic differs from them in rounding only
 // (tolerance-level, not bitwise). The commit stays a sequential replay.
 //
+// Fused conv (CONV): the key, query and value rows are the tree conv's outputs of x
+// rows, never stored. The block stages raw x rows where it would stage the rows, and at
+// each chunk its threads (two channels each) walk the chunk's nodes in preorder with the
+// raw x of the current root path kept by depth in LDS, so every node's window (its three
+// nearest ancestors, or history entries) is at hand; the conv outputs replace the raw
+// rows in place, and the keys of the root path are kept by depth for the next chunk's
+// path-stack rows. The pending path's keys and values are convolved along the path, and
+// the block publishes its slice of the history (one block per key head, so no other
+// block reads that slice).
+//
 // Deferred publication (PEND): before the slab is split, each wave replays the previous
 // iteration's accepted path on it with the sequential update (Eq. (2)-(3), one path
 // node at a time, in fp32), stores it back to the state bank, and verifies from it. The
@@ -86,6 +96,17 @@ struct PendParams {
 };
 constexpr int kPend = 16;  // path entries staged per round of the deferred publication
 
+// Fused conv (CONV kernels): x rows hold the channels q | k | v (value head h at
+// 2 h_k d + h d); w [layers][channels][4], tap 3 the newest; bias nullable.
+struct ConvFuseParams {
+    const uint16_t* x;
+    uint16_t* hist;          // [req][layers][3][channels], published in place
+    const uint16_t* x_prev;  // the pending path's rows
+    const float* w;
+    const float* bias;
+    int32_t channels, act;
+};
+
 // Block-shared staging of one chunk: [key 32 | query 32 | path-stack key 16] rows of
 // 16 slots of 8 bf16; key block kb of row n sits in slot kb ^ (n & 15), so the
 // fragment reads of a half-wave (32 rows, one key block) spread over all banks.
@@ -122,12 +143,13 @@ __device__ __forceinline__ float row_group_sum(float x) {
 // QKN: every query and key row x is used as x / sqrt(|x|^2 + eps) (Sec. IV-B). The
 // bf16 rows stay as they are in LDS and the MFMA products; the per-row factors scale
 // the Gram entries, R0 k, R0 q and k.q in the records, and the pending path's keys.
-template <int D, int NVH, bool PEND, bool QKN>
+template <int D, int NVH, bool PEND, bool QKN, bool CONV>
 __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, const uint16_t* __restrict__ kmat,
                                                     const uint16_t* __restrict__ qmat,
                                                     const uint16_t* __restrict__ vmat, const float* __restrict__ gmat,
                                                     const float* __restrict__ bmat, const float* __restrict__ state0,
-                                                    uint16_t* __restrict__ out, PendParams pd) {
+                                                    uint16_t* __restrict__ out, PendParams pd, ConvFuseParams cf) {
+    static_assert(!CONV || (NVH == 2 && PEND), "the fused conv serves two value heads per block, with publication");
     constexpr int W = Rec<D>::kWords;
     constexpr int nthr = 128 * NVH;
     // LDS, one object per role: the compiler orders LDS reads after the direct
@@ -136,7 +158,12 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     __shared__ __attribute__((aligned(16))) float G[kCand * kGS];  // block: Gram [candidate][chunk key | chunk query]
     __shared__ __attribute__((aligned(16))) float recs[2 * NVH][kTile * W];  // per wave: the chunk's coefficient records
     __shared__ float alphas[2 * NVH][64];          // per wave: exp(g) of the candidates
-    __shared__ uint4 vbufs[2 * NVH][2][kTile * 8]; // per wave: value rows, then outputs; double-buffered
+    // per wave: value rows, then outputs; double-buffered (CONV: single, for the caches)
+    __shared__ uint4 vbufs[2 * NVH][CONV ? 1 : 2][kTile * 8];
+    // CONV: raw x of the current root path by depth (rows 0..2 the history, row 3 + d
+    // depth d), two channels per thread; conv outputs of the root path's keys by depth
+    __shared__ uint32_t rawc[CONV ? D + 4 : 1][CONV ? nthr : 1];
+    __shared__ uint32_t kcache[CONV ? D + 1 : 1][CONV ? 64 : 1];
     __shared__ float nrm[kTileRows];               // QKN: 1/|row| of [stack keys 16 | chunk keys 32 | queries 32]
     const int tid = (int)threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: head and half in SGPRs
@@ -176,6 +203,9 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     // across the loop, which would not fit in the registers.
     int ln = lane;
     int tn = t;
+    // CONV: x row stride and the block's channel groups (queries, keys, values)
+    const long xc = CONV ? cf.channels : 0;
+    const int qoff = hk * kD, koff = (p.h_k + hk) * kD, voff = 2 * p.h_k * kD;
 
     // Rows of the chunk at c0 as seen by this lane: n = node t's (every lane; positions
     // past the end repeat the last node, so padding slots are exact copies of it) and
@@ -227,6 +257,13 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
             const int src = g4 == 0 ? rq[0] : g4 == 1 ? rq[1] : g4 == 2 ? rq[2] : rq[3];
             const int nr = nr0 + g4;
             const int kb = (ln & 15) ^ (nr & 15);
+            if constexpr (CONV) {
+                // raw x rows; the path-stack rows come from the key cache instead
+                if (stack_round) continue;
+                __builtin_amdgcn_global_load_lds(cf.x + (krow0 + src) * xc + (nr >= kTile ? qoff : koff) + 8 * kb,
+                                                 (lds_void*)&tile.slot[j * nthr + 64 * wave], 16, 0, 0);
+                continue;
+            }
             const uint16_t* mat = (!stack_round && nr >= kTile) ? qmat : kmat;
             __builtin_amdgcn_global_load_lds(mat + ((krow0 + src) * p.h_k + hk) * kD + 8 * kb,
                                              (lds_void*)&tile.slot[j * nthr + 64 * wave], 16, 0, 0);
@@ -264,8 +301,92 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int q = 64 * i + ln;
-            __builtin_amdgcn_global_load_lds(vmat + ((krow0 + rn[i]) * p.h_v + h) * kD + j0 + 8 * (q & 7),
-                                             (lds_void*)&dst[64 * i], 16, 0, 0);
+            const uint16_t* src = CONV ? cf.x + (krow0 + rn[i]) * xc + voff + h * kD + j0 + 8 * (q & 7)
+                                       : vmat + ((krow0 + rn[i]) * p.h_v + h) * kD + j0 + 8 * (q & 7);
+            __builtin_amdgcn_global_load_lds(src, (lds_void*)&dst[64 * i], 16, 0, 0);
+        }
+    };
+
+    // CONV walks: thread tid serves x channels 2 (tid % 4), +1 of 8-channel slot
+    // cs = tid / 4: keys (cs < 16), queries (cs < 32), values of wave (cs - 32) / 8.
+    struct Taps {
+        float lo[4], hi[4], blo, bhi;
+    };
+    auto walk_channel = [&]() -> int {
+        const int cs = tid >> 2, pt = tid & 3;
+        if (cs < 16) return koff + 8 * cs + 2 * pt;
+        if (cs < 32) return qoff + 8 * (cs - 16) + 2 * pt;
+        const int vw = (cs - 32) >> 3;
+        const int hv = hk * p.group + pp * NVH + (vw >> 1);
+        return voff + hv * kD + 64 * (vw & 1) + 8 * ((cs - 32) & 7) + 2 * pt;
+    };
+    auto load_taps = [&](Taps& tp) {
+        const long c = (long)l * xc + walk_channel();
+        const float4 a = *reinterpret_cast<const float4*>(cf.w + c * 4);
+        const float4 b = *reinterpret_cast<const float4*>(cf.w + (c + 1) * 4);
+        tp.lo[0] = a.x; tp.lo[1] = a.y; tp.lo[2] = a.z; tp.lo[3] = a.w;
+        tp.hi[0] = b.x; tp.hi[1] = b.y; tp.hi[2] = b.z; tp.hi[3] = b.w;
+        tp.blo = cf.bias ? cf.bias[c] : 0.f;
+        tp.bhi = cf.bias ? cf.bias[c + 1] : 0.f;
+    };
+    // act(bias + sum_t w_t window_t) of a channel pair, taps oldest first and the node's
+    // own entry last, fp32, then one cast: the conv kernels' arithmetic
+    auto conv2 = [&](const Taps& tp, uint32_t w0, uint32_t w1, uint32_t w2, uint32_t xr) -> uint32_t {
+        float lo = tp.blo, hi = tp.bhi;
+        lo = __builtin_fmaf(tp.lo[0], bf16_lo(w0), lo);
+        hi = __builtin_fmaf(tp.hi[0], bf16_hi(w0), hi);
+        lo = __builtin_fmaf(tp.lo[1], bf16_lo(w1), lo);
+        hi = __builtin_fmaf(tp.hi[1], bf16_hi(w1), hi);
+        lo = __builtin_fmaf(tp.lo[2], bf16_lo(w2), lo);
+        hi = __builtin_fmaf(tp.hi[2], bf16_hi(w2), hi);
+        lo = __builtin_fmaf(tp.lo[3], bf16_lo(xr), lo);
+        hi = __builtin_fmaf(tp.hi[3], bf16_hi(xr), hi);
+        if (cf.act == 1) {  // SiLU, as in the conv kernels
+            lo = lo * __builtin_amdgcn_rcpf(1.f + __expf(-lo));
+            hi = hi * __builtin_amdgcn_rcpf(1.f + __expf(-hi));
+        }
+        return f32x2_to_bf16x2(lo, hi);
+    };
+    // the chunk's nodes in preorder: window from the root-path cache, the raw entry into
+    // the cache at the node's depth, the conv output over the raw entry (tile rows,
+    // value buffers), the key into the key cache. Padding slots repeat the last node and
+    // redo it exactly.
+    auto conv_walk = [&](const Taps& tp, const LaneInfo<D>& li) {
+        const int cs = tid >> 2, pt = tid & 3;
+#pragma unroll 4
+        for (int n = 0; n < kTile; ++n) {
+            const int d = __builtin_amdgcn_readlane(li.dep, n);
+            uint32_t* px = cs < 16   ? reinterpret_cast<uint32_t*>(&tile.slot[n * 16 + (cs ^ (n & 15))]) + pt
+                           : cs < 32 ? reinterpret_cast<uint32_t*>(&tile.slot[(kTile + n) * 16 + ((cs - 16) ^ (n & 15))]) + pt
+                                     : reinterpret_cast<uint32_t*>(&vbufs[(cs - 32) >> 3][0][8 * n + ((cs - 32) & 7)]) + pt;
+            const uint32_t xr = *px;
+            const uint32_t y = conv2(tp, rawc[d][tid], rawc[d + 1][tid], rawc[d + 2][tid], xr);
+            rawc[d + 3][tid] = xr;
+            *px = y;
+            if (cs < 16) kcache[d][tid] = y;
+        }
+    };
+    // the root-path caches at the start of the walk: the history, and keys and
+    // path-stack rows cleared (finite; rows past a node's depth are masked, not skipped)
+    auto conv_cache_init = [&](uint32_t a0, uint32_t a1, uint32_t a2) {
+        rawc[0][tid] = a0;
+        rawc[1][tid] = a1;
+        rawc[2][tid] = a2;
+        if (tid < 64) {
+#pragma unroll
+            for (int m = 0; m <= D; ++m) kcache[m][tid] = 0u;
+        }
+        static_assert(kStack * 16 == nthr || !CONV, "one 16-byte piece of the stack rows per thread");
+        tile.slot[2 * kTile * 16 + tid] = make_uint4(0, 0, 0, 0);
+    };
+    // the next chunk's path-stack rows: the keys of the root path by depth
+    auto stack_from_cache = [&]() {
+        if (tid < 64) {
+            const int cs = tid >> 2, pt = tid & 3;
+            constexpr int ns = D + 1 < kStack ? D + 1 : kStack;
+#pragma unroll
+            for (int m = 0; m < ns; ++m)
+                reinterpret_cast<uint32_t*>(&tile.slot[(2 * kTile + m) * 16 + (cs ^ m)])[pt] = kcache[m][tid];
         }
     };
 
@@ -304,6 +425,36 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         uint4* kst = reinterpret_cast<uint4*>(G);       // kPend key rows x 16 slots
         uint4* vst = reinterpret_cast<uint4*>(wrec);    // kPend entries x 64 values (8 slots)
         const uint16_t* vsh = reinterpret_cast<const uint16_t*>(wrec);
+        // CONV: this thread's channels of the old history (the chain conv's first window,
+        // rolled along the path) and of the published one, the last three of (old
+        // history, the path's raw x rows)
+        uint32_t hw0 = 0, hw1 = 0, hw2 = 0, hn0 = 0, hn1 = 0, hn2 = 0;
+        uint16_t* hsl = nullptr;
+        Taps tpp;
+        if constexpr (CONV) {
+            const int c = walk_channel();
+            hsl = cf.hist + ((long)r * p.n_layers + l) * 3 * xc + c;
+            hw0 = *reinterpret_cast<const uint32_t*>(hsl);
+            hw1 = *reinterpret_cast<const uint32_t*>(hsl + xc);
+            hw2 = *reinterpret_cast<const uint32_t*>(hsl + 2 * xc);
+            int hrow = 0;  // lane j < 3: the row of path entry plen + j - 3, when there is one
+            if (lane < 3 && plen + lane >= 3) {
+                const int node = min(max(ppath[plen + lane - 3], 0), pn - 1);
+                hrow = pd.blob[pd.o_row + pbase + node];
+            }
+            uint32_t hn[3];
+#pragma unroll
+            for (int j = 0; j < 3; ++j) {
+                const int pos = plen + j;
+                const int rowj = __builtin_amdgcn_readlane(hrow, j);
+                hn[j] = pos >= 3 ? *reinterpret_cast<const uint32_t*>(cf.x_prev + (prow0 + rowj) * xc + c)
+                                 : (pos == 1 ? hw1 : hw2);  // pos is at least 1
+            }
+            hn0 = hn[0];
+            hn1 = hn[1];
+            hn2 = hn[2];
+            load_taps(tpp);
+        }
         for (int e0 = 0; e0 < plen; e0 += kPend) {
             const int ne = min(plen - e0, kPend);
             if (e0 > 0) lds_barrier();  // every wave has read the previous entries' key rows
@@ -328,18 +479,37 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                 for (int k4 = 0; k4 < 4; ++k4) rq[k4] = __builtin_amdgcn_readlane(row, nr0 + k4);
                 const int g4 = lane >> 4;
                 const int src = g4 == 0 ? rq[0] : g4 == 1 ? rq[1] : g4 == 2 ? rq[2] : rq[3];
-                __builtin_amdgcn_global_load_lds(pd.k + ((prow0 + src) * p.h_k + hk) * kD + 8 * (lane & 15),
-                                                 (lds_void*)&kst[j * nthr + 64 * wave], 16, 0, 0);
+                const uint16_t* ks = CONV ? cf.x_prev + (prow0 + src) * xc + koff + 8 * (lane & 15)
+                                          : pd.k + ((prow0 + src) * p.h_k + hk) * kD + 8 * (lane & 15);
+                __builtin_amdgcn_global_load_lds(ks, (lds_void*)&kst[j * nthr + 64 * wave], 16, 0, 0);
             }
 #pragma unroll
             for (int i = 0; i < kPend * 8 / 64; ++i) {
                 const int q = 64 * i + lane;
-                __builtin_amdgcn_global_load_lds(pd.v + ((prow0 + rv[i]) * p.h_v + h) * kD + j0 + 8 * (q & 7),
-                                                 (lds_void*)&vst[64 * i], 16, 0, 0);
+                const uint16_t* vsrc = CONV ? cf.x_prev + (prow0 + rv[i]) * xc + voff + h * kD + j0 + 8 * (q & 7)
+                                            : pd.v + ((prow0 + rv[i]) * p.h_v + h) * kD + j0 + 8 * (q & 7);
+                __builtin_amdgcn_global_load_lds(vsrc, (lds_void*)&vst[64 * i], 16, 0, 0);
             }
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
+            if constexpr (CONV) {
+                // the entries' keys and values: conv outputs along the path, in place
+                const int cs = tid >> 2, pt = tid & 3;
+                if (cs < 16 || cs >= 32) {
+                    for (int e = 0; e < ne; ++e) {
+                        uint32_t* px = cs < 16 ? reinterpret_cast<uint32_t*>(&kst[e * 16 + cs]) + pt
+                                               : reinterpret_cast<uint32_t*>(&reinterpret_cast<uint4*>(
+                                                     recs[(cs - 32) >> 3])[8 * e + ((cs - 32) & 7)]) + pt;
+                        const uint32_t xr = *px;
+                        *px = conv2(tpp, hw0, hw1, hw2, xr);
+                        hw0 = hw1;
+                        hw1 = hw2;
+                        hw2 = xr;
+                    }
+                }
+                lds_barrier();
+            }
             for (int e = 0; e < ne; ++e) {
                 const float ae = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pa), e));
                 const float be = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pb), e));
@@ -391,6 +561,12 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                                 __builtin_fmaf(dl[ct], kf[kb][e8], ae * __uint_as_float(raw[ct][kb][e8])));
             }
         }
+        if constexpr (CONV) {  // this block's slice of the history (no other block reads it)
+            *reinterpret_cast<uint32_t*>(hsl) = hn0;
+            *reinterpret_cast<uint32_t*>(hsl + xc) = hn1;
+            *reinterpret_cast<uint32_t*>(hsl + 2 * xc) = hn2;
+            conv_cache_init(hn0, hn1, hn2);
+        }
         float* Sw = pd.state + (((long)r * p.n_layers + l) * p.h_v + h) * (long)(kD * kD) +
                     (long)(8 * (lane / 16)) * kD + j0 + 4 * (lane % 16);
 #pragma unroll
@@ -405,6 +581,13 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     LaneInfo<D> info;
     if (!PEND || plen <= 0) {
         rowC = lane_rows(0);
+        uint32_t h0 = 0, h1 = 0, h2 = 0;
+        if constexpr (CONV) {  // the history of this thread's channels, as it is
+            const uint16_t* hs = cf.hist + ((long)r * p.n_layers + l) * 3 * xc + walk_channel();
+            h0 = *reinterpret_cast<const uint32_t*>(hs);
+            h1 = *reinterpret_cast<const uint32_t*>(hs + xc);
+            h2 = *reinterpret_cast<const uint32_t*>(hs + 2 * xc);
+        }
         slab_load(0);
         slab_load(1);
         asm volatile("" ::: "memory");
@@ -414,6 +597,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         rowA = N > kTile ? lane_rows(kTile) : rowC;
         slab_load(2);
         slab_load(3);
+        if constexpr (CONV) conv_cache_init(h0, h1, h2);
     } else {
         if (N > 0) rowC = lane_rows(0);
 #pragma unroll
@@ -508,6 +692,8 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     for (int c0 = 0, buf = 0; c0 < N; c0 += kTile, buf ^= 1) {
         const bool more = c0 + kTile < N;
         const bool two = c0 + kTile / 2 < N;  // the second half holds real nodes
+        Taps tp;
+        if constexpr (CONV) load_taps(tp);  // lands with the chunk's copies
         // This chunk's tile, value rows and lane view have landed for every wave. The empty
         // asm consumes the lane view here, so that no first use of it later waits on the
         // copies issued below.
@@ -515,6 +701,10 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         asm volatile("" ::"v"(info.dep), "v"(info.g), "v"(info.b), "v"(info.ci[0]), "v"(info.ci[D / 4 - 1]),
                      "v"(rowC.n), "v"(rowA.n), "v"(rowA.s));
         lds_barrier();
+        if constexpr (CONV) {  // raw rows -> conv outputs, for every wave's rows
+            conv_walk(tp, info);
+            lds_barrier();
+        }
         ln = lane;
         asm volatile("" : "+v"(ln));
         tn = ln % kTile;
@@ -542,10 +732,12 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
                         __builtin_amdgcn_rsqf(ss + p.qk_eps);
             }
         }
-        if (c0 > 0) flush(vbufs[wave][buf ^ 1], kTile);  // the previous chunk had two halves
-        if (more) {
-            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the flush has read the buffer
-            v_issue(rowA, vbufs[wave][buf ^ 1]);
+        if constexpr (!CONV) {
+            if (c0 > 0) flush(vbufs[wave][buf ^ 1], kTile);  // the previous chunk had two halves
+            if (more) {
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the flush has read the buffer
+                v_issue(rowA, vbufs[wave][buf ^ 1]);
+            }
         }
 
         // ---- Gram (head-independent) into LDS
@@ -631,7 +823,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         }
 
         const float* rec = wrec;
-        uint16_t* vs = reinterpret_cast<uint16_t*>(vbufs[wave][buf]);
+        uint16_t* vs = reinterpret_cast<uint16_t*>(vbufs[wave][CONV ? 0 : buf]);
         // Straight-line over the 16 slots of a half: slots past the chunk's end hold exact
         // copies of its last node (tile rows, value row, record), so they recompute that
         // node's delta and output bit for bit and store the same value to the same place.
@@ -684,33 +876,42 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         if (two) half_products(1, pk, pq);
         lds_barrier();  // every wave has read the tile: it may be refilled
         if (more) tile_issue(rowA);
+        if constexpr (CONV) {
+            if (more) stack_from_cache();
+        }
         if (two) {
             exchange(pk);
             exchange(pq);
             recursion(1, pk, pq);
         }
+        if constexpr (CONV) {  // single value buffer: out, then the next chunk's rows in
+            flush(vbufs[wave][0], two ? kTile : kTile / 2);
+            if (more) {
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the flush has read the buffer
+                v_issue(rowA, vbufs[wave][0]);
+            }
+        }
         rowC = rowA;
         rowA = rowB;
     }
-    // the last chunk's outputs
-    const int cl = (N - 1) / kTile;  // index of the last chunk
-    flush(vbufs[wave][cl & 1], cl * kTile + kTile / 2 < N ? kTile : kTile / 2);
+    if constexpr (!CONV) {  // the last chunk's outputs
+        const int cl = (N - 1) / kTile;  // index of the last chunk
+        flush(vbufs[wave][cl & 1], cl * kTile + kTile / 2 < N ? kTile : kTile / 2);
+    }
 }
 
-template <int D, int NVH, bool PEND, bool QKN>
+template <int D, int NVH, bool PEND, bool QKN, bool CONV = false>
 hipError_t launch_wy_kernel(const lumo_gdn_dims& d, const WyParams& p, const GdnArgs& a, hipStream_t s,
-                            const PendParams& pp) {
+                            const PendParams& pp, const ConvFuseParams& cf = ConvFuseParams{}) {
     const long nb = (long)d.n_req * d.n_layers * d.h_k * (p.group / NVH);
-    hipLaunchKernelGGL((wy_kernel<D, NVH, PEND, QKN>), dim3((unsigned)nb), dim3(128 * NVH), 0, s, p,
+    hipLaunchKernelGGL((wy_kernel<D, NVH, PEND, QKN, CONV>), dim3((unsigned)nb), dim3(128 * NVH), 0, s, p,
                        static_cast<const uint16_t*>(a.k), static_cast<const uint16_t*>(a.q),
                        static_cast<const uint16_t*>(a.v), a.g, a.beta, PEND ? pp.state : a.state0,
-                       static_cast<uint16_t*>(a.o), pp);
+                       static_cast<uint16_t*>(a.o), pp, cf);
     return hipGetLastError();
 }
 
-template <int D, bool PEND>
-hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s,
-                       const PendParams& pp) {
+WyParams wy_params(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a) {
     const lumo_plan& pl = desc.plan;
     WyParams p;
     p.blob = desc.blob;
@@ -729,6 +930,13 @@ hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.qk_eps = a.prep.qk_eps;
     p.a_log = a.prep.a_log;
     p.dt_bias = a.prep.dt_bias;
+    return p;
+}
+
+template <int D, bool PEND>
+hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s,
+                       const PendParams& pp) {
+    const WyParams p = wy_params(d, desc, a);
     // one block per (request, layer, key head, pair of value heads): the pair's waves
     // share the staged key and query rows and the Gram. Grids of fewer pair blocks than
     // CUs (one layer of a batch, few requests) take one value head per block instead:
@@ -743,6 +951,24 @@ hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
 
 }  // namespace
 
+PendParams pend_params(const PendArgs& pend) {
+    const lumo_plan& pl = pend.desc->plan;
+    PendParams pp;
+    pp.blob = pend.desc->blob;
+    pp.o_node_off = pl.o_node_off;
+    pp.o_row = pl.o_row;
+    pp.total_rows = pl.total_rows;
+    pp.max_path = pend.max_path;
+    pp.path_out = pend.path_out;
+    pp.path_len = pend.path_len;
+    pp.k = static_cast<const uint16_t*>(pend.k);
+    pp.v = static_cast<const uint16_t*>(pend.v);
+    pp.g = pend.g;
+    pp.beta = pend.beta;
+    pp.state = pend.state;
+    return pp;
+}
+
 hipError_t launch_wy(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s,
                      const PendArgs* pend) {
     if (desc.plan.max_depth > kStack + 1) return hipErrorNotSupported;
@@ -754,21 +980,31 @@ hipError_t launch_wy(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const G
         return d8 ? launch_wy_d<8, false>(d, desc, a, s, none) : launch_wy_d<16, false>(d, desc, a, s, none);
     }
     if (d.n_req == 0) return hipSuccess;  // requests without nodes are still published
-    const lumo_plan& pl = pend->desc->plan;
-    PendParams pp;
-    pp.blob = pend->desc->blob;
-    pp.o_node_off = pl.o_node_off;
-    pp.o_row = pl.o_row;
-    pp.total_rows = pl.total_rows;
-    pp.max_path = pend->max_path;
-    pp.path_out = pend->path_out;
-    pp.path_len = pend->path_len;
-    pp.k = static_cast<const uint16_t*>(pend->k);
-    pp.v = static_cast<const uint16_t*>(pend->v);
-    pp.g = pend->g;
-    pp.beta = pend->beta;
-    pp.state = pend->state;
+    const PendParams pp = pend_params(*pend);
     return d8 ? launch_wy_d<8, true>(d, desc, a, s, pp) : launch_wy_d<16, true>(d, desc, a, s, pp);
+}
+
+hipError_t launch_wy_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s,
+                          const PendArgs& pend, const ConvFuseArgs& c) {
+    if (desc.plan.max_depth > kStack + 1 || d.h_v != 2 * d.h_k) return hipErrorNotSupported;
+    if (d.n_req == 0) return hipSuccess;
+    const bool d8 = desc.plan.max_depth <= 9;
+    const WyParams p = wy_params(d, desc, a);
+    const PendParams pp = pend_params(pend);
+    ConvFuseParams cf;
+    cf.x = static_cast<const uint16_t*>(c.x);
+    cf.hist = static_cast<uint16_t*>(c.hist);
+    cf.x_prev = static_cast<const uint16_t*>(c.x_prev);
+    cf.w = c.w;
+    cf.bias = c.bias;
+    cf.channels = c.channels;
+    cf.act = c.act;
+    const bool qkn = (a.prep.flags & LUMO_PREP_QK_NORM) != 0;
+    if (d8)
+        return qkn ? launch_wy_kernel<8, 2, true, true, true>(d, p, a, s, pp, cf)
+                   : launch_wy_kernel<8, 2, true, false, true>(d, p, a, s, pp, cf);
+    return qkn ? launch_wy_kernel<16, 2, true, true, true>(d, p, a, s, pp, cf)
+               : launch_wy_kernel<16, 2, true, false, true>(d, p, a, s, pp, cf);
 }
 
 }  // namespace lumo

@@ -12,7 +12,7 @@ import torch
 
 from . import (LUMO_BF16, LumoError, TreeDesc, dims, lumo_gdn_commit_graph_create,
                lumo_gdn_commit_prep, lumo_tree_conv_gather, lumo_tree_conv_gather_pending,
-               lumo_tree_gdn_verify,
+               lumo_tree_gdn_verify, lumo_tree_gdn_verify_conv_pending,
                lumo_tree_gdn_verify_pending, lumo_tree_gdn_verify_prep,
                lumo_tree_gdn_workspace_bytes)
 
@@ -107,6 +107,19 @@ class GdnTreeStep:
                                      self.state if state is None else state, self.o, prev.desc,
                                      prev.max_path, prev.path_out, prev.path_len, prev.t["k"],
                                      prev.t["v"], prev.t["g"], prev.t["beta"], stream, self.prep)
+
+    def verify_conv_pending(self, prev: "GdnTreeStep", stream=None, state=None):
+        """conv_pending and verify_pending in one pass: the queries, keys and values are
+        this step's conv outputs of x (channels q | k | v), never stored; prev's accepted
+        path (prev.commit(defer=True, with_conv=False)) is published into the history and
+        the state bank first. self.t["q"], ["k"], ["v"] and self.y are not used."""
+        if not self.has_conv:
+            raise LumoError(1, "no conv operands")
+        lumo_tree_gdn_verify_conv_pending(self.dims, self.desc, self.channels, self.x, self.hist, self.w,
+                                          self.bias, self.act, self.t["g"], self.t["beta"],
+                                          self.state if state is None else state, self.o, prev.desc,
+                                          prev.max_path, prev.path_out, prev.path_len, prev.x, prev.t["g"],
+                                          prev.t["beta"], stream, self.prep)
 
     def commit(self, stream=None, with_conv=True, defer=False):
         """Accepted path, conv history (unless with_conv is False: then the next
