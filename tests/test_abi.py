@@ -355,3 +355,27 @@ def test_draft_select_empty_and_single_part_need_no_workspace():
     assert L.lumo_draft_select_splits(8, 248320, 0) == 30
     assert L.lumo_draft_select_splits(64, 248320, 1) == 15
     assert L.lumo_draft_select_splits(1, 10, 1) == 1
+
+
+def _fused(d, desc, pdesc=None, channels=None, act=1, ptrs=True, max_path=4):
+    P = ctypes.c_void_p
+    f = P(FAKE) if ptrs else None
+    ch = 2 * d.h_k * d.d_k + d.h_v * d.d_v if channels is None else channels
+    return L._lib.lumo_tree_gdn_verify_conv_pending(
+        ctypes.byref(d), ctypes.byref(desc), None, ch, f, f, f, None, act, f, f, f, f,
+        ctypes.byref(pdesc if pdesc is not None else desc), max_path, f, f, f, f, f, None)
+
+
+def test_fused_conv_rejects_bad_arguments():
+    wy, _b1 = _desc(policy=L.LUMO_POLICY_WY)
+    paths, _b2 = _desc(policy=L.LUMO_POLICY_PATHS)
+    ok = _dims(h_k=2, h_v=4, d_k=128, d_v=128, op_dtype=L.LUMO_BF16)
+    assert _fused(_dims(h_k=2, h_v=6, d_k=128, d_v=128, op_dtype=L.LUMO_BF16), wy) == L.LUMO_EUNSUPPORTED
+    assert _fused(ok, wy, channels=1000) == L.LUMO_ESHAPE
+    assert _fused(ok, wy, act=2) == L.LUMO_EINVAL
+    assert _fused(ok, wy, max_path=0) == L.LUMO_EINVAL
+    assert _fused(ok, paths) == L.LUMO_EUNSUPPORTED  # the WY plan only
+    assert _fused(ok, wy, ptrs=False) == L.LUMO_EINVAL
+    assert L._lib.lumo_tree_gdn_verify_conv_pending(
+        ctypes.byref(ok), ctypes.byref(wy), None, 1024, *([ctypes.c_void_p(FAKE)] * 3), None, 1,
+        *([ctypes.c_void_p(FAKE)] * 4), None, 4, *([ctypes.c_void_p(FAKE)] * 5), None) == L.LUMO_EINVAL
