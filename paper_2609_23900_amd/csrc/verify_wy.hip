@@ -124,6 +124,10 @@ struct LaneInfo {
     float g, b;
 };
 
+template <int R> struct RoleTag {
+    static constexpr int value = R;
+};
+
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
 
 // The sum of x over the four 16-lane rows, in every lane (the same bits in all four:
@@ -351,20 +355,45 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     // the cache at the node's depth, the conv output over the raw entry (tile rows,
     // value buffers), the key into the key cache. Padding slots repeat the last node and
     // redo it exactly.
-    auto conv_walk = [&](const Taps& tp, const LaneInfo<D>& li) {
+    // A wave's channels are all keys (wave 0), all queries (wave 1) or all values, so the
+    // walk is specialised per role. Node n + 1's window and raw entry are read before
+    // node n's writes: in preorder the next depth is at most d + 1, so the only entry
+    // node n writes that node n + 1 can need is its own raw entry (the newest window
+    // entry of a child), taken from the register.
+    static_assert(!CONV || nthr == 256, "one role per wave: keys, queries, two waves of values");
+    auto conv_walk_role = [&](const Taps& tp, const LaneInfo<D>& li, auto role) {
+        constexpr int R = decltype(role)::value;
         const int cs = tid >> 2, pt = tid & 3;
+        auto px = [&](int n) -> uint32_t* {
+            if constexpr (R == 0) return reinterpret_cast<uint32_t*>(&tile.slot[n * 16 + (cs ^ (n & 15))]) + pt;
+            else if constexpr (R == 1)
+                return reinterpret_cast<uint32_t*>(&tile.slot[(kTile + n) * 16 + ((cs - 16) ^ (n & 15))]) + pt;
+            else return reinterpret_cast<uint32_t*>(&vbufs[(cs - 32) >> 3][0][8 * n + ((cs - 32) & 7)]) + pt;
+        };
+        int d = __builtin_amdgcn_readlane(li.dep, 0);
+        uint32_t w0 = rawc[d][tid], w1 = rawc[d + 1][tid], w2 = rawc[d + 2][tid], xr = *px(0);
 #pragma unroll 4
         for (int n = 0; n < kTile; ++n) {
-            const int d = __builtin_amdgcn_readlane(li.dep, n);
-            uint32_t* px = cs < 16   ? reinterpret_cast<uint32_t*>(&tile.slot[n * 16 + (cs ^ (n & 15))]) + pt
-                           : cs < 32 ? reinterpret_cast<uint32_t*>(&tile.slot[(kTile + n) * 16 + ((cs - 16) ^ (n & 15))]) + pt
-                                     : reinterpret_cast<uint32_t*>(&vbufs[(cs - 32) >> 3][0][8 * n + ((cs - 32) & 7)]) + pt;
-            const uint32_t xr = *px;
-            const uint32_t y = conv2(tp, rawc[d][tid], rawc[d + 1][tid], rawc[d + 2][tid], xr);
+            const int nn = n + 1 < kTile ? n + 1 : n;
+            const int dn = __builtin_amdgcn_readlane(li.dep, nn);
+            const uint32_t v0 = rawc[dn][tid], v1 = rawc[dn + 1][tid], v2 = rawc[dn + 2][tid];
+            const uint32_t xn = *px(nn);
+            const uint32_t y = conv2(tp, w0, w1, w2, xr);
             rawc[d + 3][tid] = xr;
-            *px = y;
-            if (cs < 16) kcache[d][tid] = y;
+            *px(n) = y;
+            if constexpr (R == 0) kcache[d][tid] = y;
+            w0 = v0;
+            w1 = v1;
+            w2 = dn == d + 1 ? xr : v2;
+            xr = xn;
+            d = dn;
         }
+    };
+    auto conv_walk = [&](const Taps& tp, const LaneInfo<D>& li) {
+        const int role = __builtin_amdgcn_readfirstlane(tid >> 6);
+        if (role == 0) conv_walk_role(tp, li, RoleTag<0>{});
+        else if (role == 1) conv_walk_role(tp, li, RoleTag<1>{});
+        else conv_walk_role(tp, li, RoleTag<2>{});
     };
     // the root-path caches at the start of the walk: the history, and keys and
     // path-stack rows cleared (finite; rows past a node's depth are masked, not skipped)
