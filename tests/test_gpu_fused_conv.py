@@ -9,8 +9,9 @@ published history are compared for an iteration that publishes the previous one'
 accepted paths (a 20-node path staged in two rounds, a path into a request with no
 nodes in this tree, an empty and an invalid path), and over two iterations of the
 benchmark's serving loop (nothing pending, then the first iteration's paths) on the
-full batched workload and a 16-level one (chainmix); also with operand preparation,
-and against the oracle directly (conv then verification) on the one-layer workload.
+full batched workload and a 16-level one (chainmix); also with operand preparation, with a
+conv bias with and without the SiLU, and against the oracle directly (conv then
+verification) on the one-layer workload.
 """
 from __future__ import annotations
 
@@ -39,12 +40,12 @@ def say(*a):
     sys.stdout.flush()
 
 
-def _step(wl, arrays=None, prep=None):
+def _step(wl, arrays=None, prep=None, act=1):
     a = dict(wl.arrays if arrays is None else arrays)
     return GdnTreeStep(n_req=wl.n_req, n_layers=wl.n_layers, h_k=wl.h_k, h_v=wl.h_v, d_k=wl.d_k,
                        d_v=wl.d_v, op_dtype=wl.op_dtype, node_off=wl.node_off, parent=wl.parent_flat,
                        n_rows=wl.n_rows, arrays=a, policy=L.LUMO_POLICY_WY, max_path=wl.max_path,
-                       accepted=wl.accepted, channels=wl.channels, prep=prep)
+                       accepted=wl.accepted, channels=wl.channels, prep=prep, act=act)
 
 
 def _split(st):
@@ -87,14 +88,14 @@ def _pair(h_k=2, h_v=4, seed=41):
     return prev, cur
 
 
-def _two_iterations(prev, cur, prep=None):
+def _two_iterations(prev, cur, prep=None, act=1):
     """(fused, unfused) results of the second iteration: cur publishing prev's accepted
     paths (prev itself is only planned and its paths derived: its 20-node chain is beyond
     the WY form). Each side carries its own history and state bank."""
     out = {}
     for side in ("fused", "split"):
-        sp = _step(prev, prep=prep)
-        sc = _step(cur, prep=prep)
+        sp = _step(prev, prep=prep, act=act)
+        sc = _step(cur, prep=prep, act=act)
         sc.hist = sp.hist  # one history and one state bank across the iterations
         sp.commit(defer=True, with_conv=False)  # derives the accepted paths only
         if side == "fused":
@@ -145,6 +146,34 @@ def test_fused_with_operand_preparation():
     say("[gpu] fused conv pending, prepared operands")
     fused, split = _two_iterations(prev, cur, prep)
     _assert_equal(fused, split, "prep")
+
+
+@pytest.mark.parametrize("act", [0, 1])
+def test_fused_with_bias_and_activation(act):
+    """A conv bias (per layer and channel, shared by the iterations) with and without the
+    SiLU: the fused walk and the pending path's conv add the bias first and apply the
+    activation only when asked, as the conv kernels do."""
+    prev, cur = _pair(seed=67)
+    rng = np.random.default_rng(67 + act)
+    C = prev.channels
+    bias = (0.5 * rng.standard_normal((2, C))).astype(np.float32)
+    prev.arrays["bias"] = bias
+    cur.arrays["bias"] = bias
+    a_log = torch.from_numpy((0.5 * rng.standard_normal((2, 4))).astype(np.float32)).cuda()
+    dt_bias = torch.from_numpy(rng.standard_normal((2, 4)).astype(np.float32)).cuda()
+    prep = L.Prep(L.LUMO_PREP_QK_NORM | L.LUMO_PREP_RAW_GATES, 1e-6, a_log, dt_bias)
+    say(f"[gpu] fused conv pending, bias, act={act}")
+    fused, split = _two_iterations(prev, cur, prep, act=act)
+    _assert_equal(fused, split, f"bias act={act}")
+    # the bias and the activation are observable: without them the outputs differ
+    if act == 1:
+        prev.arrays["bias"] = None
+        cur.arrays["bias"] = None
+        plain, _ = _two_iterations(prev, cur, prep, act=act)
+        assert not torch.equal(plain["o"].view(torch.int16), fused["o"].view(torch.int16))
+    else:
+        silu, _ = _two_iterations(prev, cur, prep, act=1)
+        assert not torch.equal(silu["o"].view(torch.int16), fused["o"].view(torch.int16))
 
 
 @pytest.mark.parametrize("name", ["batched", "chainmix"])

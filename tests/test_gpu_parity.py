@@ -534,12 +534,13 @@ def lumo_commit_into(st, bank):
 
 # ---------------------------------------------------------------- tree convolution shapes
 
-@pytest.mark.parametrize("case", ["depth_first", "runs_deep", "runs_few_blocks"])
-def test_conv_tree_shapes(case):
+@pytest.mark.parametrize("case,act", [("depth_first", 1), ("runs_deep", 1), ("runs_few_blocks", 1),
+                                      ("depth_first", 0), ("runs_deep", 0)])
+def test_conv_tree_shapes(case, act):
     """Both conv kernels on edge shapes: paths of 16 nodes (the depth-first kernel's limit)
-    or 20 (run kernel), a request without nodes, a partial channel block, bias. The
-    depth-first kernel is used when it has at least 1024 blocks (requests x layers x
-    channel blocks): 4 x 52 x 5 here."""
+    or 20 (run kernel), a request without nodes, a partial channel block, bias; with the
+    SiLU and without an activation (act = 0). The depth-first kernel is used when it has
+    at least 1024 blocks (requests x layers x channel blocks): 4 x 52 x 5 here."""
     rng = np.random.default_rng(41)
     deep = case == "runs_deep"
     n_layers, C = (52, 8200) if case == "depth_first" else (2, 2056)
@@ -551,7 +552,7 @@ def test_conv_tree_shapes(case):
     wl.arrays = ops.make_conv_operands(43, n_req=4, n_layers=n_layers, total_rows=wl.total_rows,
                                        channels=C, op_dtype=ops.BF16)
     bias = rng.standard_normal((n_layers, C)).astype(np.float32)
-    say(f"[gpu] conv shapes {case}")
+    say(f"[gpu] conv shapes {case} act={act}")
     desc = L.TreeDesc.build(wl.node_off, wl.parent_flat, wl.n_rows)
     d = L.dims(4, n_layers, 1, 1, 128, 128, L.LUMO_BF16)
     x = torch.from_numpy(wl.arrays["x"]).view(torch.bfloat16).cuda()
@@ -559,10 +560,10 @@ def test_conv_tree_shapes(case):
     w = torch.from_numpy(wl.arrays["w"]).cuda()
     b = torch.from_numpy(bias).cuda()
     y = torch.zeros((n_layers, wl.total_rows, C), dtype=torch.bfloat16, device="cuda")
-    L.lumo_tree_conv_gather(d, desc, C, x, hist, w, b, 1, y)
+    L.lumo_tree_conv_gather(d, desc, C, x, hist, w, b, act, y)
     torch.cuda.synchronize()
     got = gu.to_np(y)
-    ref = oracle.conv_all(wl, bias=bias)
+    ref = oracle.conv_all(wl, bias=bias, act=act)
     rows = oracle.plan.flat_rows(wl.parents, wl.row_off)
     assert gu.max_rel(got[:, rows], ref[:, rows]) <= gu.TOL_BF16
     pad = [r for r in range(wl.total_rows) if r not in set(rows.tolist())]
