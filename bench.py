@@ -404,12 +404,19 @@ def cpu_baseline(wl, budget_s=12.0):
             "host": host_cpu()}
 
 
+def per_layer_launches(args, n_layers):
+    """Library calls per per-layer step: conv and verify per layer (one fused call with
+    --fused), and the path derivation."""
+    return (1 if args.fused else 2) * n_layers + 1
+
+
 def per_layer_graph_ms(args, st, stream):
     """The step as the paper's per-layer structure runs it: for every layer its own conv
     and verify calls (n_layers = 1), each layer with its own state bank
     [req][1][h_v][d_k][d_v] and conv history [req][1][3][C], the per-node tensors sliced
-    by layer, and one path derivation shared by all layers; ten steps captured in one
-    graph and replayed. Returns ms per step."""
+    by layer, and one path derivation shared by all layers; with --fused one call per
+    layer does the conv and the verification. Ten steps are captured in one graph and
+    replayed. Returns ms per step."""
     import torch
 
     import paper_2609_23900_amd as L
@@ -420,12 +427,20 @@ def per_layer_graph_ms(args, st, stream):
     states = [st.state[:, l:l + 1].contiguous() for l in range(nl)]
     hists = [st.hist[:, l:l + 1].contiguous() for l in range(nl)]
 
+    bias = [None] * nl if st.bias is None else [st.bias[l] for l in range(nl)]
+
     def one_step():
         for l in range(nl):
             x, y, w = st.x[l], st.y[l], st.w[l]
-            L.lumo_tree_conv_gather_pending(d1, st.desc, st.channels, x, hists[l], w, None, st.act, y, st.desc,
+            g, b = st.t["g"][l], st.t["beta"][l]
+            if args.fused:  # conv, publications and verification of the layer in one call
+                L.lumo_tree_gdn_verify_conv_pending(d1, st.desc, st.channels, x, hists[l], w, bias[l], st.act, g, b,
+                                                    states[l], st.o[l], st.desc, st.max_path, st.path_out,
+                                                    st.path_len, x, g, b, None, st.prep)
+                continue
+            L.lumo_tree_conv_gather_pending(d1, st.desc, st.channels, x, hists[l], w, bias[l], st.act, y, st.desc,
                                             st.max_path, st.path_out, st.path_len, x, None)
-            q, k, v, g, b = (st.t[key][l] for key in ("q", "k", "v", "g", "beta"))
+            q, k, v = (st.t[key][l] for key in ("q", "k", "v"))
             L.lumo_tree_gdn_verify_pending(d1, st.desc, q, k, v, g, b, states[l], st.o[l], st.desc, st.max_path,
                                            st.path_out, st.path_len, k, v, g, b, None, st.prep)
         st.commit(None, defer=True, with_conv=False)
@@ -451,7 +466,7 @@ def per_layer_graph_ms(args, st, stream):
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / (reps * per)
-    log(f"[bench] per-layer graph-replayed step {ms:.4f} ms ({2 * nl + 1} launches per step)")
+    log(f"[bench] per-layer graph-replayed step {ms:.4f} ms ({per_layer_launches(args, nl)} launches per step)")
     del g
     return ms
 
@@ -639,7 +654,7 @@ def main():
             sys.exit("--per-layer needs the wy policy and the deferred commit")
         pl_ms = per_layer_graph_ms(args, st, stream)
         kernels["per_layer_graph_step_ms"] = round(pl_ms, 4)
-        kernels["per_layer_launches_per_step"] = 2 * wl.n_layers + 1
+        kernels["per_layer_launches_per_step"] = per_layer_launches(args, wl.n_layers)
     if not deferred:
         kernels["commit_hbm_frac"] = round(ab["commit_bytes"] / (com_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
     out = {
