@@ -213,7 +213,7 @@ extern "C" lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lum
     } else {
         e = launch_scan(*dims, *desc, a, static_cast<hipStream_t>(stream));
     }
-    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: policy %d not available in this build", fn, policy);
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: policy %d not compiled into the library", fn, policy);
     if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return LUMO_OK;
 }
@@ -239,7 +239,7 @@ extern "C" lumo_status lumo_tree_gdn_verify_prep(const lumo_gdn_dims* dims, cons
     LUMO_TRY(check_ptr(o, fn, "o"));
     GdnArgs a{q, k, v, g, beta, state0, o, nullptr, nullptr, pr};
     hipError_t e = launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream));
-    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not available in this build", fn);
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not compiled into the library", fn);
     if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return LUMO_OK;
 }
@@ -283,7 +283,7 @@ extern "C" lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, c
     GdnArgs a{q, k, v, g, beta, state, o, nullptr, nullptr, pr};
     PendArgs pa{pend_desc, max_path, path_out, path_len, pend_k, pend_v, pend_g, pend_beta, state};
     hipError_t e = launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream), &pa);
-    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not available in this build", fn);
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not compiled into the library", fn);
     if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return LUMO_OK;
 }
@@ -480,7 +480,7 @@ extern "C" lumo_status lumo_tree_attention(const lumo_attn_dims* dims, const lum
     if (workspace_bytes < need) return fail(LUMO_ESPACE, "%s: workspace needs %zu bytes, got %zu", fn, need, workspace_bytes);
     AttnArgs a{ctx_off, max_ctx, n_split, scale, q, k_ctx, v_ctx, k_tree, v_tree, o, lse, static_cast<float*>(workspace)};
     hipError_t e = launch_attention(*dims, *desc, a, static_cast<hipStream_t>(stream));
-    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not available in this build", fn);
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not compiled into the library", fn);
     if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return LUMO_OK;
 }
@@ -533,7 +533,7 @@ extern "C" lumo_status lumo_draft_select(int32_t rows, int32_t vocab, int64_t ld
     }
     SelectArgs a{logits, rows, vocab, (long)ld, dtype, k, ties, n_split, spine, cand, parts};
     hipError_t e = launch_select(a, static_cast<hipStream_t>(stream));
-    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not available in this build", fn);
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not compiled into the library", fn);
     if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return LUMO_OK;
 }
