@@ -288,7 +288,8 @@ def select_bench(args):
     out = {"metric": "draft selection logits rows/sec + % of HBM roofline, 1 MI355X",
            "value": main["rows_per_s"], "unit": "logits rows/s", "n_gpus": 1, "steps": main["calls_timed"],
            "warmup": args.warmup, "ms_per_step": round(main["us_per_call"] / 1e3, 6),
-           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": f"{main['dtype']} logits, exact ordering on 64-bit integer ranking words",
            "data": "synthetic (N(0, 9) logits)",
            "config": {"workload": f"draft selection: 8 rows x {SEL_VOCAB:,} float32 logits, argmax + ordered "
                                   "top-3 (ties: higher index first), graph-replayed, 508 MB of logits cycled",
@@ -469,6 +470,19 @@ def per_layer_graph_ms(args, st, stream):
     log(f"[bench] per-layer graph-replayed step {ms:.4f} ms ({per_layer_launches(args, nl)} launches per step)")
     del g
     return ms
+
+
+def arithmetic_label(wl, policy, args):
+    """What the timed path computes in: operand and output type, state type, and where
+    the O(d^2) products run."""
+    import paper_2609_23900_amd as L
+    ops_t = "bf16" if wl.op_dtype == 1 else "f32"
+    if policy == L.LUMO_POLICY_WY:
+        core = "R0.[K|Q] on bf16 MFMA with R0 split into bf16 hi+lo (16 significant bits), f32 accumulate"
+        if args.fused:
+            core = "tree conv in f32 (one bf16 cast); " + core
+        return f"{ops_t} operands/outputs, f32 state and recurrence; {core}"
+    return f"{ops_t} operands/outputs, f32 state; f32 VALU recurrence"
 
 
 def main():
@@ -660,7 +674,8 @@ def main():
     out = {
         "metric": METRIC, "value": round(hn / (ms_step * 1e-3), 1), "unit": "head-node updates/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": arithmetic_label(wl, policy, args),
         "data": "synthetic (seeded trees and operands shaped like the paper's workloads)",
         "config": {"workload": f"{args.config}: {WORKLOAD_TEXT[args.config]}",
                    "policy": args.policy, "commit": mode, "conv": "fused into verify" if args.fused else "separate",

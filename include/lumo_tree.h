@@ -400,7 +400,6 @@ lumo_status lumo_gdn_commit_prep(const lumo_gdn_dims* dims, const lumo_tree_desc
                                  const float* beta, float* state, int32_t channels,
                                  const void* x, void* conv_hist, void* stream);
 
-/* Opaque captured commit (Sec. V-A: one fixed-shape committer graph). */
 /*
  * Tree attention (Sec. V-B; visibility Sec. III-A): the attention layers' verification
  * of the same candidate tree. Query row i (a tree node) attends to its request's
@@ -473,13 +472,19 @@ lumo_status lumo_draft_select(int32_t rows, int32_t vocab, int64_t ld, int32_t d
                               int32_t n_split, void* workspace, size_t workspace_bytes,
                               void* stream);
 
+/* Opaque captured commit: the fixed-shape committer graph of Sec. V-A. */
 typedef struct lumo_commit_graph lumo_commit_graph;
 
 /*
- * lumo_gdn_commit_graph_create - capture the launches of lumo_gdn_commit with
- * these exact arguments into an instantiated HIP graph. Device buffers are bound
- * by address: replays read the current contents of accepted_node (and every
- * operand) at launch time. The caller keeps all buffers alive until destroy.
+ * lumo_gdn_commit_graph_create - the fixed-shape committer of Sec. V-A (Alg. 1
+ * publication): capture the launches of lumo_gdn_commit with these exact arguments
+ * into an instantiated HIP graph, so that one replay per serving iteration derives the
+ * device-selected path, replays it into the native state and publishes the conv
+ * history with no host path list. The work shape depends only on max_path. Device
+ * buffers are bound by address: replays read the current contents of accepted_node
+ * (and every operand) at launch time. The caller keeps all buffers alive until
+ * destroy. Errors: the validation of lumo_gdn_commit, before any capture; LUMO_EHIP
+ * when capture or instantiation fails (nothing is left captured).
  */
 lumo_status lumo_gdn_commit_graph_create(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
                                          int32_t max_path, const int32_t* accepted_node,
@@ -488,7 +493,8 @@ lumo_status lumo_gdn_commit_graph_create(const lumo_gdn_dims* dims, const lumo_t
                                          float* state, int32_t channels, const void* x,
                                          void* conv_hist, lumo_commit_graph** out);
 
-/* Replay the captured commit on `stream`. */
+/* Replay the captured commit (Sec. V-A) on `stream`; LUMO_EINVAL for a NULL graph,
+ * LUMO_EHIP when the launch fails. */
 lumo_status lumo_gdn_commit_graph_launch(lumo_commit_graph* graph, void* stream);
 
 /* Release the graph (NULL is ignored). */

@@ -268,8 +268,12 @@ int orc_verify_all(const orc_dims* d, const int* node_off, const int* parent, co
  * Accepted-path replay (Alg. 1 publication, Alg. 2 replay) for all instances.
  *   accepted[n_req]: request-local accepted node, -1 = none (empty replay).
  *   path_out[n_req][max_path]: root-first node ids padded with -1; path_len[n_req].
+ *   An accepted node outside [-1, nodes of r), or a path longer than max_path, is a
+ *   selection that names no publishable path: path_len[r] = -1, path_out[r] all -1,
+ *   and request r's state is published unchanged (the paper publishes only a path it
+ *   accepted; the report of -1 is this interface's convention).
  *   state_in: pre-tree state; state_out: published state (fp64, same layout).
- * Returns 0, or -1 when a path is malformed or longer than max_path.
+ * Returns 0, or -1 when a parent array is malformed.
  */
 int orc_commit(const orc_dims* d, const int* node_off, const int* parent, const int* row,
                const int* accepted, int max_path, const void* k, const void* v, const float* g,
@@ -281,13 +285,21 @@ int orc_commit(const orc_dims* d, const int* node_off, const int* parent, const 
         int* po = path_out + (long)r * max_path;
         for (int p = 0; p < max_path; ++p) po[p] = -1;
         path_len[r] = 0;
-        if (accepted[r] < 0) continue;
-        if (accepted[r] >= n) return -1;
+        if (accepted[r] == -1) continue;
+        if (accepted[r] < -1 || accepted[r] >= n) {
+            path_len[r] = -1;
+            continue;
+        }
         int* tmp = (int*)malloc(sizeof(int) * (size_t)(n > 0 ? n : 1));
         const int len = ancestry(parent + node_off[r], n, accepted[r], tmp, n);
-        if (len < 0 || len > max_path) {
+        if (len < 0) {
             free(tmp);
             return -1;
+        }
+        if (len > max_path) {
+            path_len[r] = -1;
+            free(tmp);
+            continue;
         }
         for (int p = 0; p < len; ++p) po[p] = tmp[p];
         path_len[r] = len;

@@ -118,12 +118,17 @@ def conv_sources(parent, row) -> list:
 
 
 def accepted_path(parent, accepted, max_path) -> tuple:
-    """(root-first path padded with -1 to max_path, length)."""
-    if accepted < 0:
+    """(root-first path padded with -1 to max_path, length).
+
+    -1 accepts nothing (length 0). A node outside the tree, or a path longer than
+    max_path, names no publishable path: all -1 with length -1."""
+    if accepted == -1:
         return [-1] * max_path, 0
+    if not 0 <= accepted < len(parent):
+        return [-1] * max_path, -1
     p = ancestry(parent, accepted)
     if len(p) > max_path:
-        raise ValueError("accepted path longer than max_path")
+        return [-1] * max_path, -1
     return p + [-1] * (max_path - len(p)), len(p)
 
 

@@ -372,6 +372,158 @@ def pin_fig1_worked_commit():
     np.testing.assert_allclose(st[0, 0, 0], states[-1], rtol=1e-12, atol=1e-13)
 
 
+# --------------------------------------------------------------------------- batch drivers
+
+def _batch_wl(rng, n_layers=2, h_k=2, h_v=4, d_k=5, d_v=3, channels=3):
+    """Three requests laid out as the boundary lays them out: a random tree with two pad
+    rows, a request without nodes (two pad rows), and the Fig. 1 tree with two pad
+    rows, so that a node's physical row differs from its id and from its position in
+    the flat node list, and each request's rows start at its own offset."""
+    parents = [trees.random_tree(rng, 11, 5, trees.bmax_uniform(3)), np.zeros(0, np.int32),
+               trees.FIG1_PARENT.copy()]
+    wl = make_wl(parents, d_k=d_k, d_v=d_v, h_k=h_k, h_v=h_v, n_layers=n_layers,
+                 n_rows=[13, 2, 9], channels=channels, max_path=6)
+    return wl
+
+
+def _hand_rows(parents, n_rows):
+    """Physical rows written out from the layout rule (spine first by depth, then the
+    other nodes in id order) and the per-request row offsets, without the planner."""
+    out, base = [], 0
+    for par, nr in zip(parents, n_rows):
+        n = len(par)
+        spine = []
+        if n:
+            spine = [0]
+            while True:
+                kids = [i for i in range(n) if par[i] == spine[-1]]
+                if not kids:
+                    break
+                spine.append(min(kids))
+        order = spine + [i for i in range(n) if i not in spine]
+        slot = [0] * n
+        for pos, node in enumerate(order):
+            slot[node] = pos
+        out.append([base + slot[i] for i in range(n)])
+        base += nr
+    return out
+
+
+def pin_verify_all_batch_layout():
+    """Every (request, layer, value head) instance of a padded three-request batch, one
+    request without nodes: each node's output sits at its own physical row and equals
+    the WY closed form of its request's tree; pad rows stay unwritten."""
+    rng = np.random.default_rng(51)
+    wl = _batch_wl(rng)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    o = oracle.verify_all(wl, n_threads=2)
+    rows = _hand_rows(wl.parents, wl.n_rows)
+    written = np.zeros((wl.n_layers, wl.total_rows, wl.h_v), bool)
+    for r in (0, 2):
+        for l in range(wl.n_layers):
+            for h in range(wl.h_v):
+                al, be, K, Q, V = _node_operands(wl, a, r, l, h)
+                want = tree_wy_form(wl.parents[r], a["state0"][r, l, h], al, be, K, V, Q)
+                for i, rw in enumerate(rows[r]):
+                    np.testing.assert_allclose(o[l, rw, h], want[i], rtol=1e-11, atol=1e-12)
+                    written[l, rw, h] = True
+    assert np.all(np.isnan(o[~written])), "pad rows or the empty request were written"
+
+
+def pin_commit_batch_layout():
+    """Per request of the padded batch, the published state of every (layer, head) is
+    the chain scan of that request's own accepted path; the request without nodes and an
+    invalid selection publish the state unchanged; path_out / path_len are the
+    hand-derived ancestries (-1 for a selection outside the tree)."""
+    rng = np.random.default_rng(52)
+    wl = _batch_wl(rng)
+    a = random_arrays(wl, rng)
+    wl.arrays = a
+    par0 = wl.parents[0]
+    deep = int(np.argmax(trees.depths(par0)))
+    want_path0 = []
+    x = deep
+    while x != -1:
+        want_path0.insert(0, x)
+        x = int(par0[x])
+    for acc, want2, want_len2 in (([deep, -1, 6], [0, 1, 3, 6], 4), ([deep, -1, 7], [], -1),
+                                  ([deep, -1, -2], [], -1), ([deep, -1, 2], [0, 2], 2)):
+        st, po, pl = oracle.commit(wl, accepted=np.array(acc, np.int32), max_path=6, n_threads=2)
+        assert pl.tolist() == [len(want_path0), 0, want_len2]
+        assert po[0].tolist() == want_path0 + [-1] * (6 - len(want_path0))
+        assert po[1].tolist() == [-1] * 6
+        assert po[2].tolist() == want2 + [-1] * (6 - len(want2))
+        for l in range(wl.n_layers):
+            for h in range(wl.h_v):
+                assert np.array_equal(st[1, l, h], a["state0"][1, l, h].astype(np.float64))
+                for r, path in ((0, want_path0), (2, want2)):
+                    if not path:
+                        assert np.array_equal(st[r, l, h], a["state0"][r, l, h].astype(np.float64))
+                        continue
+                    al, be, K, Q, V = _node_operands(wl, a, r, l, h)
+                    _, states = chain_matrix_form(a["state0"][r, l, h], [al[x] for x in path],
+                                                  [be[x] for x in path], K[path], V[path], Q[path])
+                    np.testing.assert_allclose(st[r, l, h], states[-1], rtol=1e-12, atol=1e-13)
+
+
+def _batch_conv_arrays(wl, rng):
+    return dict(x=rng.standard_normal((wl.n_layers, wl.total_rows, wl.channels)).astype(np.float32),
+                hist=rng.standard_normal((wl.n_req, wl.n_layers, 3, wl.channels)).astype(np.float32),
+                w=rng.uniform(-0.5, 0.5, (wl.n_layers, wl.channels, 4)).astype(np.float32))
+
+
+def pin_conv_batch_layout():
+    """Tree conv over the padded batch: each node's output at its physical row equals
+    numpy.convolve over its own request's history followed by its ancestry's x rows;
+    pad rows stay unwritten."""
+    rng = np.random.default_rng(53)
+    wl = _batch_wl(rng)
+    wl.arrays = _batch_conv_arrays(wl, rng)
+    bias = rng.standard_normal((wl.n_layers, wl.channels)).astype(np.float32)
+    y = oracle.conv_all(wl, bias=bias, act=0)
+    rows = _hand_rows(wl.parents, wl.n_rows)
+    written = np.zeros((wl.n_layers, wl.total_rows), bool)
+    x, hist, w = wl.arrays["x"], wl.arrays["hist"], wl.arrays["w"]
+    for r in (0, 2):
+        par = wl.parents[r]
+        for i, rw in enumerate(rows[r]):
+            anc = []
+            n_ = i
+            while n_ != -1:
+                anc.insert(0, n_)
+                n_ = int(par[n_])
+            for l in range(wl.n_layers):
+                for c in range(wl.channels):
+                    seq = np.concatenate([hist[r, l, :, c], x[l, [rows[r][m] for m in anc], c]]).astype(np.float64)
+                    full = np.convolve(seq, w[l, c].astype(np.float64)[::-1], mode="full")
+                    np.testing.assert_allclose(y[l, rw, c], full[len(seq) - 1] + bias[l, c],
+                                               rtol=1e-13, atol=1e-14)
+                written[l, rw] = True
+    assert np.all(np.isnan(y[~written]))
+
+
+def pin_conv_hist_publish_batch_layout():
+    """History publication over the padded batch: request r's new history is the last
+    three of (its own old history, the x rows of its own path); a request with an empty
+    or invalid path keeps its history."""
+    rng = np.random.default_rng(54)
+    wl = _batch_wl(rng)
+    wl.arrays = _batch_conv_arrays(wl, rng)
+    rows = _hand_rows(wl.parents, wl.n_rows)
+    x, hist = wl.arrays["x"], wl.arrays["hist"]
+    for paths in (([0, 2], [], [0, 1, 3, 6]), ([0], [], [0, 2, 5]), ([], [], [0])):
+        po = np.full((3, 6), -1, np.int32)
+        pl = np.array([len(p) for p in paths], np.int32)
+        for r, p in enumerate(paths):
+            po[r, :len(p)] = p
+        out = oracle.conv_hist_publish(wl, po, pl)
+        for r, p in enumerate(paths):
+            for l in range(wl.n_layers):
+                seq = list(hist[r, l]) + [x[l, rows[r][m]] for m in p]
+                assert np.array_equal(out[r, l], np.array(seq[-3:], np.float64)), (r, l, p)
+
+
 # --------------------------------------------------------------------------- convolution
 
 def _conv_wl(par, C=5, n_layers=1):

@@ -203,10 +203,11 @@ def test_accepted_edge_cases():
         torch.cuda.synchronize()
         pl = int(st.path_len.cpu()[0])
         po = st.path_out.cpu().numpy()[0]
-        if want_len is None:
-            path, L_ = oracle.plan.accepted_path(wl.parents[0], acc, 12)
-            assert pl == L_ and list(po) == path
-        else:
+        # the descriptor products equal the oracle's bit for bit, invalid selections included
+        path, L_ = oracle.plan.accepted_path(wl.parents[0], acc, 12)
+        _, opo, opl = oracle.commit(wl, accepted=np.array([acc], np.int32), max_path=12)
+        assert pl == L_ == int(opl[0]) and list(po) == path == opo[0].tolist()
+        if want_len is not None:
             assert pl == want_len
         if pl <= 0:
             assert np.all(po == -1)
@@ -221,6 +222,9 @@ def test_accepted_edge_cases():
     st.commit()
     torch.cuda.synchronize()
     assert int(st.path_len.cpu()[0]) == -1 and torch.equal(st.state, st.state0)
+    ost, opo, opl = oracle.commit(wl, accepted=np.array([deep], np.int32), max_path=4)
+    assert int(opl[0]) == -1 and st.path_out.cpu().numpy().tolist() == opo.tolist()
+    assert np.array_equal(ost, wl.arrays["state0"].astype(np.float64))
 
 
 def test_empty_batch_and_root_only_requests():

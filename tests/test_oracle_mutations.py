@@ -61,6 +61,24 @@ MUTATIONS = {
     "select_repeats_candidates": ("                if (taken) continue;\n", ""),
     "select_spine_skips_index_1": ("for (int i = 1; i < vocab; ++i)\n            if (sel_greater(",
                                    "for (int i = 2; i < vocab; ++i)\n            if (sel_greater("),
+    # batch drivers: per-request offsets and per-instance indices
+    "verify_all_output_at_node_id": ("double* dst = o_all + (((long)l * d->total_rows + rw[i]) * d->h_v + h) * d->d_v;",
+                                     "double* dst = o_all + (((long)l * d->total_rows + i) * d->h_v + h) * d->d_v;"),
+    "verify_all_layer_from_head": ("const int l = (int)((inst / d->h_v) % d->n_layers);\n        const int r = (int)(inst / ((long)d->h_v * d->n_layers));\n        const int n = node_off[r + 1] - node_off[r];",
+                                   "const int l = (int)(inst % d->n_layers);\n        const int r = (int)(inst / ((long)d->h_v * d->n_layers));\n        const int n = node_off[r + 1] - node_off[r];"),
+    "commit_rows_of_request0": ("const int* rw = row + node_off[r];\n        load_state(d, state_in",
+                                "const int* rw = row;\n        load_state(d, state_in"),
+    "commit_state_of_request0": ("load_state(d, state_in, r, l, h, s.R);", "load_state(d, state_in, 0, l, h, s.R);"),
+    "commit_invalid_reports_zero": ("path_len[r] = -1;\n            continue;\n        }\n        int* tmp",
+                                    "path_len[r] = 0;\n            continue;\n        }\n        int* tmp"),
+    "conv_history_of_request0": ("xv = ld_op(hist, (((long)r * n_layers + l) * 3 + pos) * channels + c, op_dtype);",
+                                 "xv = ld_op(hist, (((long)0 * n_layers + l) * 3 + pos) * channels + c, op_dtype);"),
+    "conv_rows_of_request0": ("const int* rw = row + node_off[r];\n        int* path = (int*)malloc(sizeof(int) * (size_t)(n > 0 ? n : 1));",
+                              "const int* rw = row;\n        int* path = (int*)malloc(sizeof(int) * (size_t)(n > 0 ? n : 1));"),
+    "hist_publish_rows_of_request0": ("const int* rw = row + node_off[r];\n        for (int l = 0; l < n_layers; ++l)",
+                                      "const int* rw = row;\n        for (int l = 0; l < n_layers; ++l)"),
+    "hist_publish_history_of_request0": ("val = ld_op(hist, (((long)r * n_layers + l) * 3 + pos) * channels + c, op_dtype);",
+                                         "val = ld_op(hist, (((long)0 * n_layers + l) * 3 + pos) * channels + c, op_dtype);"),
 }
 
 
