@@ -440,6 +440,27 @@ lumo_status lumo_tree_attention(const lumo_attn_dims* dims, const lumo_tree_desc
                                 void* stream);
 
 /*
+ * lumo_tree_attention_noalloc - lumo_tree_attention for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the partial results of the key ranges go to a fixed scratch array
+ * of LUMO_TREE_ATTENTION_SCRATCH_BYTES (32 MiB) that the library holds on each device it
+ * runs on until the process ends, instead of a caller workspace. Same arguments and
+ * results as lumo_tree_attention otherwise (bitwise, for the same n_split); it calls no
+ * allocating routine. LUMO_ESPACE, before any launch, when
+ * lumo_tree_attention_workspace_bytes(dims, plan, n_split) exceeds the array (at d =
+ * 128: (n_split + 1) x total_rows x h_q <= 65,027). Every call on one device shares
+ * that device's array: calls that overlap in time on one device (two streams, two
+ * threads) race and must be ordered by the caller. The first call on a device, with
+ * that device current, looks up the array's device address.
+ */
+#define LUMO_TREE_ATTENTION_SCRATCH_BYTES (32u << 20)
+lumo_status lumo_tree_attention_noalloc(const lumo_attn_dims* dims, const lumo_tree_desc* desc,
+                                        const int32_t* ctx_off, int32_t max_ctx, float scale,
+                                        const void* q, const void* k_ctx, const void* v_ctx,
+                                        const void* k_tree, const void* v_tree, void* o, float* lse,
+                                        int32_t n_split, void* stream);
+
+/*
  * Fused draft selection (Sec. V-D): from one full-vocabulary logits row per drafting
  * position, the principal (spine) token and k ordered sibling candidates in one pass.
  * The two reference operations break ties differently, and both are reproduced:

@@ -6,7 +6,8 @@ The functions keep the names of the C ABI (include/lumo_tree.h):
   lumo_tree_plan, lumo_tree_gdn_workspace_bytes, lumo_tree_conv_gather,
   lumo_tree_conv_gather_pending, lumo_tree_gdn_verify, lumo_tree_gdn_verify_prep, lumo_tree_gdn_verify_pending,
   lumo_tree_gdn_verify_conv_pending, lumo_gdn_commit,
-  lumo_gdn_commit_prep, lumo_tree_attention, lumo_tree_attention_workspace_bytes,
+  lumo_gdn_commit_prep, lumo_tree_attention, lumo_tree_attention_noalloc,
+  lumo_tree_attention_workspace_bytes,
   lumo_tree_attention_splits, lumo_draft_select, lumo_draft_select_workspace_bytes,
   lumo_draft_select_splits, lumo_gdn_commit_graph_create,
   lumo_gdn_commit_graph_launch, lumo_gdn_commit_graph_destroy, lumo_last_error,
@@ -110,6 +111,7 @@ def _load():
     L.lumo_tree_attention_splits.argtypes = [PA, ctypes.POINTER(lumo_plan), I32]
     L.lumo_tree_attention_splits.restype = I32
     L.lumo_tree_attention.argtypes = [PA, PT, P, I32, ctypes.c_float, P, P, P, P, P, P, P, I32, P, SZ, P]
+    L.lumo_tree_attention_noalloc.argtypes = [PA, PT, P, I32, ctypes.c_float, P, P, P, P, P, P, P, I32, P]
     L.lumo_draft_select_workspace_bytes.argtypes = [I32, I32, I32]
     L.lumo_draft_select_workspace_bytes.restype = SZ
     L.lumo_draft_select_splits.argtypes = [I32, I32, I32]
@@ -131,7 +133,7 @@ def _load():
     L.lumo_version.restype = ctypes.c_char_p
     for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_conv_gather_pending", "lumo_tree_gdn_verify",
               "lumo_tree_gdn_verify_prep", "lumo_tree_gdn_verify_pending", "lumo_tree_gdn_verify_conv_pending", "lumo_gdn_commit",
-              "lumo_gdn_commit_prep", "lumo_tree_attention", "lumo_draft_select", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
+              "lumo_gdn_commit_prep", "lumo_tree_attention", "lumo_tree_attention_noalloc", "lumo_draft_select", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -309,6 +311,18 @@ def lumo_tree_attention(d, desc: TreeDesc, ctx_off, max_ctx, scale, q, k_ctx, v_
                                     int(max_ctx), float(scale), _dptr(q), _dptr(k_ctx), _dptr(v_ctx),
                                     _dptr(k_tree), _dptr(v_tree), _dptr(o), _dptr(lse), int(n_split),
                                     _dptr(workspace), ws_bytes, _stream(stream)))
+
+
+# Bytes of the fixed per-device scratch array behind lumo_tree_attention_noalloc.
+LUMO_TREE_ATTENTION_SCRATCH_BYTES = 32 << 20
+
+
+def lumo_tree_attention_noalloc(d, desc: TreeDesc, ctx_off, max_ctx, scale, q, k_ctx, v_ctx, k_tree,
+                                v_tree, o, lse, n_split, stream=None):
+    _check(_lib.lumo_tree_attention_noalloc(ctypes.byref(d), ctypes.byref(desc.desc), _dptr(ctx_off),
+                                            int(max_ctx), float(scale), _dptr(q), _dptr(k_ctx),
+                                            _dptr(v_ctx), _dptr(k_tree), _dptr(v_tree), _dptr(o),
+                                            _dptr(lse), int(n_split), _stream(stream)))
 
 
 def _logits_dtype(t):

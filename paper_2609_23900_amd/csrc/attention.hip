@@ -19,6 +19,8 @@
 // LDS read (ds_read_b64_tr_b16: within 16 lanes, lane i receives element i % 4 of
 // lanes 4 e + i / 4, e = 0..3), so V never passes through registers. Tiles of 64 keys,
 // double-buffered.
+#include <mutex>
+
 #include "device_common.h"
 #include "internal.h"
 #include "launch.h"
@@ -327,7 +329,35 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p, uint16_
     if (lane == 0) lse[(long)row * p.h_q + h] = (mx + __log2f(ws)) * 0.69314718055994531f;
 }
 
+// Partial results of the key ranges for lumo_tree_attention_noalloc: one fixed array
+// per device, held until the process ends. Host code must not pass `scratch` itself
+// to a kernel (on the host it names a stand-in, not device memory); the device
+// address comes from attn_scratch() below.
+static __device__ __align__(256) float scratch[LUMO_TREE_ATTENTION_SCRATCH_BYTES / sizeof(float)];
+
 }  // namespace
+
+hipError_t attn_scratch(float** out) {
+    // one lookup per device, with that device current; the address is kept per device
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    *out = nullptr;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *out = static_cast<float*>(addr[dev]);
+    return hipSuccess;
+}
 
 int attn_part_len(int max_ctx, int n_split) {
     const int per = (max(max_ctx, 1) + n_split - 1) / n_split;

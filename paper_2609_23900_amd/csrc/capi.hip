@@ -485,6 +485,51 @@ extern "C" lumo_status lumo_tree_attention(const lumo_attn_dims* dims, const lum
     return LUMO_OK;
 }
 
+extern "C" lumo_status lumo_tree_attention_noalloc(const lumo_attn_dims* dims, const lumo_tree_desc* desc,
+                                                   const int32_t* ctx_off, int32_t max_ctx, float scale,
+                                                   const void* q, const void* k_ctx, const void* v_ctx,
+                                                   const void* k_tree, const void* v_tree, void* o, float* lse,
+                                                   int32_t n_split, void* stream) {
+    static const char* fn = "lumo_tree_attention_noalloc";
+    clear_error();
+    LUMO_TRY(check_attn_dims(dims, fn));
+    if (!desc) return fail(LUMO_EINVAL, "%s: desc is NULL", fn);
+    const lumo_plan& pl = desc->plan;
+    if (pl.n_req != dims->n_req) return fail(LUMO_EDESC, "%s: plan has %d requests, dims %d", fn, pl.n_req, dims->n_req);
+    if (!desc->blob) return fail(LUMO_EINVAL, "%s: desc blob is NULL", fn);
+    if (n_split < 1 || n_split > 4096) return fail(LUMO_EINVAL, "%s: n_split %d (1..4096)", fn, n_split);
+    if (max_ctx < 0) return fail(LUMO_EINVAL, "%s: max_ctx %d", fn, max_ctx);
+    if (!(scale > 0.f && scale < 3.0e38f)) return fail(LUMO_EINVAL, "%s: scale must be positive and finite", fn);
+    const size_t need = lumo_tree_attention_workspace_bytes(dims, &pl, n_split);
+    if (need > (size_t)LUMO_TREE_ATTENTION_SCRATCH_BYTES)
+        return fail(LUMO_ESPACE,
+                    "%s: the partial results need %zu bytes, more than the fixed %u-byte scratch array; "
+                    "use fewer splits (n_split %d) or lumo_tree_attention with a workspace",
+                    fn, need, (unsigned)LUMO_TREE_ATTENTION_SCRATCH_BYTES, n_split);
+    if (dims->n_req == 0 || pl.total_nodes == 0) return LUMO_OK;
+    LUMO_TRY(check_ptr(ctx_off, fn, "ctx_off"));
+    LUMO_TRY(check_ptr(q, fn, "q"));
+    LUMO_TRY(check_ptr(k_tree, fn, "k_tree"));
+    LUMO_TRY(check_ptr(v_tree, fn, "v_tree"));
+    LUMO_TRY(check_ptr(o, fn, "o"));
+    LUMO_TRY(check_ptr(lse, fn, "lse"));
+    if (max_ctx > 0) {
+        LUMO_TRY(check_ptr(k_ctx, fn, "k_ctx"));
+        LUMO_TRY(check_ptr(v_ctx, fn, "v_ctx"));
+    } else {
+        k_ctx = k_tree;  // never read: every context range is empty
+        v_ctx = v_tree;
+    }
+    float* ws = nullptr;
+    hipError_t e = attn_scratch(&ws);
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: scratch address lookup failed: %s", fn, hipGetErrorString(e));
+    AttnArgs a{ctx_off, max_ctx, n_split, scale, q, k_ctx, v_ctx, k_tree, v_tree, o, lse, ws};
+    e = launch_attention(*dims, *desc, a, static_cast<hipStream_t>(stream));
+    if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not compiled into the library", fn);
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
 extern "C" size_t lumo_draft_select_workspace_bytes(int32_t rows, int32_t k, int32_t n_split) {
     if (rows < 0 || k < 1 || n_split <= 1) return 0;
     return (size_t)rows * n_split * 4 * (k + 1) * sizeof(uint64_t);  // one entry per wavefront

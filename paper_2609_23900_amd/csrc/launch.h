@@ -127,5 +127,8 @@ struct AttnArgs {
 };
 int attn_part_len(int max_ctx, int n_split);
 hipError_t launch_attention(const lumo_attn_dims& d, const lumo_tree_desc& desc, const AttnArgs& a, hipStream_t s);
+// Device address of the current device's fixed attention scratch array
+// (LUMO_TREE_ATTENTION_SCRATCH_BYTES), looked up once per device.
+hipError_t attn_scratch(float** out);
 
 }  // namespace lumo

@@ -310,6 +310,25 @@ def test_attention_rejects_bad_arguments():
     assert 1 <= L.lumo_tree_attention_splits(ok, desc.plan, 131072) <= 512
 
 
+def test_attention_noalloc_refuses_on_the_host():
+    """The no-allocation form refuses partial results beyond its fixed array before any
+    device call (so this runs without a GPU), and validates like the workspace form."""
+    desc, _blob = _desc()
+    P = ctypes.c_void_p
+
+    def call(d, n_split, scale=0.1):
+        return L._lib.lumo_tree_attention_noalloc(ctypes.byref(d), ctypes.byref(desc), P(FAKE), 16, scale,
+                                                  P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+                                                  P(FAKE), n_split, None)
+    big = L.attn_dims(1, 8, 8)
+    assert L.lumo_tree_attention_workspace_bytes(big, desc.plan, 4096) > L.LUMO_TREE_ATTENTION_SCRATCH_BYTES
+    assert call(big, 4096) == L.LUMO_ESPACE
+    assert "scratch" in L.lumo_last_error()
+    assert call(L.attn_dims(1, 6, 2), 2) == L.LUMO_EUNSUPPORTED
+    assert call(L.attn_dims(1, 4, 2), 0) == L.LUMO_EINVAL
+    assert call(L.attn_dims(1, 4, 2), 2, scale=0.0) == L.LUMO_EINVAL
+
+
 def test_attention_empty_batch_is_a_no_op():
     plan, blob = L.lumo_tree_plan(np.array([0], np.int32), np.zeros(0, np.int32),
                                   np.zeros(0, np.int32), 0)
