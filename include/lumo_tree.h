@@ -280,9 +280,12 @@ lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lumo_tree_desc
 
 /*
  * lumo_tree_gdn_verify_prep - lumo_tree_gdn_verify with the operands prepared as
- * `prep` says (nullable). Needs a plan built for LUMO_POLICY_WY (bf16 operands,
- * d_k = d_v = 128, paths of at most 17 nodes), else LUMO_EUNSUPPORTED; no workspace,
- * no node-state dump.
+ * `prep` says (nullable; Sec. IV-B). Takes a plan built for LUMO_POLICY_WY (bf16
+ * operands, d_k = d_v = 128, paths of at most 17 nodes) or LUMO_POLICY_RECOMPUTE (the
+ * sequential scan of every path from the pre-tree state: any supported shape, either
+ * operand type, any depth; bitwise what lumo_gdn_commit_prep publishes for the same
+ * path); plans that export cut states to a workspace (PATHS, TWO_LEVEL) are refused
+ * with LUMO_EUNSUPPORTED, as this call takes no workspace. No node-state dump.
  */
 lumo_status lumo_tree_gdn_verify_prep(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
                                       const lumo_gdn_prep* prep, const void* q, const void* k,
@@ -501,14 +504,17 @@ typedef struct lumo_commit_graph lumo_commit_graph;
  * publication): capture the launches of lumo_gdn_commit with these exact arguments
  * into an instantiated HIP graph, so that one replay per serving iteration derives the
  * device-selected path, replays it into the native state and publishes the conv
- * history with no host path list. The work shape depends only on max_path. Device
- * buffers are bound by address: replays read the current contents of accepted_node
- * (and every operand) at launch time. The caller keeps all buffers alive until
+ * history with no host path list. The work shape depends only on max_path. `prep`
+ * (nullable) prepares the replayed operands as lumo_gdn_commit_prep does (Sec. IV-B:
+ * the recorded keys normalised, the gates from raw inputs); its a_log and dt_bias are
+ * bound by address too. Device buffers are bound by address: replays read the current
+ * contents of accepted_node (and every operand) at launch time. The caller keeps all buffers alive until
  * destroy. Errors: the validation of lumo_gdn_commit, before any capture; LUMO_EHIP
  * when capture or instantiation fails (nothing is left captured).
  */
 lumo_status lumo_gdn_commit_graph_create(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
-                                         int32_t max_path, const int32_t* accepted_node,
+                                         const lumo_gdn_prep* prep, int32_t max_path,
+                                         const int32_t* accepted_node,
                                          int32_t* path_out, int32_t* path_len, const void* k,
                                          const void* v, const float* g, const float* beta,
                                          float* state, int32_t channels, const void* x,

@@ -124,7 +124,7 @@ def _load():
                                                     P, P, P, P]
     L.lumo_gdn_commit_prep.argtypes = [PD, PT, PP, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
     L.lumo_gdn_commit.argtypes = [PD, PT, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
-    L.lumo_gdn_commit_graph_create.argtypes = [PD, PT, I32, P, P, P, P, P, P, P, P, I32, P, P,
+    L.lumo_gdn_commit_graph_create.argtypes = [PD, PT, PP, I32, P, P, P, P, P, P, P, P, I32, P, P,
                                                ctypes.POINTER(ctypes.c_void_p)]
     L.lumo_gdn_commit_graph_launch.argtypes = [P, P]
     L.lumo_gdn_commit_graph_destroy.argtypes = [P]
@@ -375,15 +375,15 @@ class CommitGraph:
 
 
 def lumo_gdn_commit_graph_create(d, desc: TreeDesc, max_path, accepted_node, path_out, path_len,
-                                 k, v, g, beta, state, channels=0, x=None, conv_hist=None):
+                                 k, v, g, beta, state, channels=0, x=None, conv_hist=None, prep=None):
     h = ctypes.c_void_p()
-    _check(_lib.lumo_gdn_commit_graph_create(ctypes.byref(d), ctypes.byref(desc.desc),
+    _check(_lib.lumo_gdn_commit_graph_create(ctypes.byref(d), ctypes.byref(desc.desc), _prep_ptr(prep),
                                              int(max_path), _dptr(accepted_node), _dptr(path_out),
                                              _dptr(path_len), _dptr(k), _dptr(v), _dptr(g),
                                              _dptr(beta), _dptr(state), int(channels), _dptr(x),
                                              _dptr(conv_hist), ctypes.byref(h)))
     return CommitGraph(h, (desc, accepted_node, path_out, path_len, k, v, g, beta, state, x,
-                           conv_hist))
+                           conv_hist, prep))
 
 
 def lumo_gdn_commit_graph_launch(graph: CommitGraph, stream=None):

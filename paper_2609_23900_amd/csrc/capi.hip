@@ -226,7 +226,12 @@ extern "C" lumo_status lumo_tree_gdn_verify_prep(const lumo_gdn_dims* dims, cons
     clear_error();
     LUMO_TRY(check_dims(dims, fn));
     LUMO_TRY(check_desc(dims, desc, fn));
-    LUMO_TRY(check_wy(dims, desc, fn));
+    const int policy = desc->plan.policy;
+    if (policy == LUMO_POLICY_PATHS || policy == LUMO_POLICY_TWO_LEVEL)
+        return fail(LUMO_EUNSUPPORTED,
+                    "%s: plan policy %d exports cut states to a workspace, which this call does not take "
+                    "(use LUMO_POLICY_RECOMPUTE or LUMO_POLICY_WY)", fn, policy);
+    if (policy != LUMO_POLICY_RECOMPUTE) LUMO_TRY(check_wy(dims, desc, fn));
     PrepArgs pr;
     LUMO_TRY(check_prep(prep, fn, pr));
     if (desc->plan.total_nodes == 0) return LUMO_OK;
@@ -238,7 +243,8 @@ extern "C" lumo_status lumo_tree_gdn_verify_prep(const lumo_gdn_dims* dims, cons
     LUMO_TRY(check_ptr(state0, fn, "state0"));
     LUMO_TRY(check_ptr(o, fn, "o"));
     GdnArgs a{q, k, v, g, beta, state0, o, nullptr, nullptr, pr};
-    hipError_t e = launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream));
+    hipError_t e = policy == LUMO_POLICY_WY ? launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream))
+                                            : launch_scan(*dims, *desc, a, static_cast<hipStream_t>(stream));
     if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not compiled into the library", fn);
     if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return LUMO_OK;
@@ -589,7 +595,8 @@ struct lumo_commit_graph {
 };
 
 extern "C" lumo_status lumo_gdn_commit_graph_create(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
-                                                    int32_t max_path, const int32_t* accepted_node, int32_t* path_out,
+                                                    const lumo_gdn_prep* prep, int32_t max_path,
+                                                    const int32_t* accepted_node, int32_t* path_out,
                                                     int32_t* path_len, const void* k, const void* v, const float* g,
                                                     const float* beta, float* state, int32_t channels, const void* x,
                                                     void* conv_hist, lumo_commit_graph** out) {
@@ -599,6 +606,8 @@ extern "C" lumo_status lumo_gdn_commit_graph_create(const lumo_gdn_dims* dims, c
     *out = nullptr;
     LUMO_TRY(check_commit(dims, desc, max_path, accepted_node, path_out, path_len, k, v, g, beta, state, channels, x,
                           conv_hist, fn));
+    PrepArgs pr;
+    LUMO_TRY(check_prep(prep, fn, pr));
     lumo_commit_graph* cg = new (std::nothrow) lumo_commit_graph();
     if (!cg) return fail(LUMO_EHIP, "%s: out of host memory", fn);
     hipStream_t s = nullptr;
@@ -607,7 +616,7 @@ extern "C" lumo_status lumo_gdn_commit_graph_create(const lumo_gdn_dims* dims, c
     if (e == hipSuccess) {
         hipError_t le = hipSuccess;
         if (dims->n_req > 0) {
-            CommitArgs a{max_path, accepted_node, path_out, path_len, k, v, g, beta, state, channels, x, conv_hist};
+            CommitArgs a{max_path, accepted_node, path_out, path_len, k, v, g, beta, state, channels, x, conv_hist, pr};
             le = launch_commit(*dims, *desc, a, s);
         }
         e = hipStreamEndCapture(s, &cg->graph);

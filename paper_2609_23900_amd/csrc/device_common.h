@@ -88,10 +88,13 @@ struct Dot4 {
 //   u = (R_pi k)_j;  delta = beta (v_j - alpha u);  R_j <- alpha R_j + delta k
 // alpha is applied to the dot product instead of the matrix (same value in exact
 // arithmetic). The operation order is fixed (explicit fma, contraction off), so
-// verification and commit produce bitwise identical states.
+// verification and commit produce bitwise identical states. ks scales the key (1/|k|
+// with query/key normalisation, else exactly 1, which leaves every value unchanged):
+// delta = beta (v_j - alpha ks u) ks and R_j <- alpha R_j + delta k, the update with the
+// normalised key.
 template <int DK, int OPT>
 __device__ __forceinline__ void gdn_row_update(float (&S)[DK], const typename Op<OPT>::T* __restrict__ kp,
-                                               float vj, float alpha, float beta) {
+                                               float vj, float alpha, float beta, float ks = 1.f) {
     constexpr int C = kChunk < DK ? kChunk : DK;
     Dot4 u;
 #pragma unroll
@@ -101,7 +104,7 @@ __device__ __forceinline__ void gdn_row_update(float (&S)[DK], const typename Op
 #pragma unroll
         for (int i = 0; i < C; ++i) u.add(c + i, S[c + i], kf[i]);
     }
-    const float delta = beta * __builtin_fmaf(-alpha, u.sum(), vj);
+    const float delta = beta * __builtin_fmaf(-alpha, u.sum() * ks, vj) * ks;
 #pragma unroll
     for (int c = 0; c < DK; c += C) {
         float kf[C];
@@ -111,9 +114,10 @@ __device__ __forceinline__ void gdn_row_update(float (&S)[DK], const typename Op
     }
 }
 
-// o_j = R_j . q
+// o_j = (R_j . q) qs  (qs = 1/|q| with query/key normalisation, else exactly 1)
 template <int DK, int OPT>
-__device__ __forceinline__ float gdn_row_output(const float (&S)[DK], const typename Op<OPT>::T* __restrict__ qp) {
+__device__ __forceinline__ float gdn_row_output(const float (&S)[DK], const typename Op<OPT>::T* __restrict__ qp,
+                                                float qs = 1.f) {
     constexpr int C = kChunk < DK ? kChunk : DK;
     Dot4 o;
 #pragma unroll
@@ -123,7 +127,24 @@ __device__ __forceinline__ float gdn_row_output(const float (&S)[DK], const type
 #pragma unroll
         for (int i = 0; i < C; ++i) o.add(c + i, S[c + i], qf[i]);
     }
-    return o.sum();
+    return o.sum() * qs;
+}
+
+// 1/sqrt(|x|^2 + eps) of a wave-uniform query or key row (Sec. IV-B normalisation):
+// one fma chain over the elements in index order, the order the commit's replay uses
+// for its keys, so that prepared verification and prepared commit agree bit for bit.
+template <int DK, int OPT>
+__device__ __forceinline__ float row_rsq_norm(const typename Op<OPT>::T* __restrict__ xp, float eps) {
+    constexpr int C = kChunk < DK ? kChunk : DK;
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < DK; c += C) {
+        float xf[C];
+        Op<OPT>::template ld_row<C>(xp + opaque(c), xf);
+#pragma unroll
+        for (int i = 0; i < C; ++i) ss = __builtin_fmaf(xf[i], xf[i], ss);
+    }
+    return __builtin_amdgcn_rsqf(ss + eps);
 }
 
 // ---------------------------------------------------------------- operand preparation

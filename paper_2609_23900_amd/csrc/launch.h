@@ -26,7 +26,7 @@ struct GdnArgs {
     void* o;
     float* node_states;
     float* ws;
-    PrepArgs prep;  // WY kernel only
+    PrepArgs prep;  // WY kernel, and the scans of lumo_tree_gdn_verify_prep
 };
 
 // Sequential path scans (PATHS / TWO_LEVEL / RECOMPUTE): one launch per dependency level.

@@ -9,7 +9,9 @@
 // the node's k and q rows are wave-uniform and are read with scalar loads.
 // Segments of a dependency level are independent and run in one launch; a segment
 // exports its tile to the workspace at nodes whose other children start segments of
-// the next level (cut states, Sec. IV-C, Eq. (4)).
+// the next level (cut states, Sec. IV-C, Eq. (4)). With operand preparation (Sec.
+// IV-B) the gates come from raw inputs and the key and query rows are used divided by
+// sqrt(|x|^2 + eps), computed as the commit's replay computes them.
 #include "device_common.h"
 #include "internal.h"
 #include "launch.h"
@@ -24,6 +26,7 @@ struct ScanParams {
     int32_t o_seg, o_seg_nodes;
     int32_t n_layers, total_rows, h_k, h_v, d_v, group, n_vtiles;
     int32_t seg_first;
+    PrepArgs prep;  // operand preparation (Sec. IV-B); flags 0 = operands as given
 };
 
 template <int DK, int OPT>
@@ -56,17 +59,24 @@ __global__ __launch_bounds__(64) void scan_kernel(ScanParams p, const typename O
 #pragma unroll
     for (int i = 0; i < DK; ++i) S[i] = S0[(long)i * p.d_v + jc];
 
+    const bool qkn = (p.prep.flags & LUMO_PREP_QK_NORM) != 0;  // uniform
+    const bool rawg = (p.prep.flags & LUMO_PREP_RAW_GATES) != 0;
+    const float alog = rawg ? p.prep.a_log[l * p.h_v + h] : 0.f;
+    const float dtb = rawg ? p.prep.dt_bias[l * p.h_v + h] : 0.f;
     for (int e = first; e < first + len; ++e) {
         const int32_t* en = p.blob + p.o_seg_nodes + kSegNodeWords * e;
         const int row = en[0], wout = en[1], cut = en[2];
         const long gi = ((long)l * p.total_rows + row) * p.h_v + h;
         const long ki = (((long)l * p.total_rows + row) * p.h_k + hk) * DK;
-        const float alpha = __expf(g[gi]);
-        const float beta = gbeta[gi];
+        const float gv = g[gi], bv = gbeta[gi];
+        const float alpha = __expf(rawg ? raw_log_alpha(gv, alog, dtb) : gv);
+        const float beta = rawg ? raw_beta(bv) : bv;
         const float vj = Op<OPT>::ld(v, gi * p.d_v + jc);
-        gdn_row_update<DK, OPT>(S, k + ki, vj, alpha, beta);
+        const float ks = qkn ? row_rsq_norm<DK, OPT>(k + ki, p.prep.qk_eps) : 1.f;
+        gdn_row_update<DK, OPT>(S, k + ki, vj, alpha, beta, ks);
         if (wout) {
-            const float ov = gdn_row_output<DK, OPT>(S, q + ki);
+            const float qs = qkn ? row_rsq_norm<DK, OPT>(q + ki, p.prep.qk_eps) : 1.f;
+            const float ov = gdn_row_output<DK, OPT>(S, q + ki, qs);
             if (act) {
                 Op<OPT>::st(o, gi * p.d_v + j, ov);
                 if (node_states) {
@@ -118,6 +128,7 @@ hipError_t launch_scan(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.d_v = d.d_v;
     p.group = d.h_v / d.h_k;
     p.n_vtiles = (d.d_v + 63) / 64;
+    p.prep = a.prep;
     // Level boundaries come from the host copy of the plan words.
     for (int lv = 0; lv < pl.n_levels; ++lv) {
         const int first = desc.host_blob[pl.o_level_off + lv];

@@ -137,7 +137,7 @@ class GdnTreeStep:
             self.dims, self.desc, self.max_path, self.accepted, self.path_out, self.path_len,
             self.t["k"], self.t["v"], self.t["g"], self.t["beta"], self.state,
             self.channels if use_conv else 0, self.x if use_conv else None,
-            self.hist if use_conv else None)
+            self.hist if use_conv else None, self.prep)
 
     def reset_state(self):
         self.state.copy_(self.state0)

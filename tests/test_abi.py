@@ -180,10 +180,16 @@ def test_graph_create_rejects_and_null_launch():
     desc, _blob = _desc()
     h = ctypes.c_void_p()
     P = ctypes.c_void_p
-    st = L._lib.lumo_gdn_commit_graph_create(ctypes.byref(_dims()), ctypes.byref(desc), 0, P(FAKE),
+    st = L._lib.lumo_gdn_commit_graph_create(ctypes.byref(_dims()), ctypes.byref(desc), None, 0, P(FAKE),
                                              P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
                                              P(FAKE), 0, None, None, ctypes.byref(h))
     assert st == L.LUMO_EINVAL and not h.value
+    # a malformed preparation is refused before anything is captured
+    bad = L.lumo_gdn_prep(8, 0.0, None, None)
+    st = L._lib.lumo_gdn_commit_graph_create(ctypes.byref(_dims()), ctypes.byref(desc), ctypes.byref(bad), 4,
+                                             P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+                                             P(FAKE), 0, None, None, ctypes.byref(h))
+    assert st == L.LUMO_EINVAL and not h.value and "prep" in L.lumo_last_error()
     assert L._lib.lumo_gdn_commit_graph_launch(None, None) == L.LUMO_EINVAL
     L._lib.lumo_gdn_commit_graph_destroy(None)
 

@@ -298,6 +298,40 @@ def test_commit_graph_replays():
     g.close()
 
 
+def test_commit_graph_replays_prepared():
+    """The captured committer with operand preparation (Sec. V-A with Sec. IV-B): 24
+    replays with a changing device accepted_node, each against the oracle's prepared
+    commit; the unprepared graph over the same raw operands publishes something else."""
+    wl = workload("widedeep")
+    a, oprep, gprep = _prep_inputs(wl, QKN | RAWG, seed=85)
+    st = _prep_step(wl, a, gprep, policy=L.LUMO_POLICY_WY)
+    g = st.commit_graph(with_conv=False)
+    rng = np.random.default_rng(6)
+    inst = gu.sample_instances(wl, 8, seed=4)
+    for rep in range(24):
+        lens = rng.integers(0, 17, size=wl.n_req)
+        acc = np.array([configs._pick_accepted(rng, p, int(L_), int(L_)) if L_ > 0 else -1
+                        for p, L_ in zip(wl.parents, lens)], np.int32)
+        st.state.copy_(st.state0)
+        st.accepted.copy_(torch.from_numpy(acc))
+        torch.cuda.synchronize()
+        g.launch()
+        torch.cuda.synchronize()
+        ref, po, pl = oracle.commit(wl, accepted=acc, arrays=a, prep=oprep)
+        assert np.array_equal(st.path_out.cpu().numpy(), po), rep
+        assert np.array_equal(st.path_len.cpu().numpy(), pl), rep
+        gu.check_states(wl, st.state.cpu().numpy(), ref, inst)
+    g.close()
+    plain = _prep_step(wl, a, None, policy=L.LUMO_POLICY_WY)
+    gp = plain.commit_graph(with_conv=False)
+    plain.accepted.copy_(torch.from_numpy(acc))
+    gp.launch()
+    torch.cuda.synchronize()
+    gp.close()
+    r = int(np.argmax(pl))
+    assert pl[r] > 1 and gu.max_rel(plain.state.cpu().numpy()[r], ref[r]) > 1e-2
+
+
 # ---------------------------------------------------------------- negative controls
 
 def test_negative_control_sibling_swap_detected():
@@ -754,6 +788,59 @@ def test_wy_prep_deep_and_groupings():
     torch.cuda.synchronize()
     inst = [(r, l, h) for r in range(3) for l in range(2) for h in (0, 3)]
     _check_prep_outputs(wl, gu.to_np(st.o), a, oprep, inst)
+
+
+@pytest.mark.parametrize("case", ["layer1", "tiny_f32", "deep_f32"])
+def test_scan_prep_parity(case):
+    """Prepared operands on the sequential scan (RECOMPUTE, the schedule that needs no
+    workspace): outputs against the oracle with the same preparation, for the shapes the
+    WY kernel does not take (fp32 operands, d < 128, paths longer than 17 nodes)."""
+    if case == "layer1":
+        wl = workload("layer1")
+        inst = [(0, 0, h) for h in range(0, wl.h_v, 5)]
+    elif case == "tiny_f32":
+        wl = workload("tiny")
+        inst = [(0, 0, 0)]
+    else:
+        rng = np.random.default_rng(81)
+        parents = [trees.chain(23), trees.random_tree(rng, 30, 20, trees.bmax_uniform(2))]
+        wl = pins.make_wl(parents, d_k=64, d_v=32, h_k=2, h_v=4, op_dtype=ops.F32, n_rows=[23, 33],
+                          n_layers=2, max_path=23)
+        wl.arrays = ops.make_gdn_operands(82, n_req=2, n_layers=2, total_rows=56, h_k=2, h_v=4,
+                                          d_k=64, d_v=32, op_dtype=ops.F32)
+        wl.accepted = np.array([22, int(np.argmax(trees.depths(parents[1])))], np.int32)
+        inst = [(r, l, h) for r in range(2) for l in range(2) for h in range(4)]
+    flags = QKN | RAWG
+    if wl.op_dtype == ops.F32:
+        # fp32 operand rows rescaled for the normalisation to matter
+        rng = np.random.default_rng(83)
+        a = dict(wl.arrays)
+        for key in ("q", "k"):
+            a[key] = (a[key] * rng.uniform(0.3, 3.0, size=a[key].shape[:-1] + (1,))).astype(np.float32)
+        a["g"] = rng.standard_normal(a["g"].shape).astype(np.float32)
+        a["beta"] = rng.standard_normal(a["beta"].shape).astype(np.float32)
+        a_log = (0.5 * rng.standard_normal((wl.n_layers, wl.h_v))).astype(np.float32)
+        dt_bias = rng.standard_normal((wl.n_layers, wl.h_v)).astype(np.float32)
+        oprep = oracle.Prep(flags, 1e-6, a_log, dt_bias)
+        gprep = L.Prep(flags, 1e-6, torch.from_numpy(a_log).cuda(), torch.from_numpy(dt_bias).cuda())
+    else:
+        a, oprep, gprep = _prep_inputs(wl, flags, seed=84)
+    say(f"[gpu] scan prep {case}")
+    st = _prep_step(wl, a, gprep, policy=L.LUMO_POLICY_RECOMPUTE)
+    st.verify()
+    st.commit()
+    torch.cuda.synchronize()
+    worst = _check_prep_outputs(wl, gu.to_np(st.o), a, oprep, inst, tol=gu.out_tol(wl))
+    say(f"  outputs worst max-rel {worst:.3e}")
+    ref_state, _, pl = oracle.commit(wl, arrays=a, prep=oprep)
+    assert np.array_equal(st.path_len.cpu().numpy(), pl)
+    gu.check_states(wl, st.state.cpu().numpy(), ref_state, inst)
+    plain = _prep_step(wl, a, None, policy=L.LUMO_POLICY_RECOMPUTE)
+    plain.verify()
+    torch.cuda.synchronize()
+    r0, l0, h0 = inst[0]
+    rows = gu.node_rows(wl, r0)
+    assert gu.max_rel(gu.to_np(plain.o)[l0, rows, h0], gu.to_np(st.o)[l0, rows, h0]) > 0.05
 
 
 def test_commit_prep_on_scan_plan():
