@@ -158,6 +158,16 @@ __device__ __forceinline__ float raw_log_alpha(float a, float a_log, float dt_bi
 }
 __device__ __forceinline__ float raw_beta(float b) { return 1.f / (1.f + __expf(-b)); }
 
+// ---------------------------------------------------------------- lane groups
+// The sum of x over the four 16-lane rows of a wave, in every lane (the same bits in all
+// four: (x0 + x1) + (x2 + x3)).
+__device__ __forceinline__ float row_group_sum(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // ---------------------------------------------------------------- launch geometry
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).
 // Remap so that consecutive logical block ids run on the same XCD: blocks that

@@ -130,17 +130,12 @@ template <int R> struct RoleTag {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
 
-// The sum of x over the four 16-lane rows, in every lane (the same bits in all four:
-// (x0 + x1) + (x2 + x3)).
-__device__ __forceinline__ float row_group_sum(float x) {
-    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
-    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
 
-// Two waves per SIMD for D = 8 (79 KB of LDS per 4-wave block); with D = 16 the
-// records make a 4-wave block too large for two per CU, so one wave per SIMD.
+// Two waves per SIMD for D = 8 (79 KB of LDS per 4-wave block). With D = 16 (and no
+// fused conv) the two waves of a value head share one record buffer (the even wave
+// writes it, a barrier publishes it), which keeps the 4-wave block at 76 KB, so two
+// blocks fit a CU, and the block is compiled for two waves per SIMD (256 registers).
+// The fused conv's D = 16 instance keeps per-wave buffers and one wave per SIMD.
 // PEND: the state bank (state0 = pd.state) first receives the replay of the previous
 // iteration's accepted path (Eq. (2)-(3) per path node), is stored back, and the
 // verification then starts from it; requests without nodes are published only.
@@ -148,7 +143,7 @@ __device__ __forceinline__ float row_group_sum(float x) {
 // bf16 rows stay as they are in LDS and the MFMA products; the per-row factors scale
 // the Gram entries, R0 k, R0 q and k.q in the records, and the pending path's keys.
 template <int D, int NVH, bool PEND, bool QKN, bool CONV>
-__global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, const uint16_t* __restrict__ kmat,
+__global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void wy_kernel(WyParams p, const uint16_t* __restrict__ kmat,
                                                     const uint16_t* __restrict__ qmat,
                                                     const uint16_t* __restrict__ vmat, const float* __restrict__ gmat,
                                                     const float* __restrict__ bmat, const float* __restrict__ state0,
@@ -156,11 +151,14 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     static_assert(!CONV || (NVH == 2 && PEND), "the fused conv serves two value heads per block, with publication");
     constexpr int W = Rec<D>::kWords;
     constexpr int nthr = 128 * NVH;
+    // the waves of a value head share its records (D = 16 without the fused conv)
+    constexpr bool SHR = D == 16 && !CONV;
     // LDS, one object per role: the compiler orders LDS reads after the direct
     // global-to-LDS copies only where they may touch the same object.
     __shared__ KQTile tile;                        // block: chunk keys, queries, path-stack keys
     __shared__ __attribute__((aligned(16))) float G[kCand * kGS];  // block: Gram [candidate][chunk key | chunk query]
-    __shared__ __attribute__((aligned(16))) float recs[2 * NVH][kTile * W];  // per wave: the chunk's coefficient records
+    // per wave (SHR: per value head): the chunk's coefficient records
+    __shared__ __attribute__((aligned(16))) float recs[SHR ? NVH : 2 * NVH][kTile * W];
     __shared__ float alphas[2 * NVH][64];          // per wave: exp(g) of the candidates
     // per wave: value rows, then outputs; double-buffered (CONV: single, for the caches)
     __shared__ uint4 vbufs[2 * NVH][CONV ? 1 : 2][kTile * 8];
@@ -172,8 +170,9 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
     const int tid = (int)threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: head and half in SGPRs
     const int lane = tid & 63;
-    float* wrec = recs[wave];
+    float* wrec = recs[SHR ? wave >> 1 : wave];
     float* walpha = alphas[wave];
+    const bool rec_writer = !SHR || (wave & 1) == 0;  // uniform
 
     int blk = xcd_remap(blockIdx.x, gridDim.x);
     const int pairs = p.group / NVH;
@@ -452,8 +451,12 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         const int32_t* ppath = pd.path_out + (long)r * pd.max_path;
         const long prow0 = (long)l * pd.total_rows;
         uint4* kst = reinterpret_cast<uint4*>(G);       // kPend key rows x 16 slots
-        uint4* vst = reinterpret_cast<uint4*>(wrec);    // kPend entries x 64 values (8 slots)
-        const uint16_t* vsh = reinterpret_cast<const uint16_t*>(wrec);
+        // kPend entries x 64 values (8 slots) in the record space; with shared records
+        // each wave of the head takes its own half of it
+        static_assert(!SHR || kTile * W >= 2 * (kPend * 64 / 2), "two staging areas fit one record buffer");
+        float* vstage = wrec + (SHR ? (wave & 1) * (kPend * 64 / 2) : 0);
+        uint4* vst = reinterpret_cast<uint4*>(vstage);
+        const uint16_t* vsh = reinterpret_cast<const uint16_t*>(vstage);
         // CONV: this thread's channels of the old history (the chain conv's first window,
         // rolled along the path) and of the published one, the last three of (old
         // history, the path's raw x rows)
@@ -805,10 +808,12 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
         half_products(0, pk, pq);
         lds_barrier();  // the Gram is complete
 
-        // ---- coefficient records of the wave's head (lanes 0..31: A, lanes 32..63: B)
-        if (ln < kTile + kStack)
-            walpha[ln < kTile ? kStack + ln : ln - kTile] = __expf(rawg ? raw_log_alpha(info.g, alog, dtb) : info.g);
-        {
+        // ---- coefficient records of the wave's head (lanes 0..31: A, lanes 32..63: B);
+        // with shared records the even wave of the head writes them
+        if (rec_writer) {
+            if (ln < kTile + kStack)
+                walpha[ln < kTile ? kStack + ln : ln - kTile] =
+                    __expf(rawg ? raw_log_alpha(info.g, alog, dtb) : info.g);
             const bool isB = ln >= kTile;
             const float* Gc = G + (isB ? kTile : 0) + tn;
             const float bt = rawg ? raw_beta(info.b) : info.b;
@@ -850,6 +855,7 @@ __global__ __launch_bounds__(256, D == 8 ? 2 : 1) void wy_kernel(WyParams p, con
             lane_info(c0 + kTile, rowA, info);
             if (c0 + 2 * kTile < N) rowB = lane_rows(c0 + 2 * kTile);
         }
+        if constexpr (SHR) lds_barrier();  // the head's records are written
 
         const float* rec = wrec;
         uint16_t* vs = reinterpret_cast<uint16_t*>(vbufs[wave][CONV ? 0 : buf]);
