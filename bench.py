@@ -477,6 +477,8 @@ def arithmetic_label(wl, policy, args):
     the O(d^2) products run."""
     import paper_2609_23900_amd as L
     ops_t = "bf16" if wl.op_dtype == 1 else "f32"
+    if policy == L.LUMO_POLICY_WY and wl.op_dtype == 0:
+        return f"{ops_t} operands/outputs, f32 state; WY form on the vector ALUs in f32"
     if policy == L.LUMO_POLICY_WY:
         core = "R0.[K|Q] on bf16 MFMA with R0 split into bf16 hi+lo (16 significant bits), f32 accumulate"
         if args.fused:
@@ -496,6 +498,9 @@ def main():
     ap.add_argument("--prep", action="store_true",
                     help="prepare operands in the kernels (query/key normalisation, gates from raw "
                          "inputs; wy policy): g and beta are then read as raw inputs")
+    ap.add_argument("--f32", action="store_true",
+                    help="fp32 operands and outputs (the wy policy then runs its vector-ALU kernel, and the "
+                         "commit replays eagerly: the deferred publication lives in the matrix-core kernel)")
     ap.add_argument("--copy-probe", action="store_true", help="only run the counter-calibration copy")
     ap.add_argument("--attention", action="store_true", help="only run the tree-attention benchmark")
     ap.add_argument("--select", action="store_true", help="only run the draft-selection benchmark")
@@ -538,7 +543,7 @@ def main():
     from lumo_synth import configs
 
     policy = L.POLICIES[args.policy]
-    deferred = args.commit == "deferred" and policy == L.LUMO_POLICY_WY
+    deferred = args.commit == "deferred" and policy == L.LUMO_POLICY_WY and not args.f32
     if args.fused and not deferred:
         sys.exit("--fused needs the wy policy and the deferred commit")
     if args.fused and not args.prep:
@@ -546,7 +551,7 @@ def main():
         # normalised after the conv (in the kernel), else the replays diverge
         sys.exit("--fused needs --prep (query/key normalisation of the conv outputs)")
     log(f"[bench] generating {args.config}")
-    wl = configs.build(args.config)
+    wl = configs.build(args.config, op_dtype=0) if args.f32 else configs.build(args.config)
     log(f"[bench] uploading; policy {args.policy}")
     prep = None
     if args.prep:
@@ -638,6 +643,7 @@ def main():
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
     else:
+        vb = ab["verify_bytes"]
         ach = ab["verify_flops"] / (ver_ms * 1e-3) / 1e12
         roof = {"bound": "alu", "achieved": round(ach, 2), "peak": PEAK_VALU_F32_TFS,
                 "unit": "TFLOP/s", "frac": round(ach / PEAK_VALU_F32_TFS, 4), "traffic": None}
@@ -677,7 +683,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": arithmetic_label(wl, policy, args),
         "data": "synthetic (seeded trees and operands shaped like the paper's workloads)",
-        "config": {"workload": f"{args.config}: {WORKLOAD_TEXT[args.config]}",
+        "config": {"workload": f"{args.config}: " + (WORKLOAD_TEXT[args.config].replace("bf16 operands", "fp32 operands")
+                                                      if wl.op_dtype == 0 else WORKLOAD_TEXT[args.config]),
                    "policy": args.policy, "commit": mode, "conv": "fused into verify" if args.fused else "separate",
                    "head_node_updates_per_step": hn,
                    "operand_prep": "qk_norm+raw_gates" if args.prep else "none",

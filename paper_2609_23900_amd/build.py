@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "liblumo_tree.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
-SOURCES = ["capi.hip", "plan.cpp", "verify_scan.hip", "verify_wy.hip", "commit.hip", "conv.hip",
+SOURCES = ["capi.hip", "plan.cpp", "verify_scan.hip", "verify_wy.hip", "verify_wyv.hip", "commit.hip", "conv.hip",
            "attention.hip", "select.hip"]
 ARCH = "gfx950"
 

@@ -60,17 +60,35 @@ lumo_status check_dims(const lumo_gdn_dims* d, const char* fn) {
     return LUMO_OK;
 }
 
-// The WY policy's shape limits (bf16, d_k = d_v = 128, at most kWyMaxDepth nodes per path).
+// The matrix-core WY kernel's shape limits (bf16, d_k = d_v = 128, at most kWyMaxDepth
+// nodes per path): the deferred publication and the fused conv live in it.
 lumo_status check_wy(const lumo_gdn_dims* d, const lumo_tree_desc* desc, const char* fn) {
     if (desc->plan.policy != LUMO_POLICY_WY)
         return fail(LUMO_EUNSUPPORTED, "%s: needs a plan built for LUMO_POLICY_WY (plan policy %d)", fn,
                     desc->plan.policy);
     if (d->op_dtype != LUMO_BF16 || d->d_k != 128 || d->d_v != 128)
-        return fail(LUMO_EUNSUPPORTED, "%s: the WY policy is built for bf16 operands with d_k = d_v = 128", fn);
+        return fail(LUMO_EUNSUPPORTED, "%s: built for bf16 operands with d_k = d_v = 128", fn);
     if (desc->plan.max_depth > kWyMaxDepth)
-        return fail(LUMO_EUNSUPPORTED, "%s: the WY policy handles paths of at most %d nodes (plan has %d)", fn,
-                    kWyMaxDepth, desc->plan.max_depth);
+        return fail(LUMO_EUNSUPPORTED, "%s: handles paths of at most %d nodes (plan has %d)", fn, kWyMaxDepth,
+                    desc->plan.max_depth);
     return LUMO_OK;
+}
+
+// A WY plan's verification: the matrix-core kernel for its shapes, the vector-ALU WY
+// kernel for the others (any supported d_k, d_v and operand type; paths of at most
+// kWyvMaxDepth nodes).
+lumo_status check_wy_verify(const lumo_gdn_dims* d, const lumo_tree_desc* desc, const char* fn) {
+    if (desc->plan.policy != LUMO_POLICY_WY)
+        return fail(LUMO_EUNSUPPORTED, "%s: needs a plan built for LUMO_POLICY_WY (plan policy %d)", fn,
+                    desc->plan.policy);
+    if (!wy_mfma_shape(*d, desc->plan) && desc->plan.max_depth > kWyvMaxDepth)
+        return fail(LUMO_EUNSUPPORTED, "%s: the WY policy handles paths of at most %d nodes (plan has %d)", fn,
+                    kWyvMaxDepth, desc->plan.max_depth);
+    return LUMO_OK;
+}
+
+hipError_t launch_wy_any(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s) {
+    return wy_mfma_shape(d, desc.plan) ? launch_wy(d, desc, a, s) : launch_wyv(d, desc, a, s);
 }
 
 // Operand preparation: flags, constant and gate parameters; NULL means none.
@@ -198,7 +216,7 @@ extern "C" lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lum
     LUMO_TRY(check_ptr(node_states, fn, "node_states", true));
     if (policy == LUMO_POLICY_WY) {
         if (node_states) return fail(LUMO_EUNSUPPORTED, "%s: the WY policy keeps no per-node states", fn);
-        LUMO_TRY(check_wy(dims, desc, fn));
+        LUMO_TRY(check_wy_verify(dims, desc, fn));
     }
     const size_t need = lumo_tree_gdn_workspace_bytes(dims, &desc->plan);
     if (need) {
@@ -209,7 +227,7 @@ extern "C" lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lum
     GdnArgs a{q, k, v, g, beta, state0, o, node_states, static_cast<float*>(workspace)};
     hipError_t e;
     if (policy == LUMO_POLICY_WY) {
-        e = launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream));
+        e = launch_wy_any(*dims, *desc, a, static_cast<hipStream_t>(stream));
     } else {
         e = launch_scan(*dims, *desc, a, static_cast<hipStream_t>(stream));
     }
@@ -231,7 +249,7 @@ extern "C" lumo_status lumo_tree_gdn_verify_prep(const lumo_gdn_dims* dims, cons
         return fail(LUMO_EUNSUPPORTED,
                     "%s: plan policy %d exports cut states to a workspace, which this call does not take "
                     "(use LUMO_POLICY_RECOMPUTE or LUMO_POLICY_WY)", fn, policy);
-    if (policy != LUMO_POLICY_RECOMPUTE) LUMO_TRY(check_wy(dims, desc, fn));
+    if (policy != LUMO_POLICY_RECOMPUTE) LUMO_TRY(check_wy_verify(dims, desc, fn));
     PrepArgs pr;
     LUMO_TRY(check_prep(prep, fn, pr));
     if (desc->plan.total_nodes == 0) return LUMO_OK;
@@ -243,7 +261,7 @@ extern "C" lumo_status lumo_tree_gdn_verify_prep(const lumo_gdn_dims* dims, cons
     LUMO_TRY(check_ptr(state0, fn, "state0"));
     LUMO_TRY(check_ptr(o, fn, "o"));
     GdnArgs a{q, k, v, g, beta, state0, o, nullptr, nullptr, pr};
-    hipError_t e = policy == LUMO_POLICY_WY ? launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream))
+    hipError_t e = policy == LUMO_POLICY_WY ? launch_wy_any(*dims, *desc, a, static_cast<hipStream_t>(stream))
                                             : launch_scan(*dims, *desc, a, static_cast<hipStream_t>(stream));
     if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not compiled into the library", fn);
     if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));

@@ -69,6 +69,16 @@ hipError_t launch_wy_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, co
                           const PendArgs& pend, const ConvFuseArgs& cf);
 constexpr int kWyMaxDepth = 17;  // nodes on a root-to-leaf path
 
+// The WY form on the vector ALUs for the shapes the matrix-core kernel does not take
+// (fp32 operands, d_k or d_v below 128, paths of 18 to kWyvMaxDepth nodes). No
+// workspace; operand preparation as in GdnArgs::prep.
+constexpr int kWyvMaxDepth = 32;
+hipError_t launch_wyv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const GdnArgs& a, hipStream_t s);
+// Whether the matrix-core WY kernel serves these dimensions and plan.
+inline bool wy_mfma_shape(const lumo_gdn_dims& d, const lumo_plan& p) {
+    return d.op_dtype == LUMO_BF16 && d.d_k == 128 && d.d_v == 128 && p.max_depth <= kWyMaxDepth;
+}
+
 struct CommitArgs {
     int32_t max_path;
     const int32_t* accepted;

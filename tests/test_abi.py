@@ -109,9 +109,13 @@ def test_verify_rejects_null_desc_blob():
     assert _verify(_dims(), desc) == L.LUMO_EINVAL
 
 
-def test_wy_requires_bf16_d128():
+def test_wy_node_states_refused():
+    """The WY form keeps no per-node states: a debug dump is refused before any launch."""
     desc, _blob = _desc(policy=L.LUMO_POLICY_WY)
-    assert _verify(_dims(), desc) == L.LUMO_EUNSUPPORTED
+    P = ctypes.c_void_p
+    st = L._lib.lumo_tree_gdn_verify(ctypes.byref(_dims()), ctypes.byref(desc), *([P(FAKE)] * 7), P(FAKE),
+                                     P(FAKE), 0, 0, None)
+    assert st == L.LUMO_EUNSUPPORTED and "node states" in L.lumo_last_error()
 
 
 def _commit(d, desc, max_path=4, x=True, hist=True, channels=8, accepted=FAKE):
@@ -203,14 +207,23 @@ def test_empty_batch_is_a_no_op():
     assert _commit(d, desc, accepted=0) == L.LUMO_OK
 
 
-def test_wy_rejects_paths_longer_than_17():
+def test_wy_rejects_paths_longer_than_32():
+    """The WY policy's verification takes paths of up to 32 nodes (the matrix-core kernel
+    17, the vector-ALU kernel the rest); the deferred publication keeps the 17-node
+    limit of the matrix-core kernel."""
+    par = trees.chain(33)
+    plan, blob = L.lumo_tree_plan(np.array([0, 33], np.int32), par, np.array([33], np.int32),
+                                  L.LUMO_POLICY_WY)
+    desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
+    for d in (_dims(h_k=1, h_v=1, d_k=128, d_v=128, op_dtype=1), _dims()):
+        assert _verify(d, desc, ws=L.lumo_tree_gdn_workspace_bytes(d, plan)) == L.LUMO_EUNSUPPORTED
+        assert "32" in L.lumo_last_error()
     par = trees.chain(18)
     plan, blob = L.lumo_tree_plan(np.array([0, 18], np.int32), par, np.array([18], np.int32),
                                   L.LUMO_POLICY_WY)
     desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
-    d = _dims(h_k=1, h_v=1, d_k=128, d_v=128, op_dtype=1)
-    assert _verify(d, desc, ws=L.lumo_tree_gdn_workspace_bytes(d, plan)) == L.LUMO_EUNSUPPORTED
-    assert "17" in L.lumo_last_error()
+    dw = _dims(h_k=1, h_v=1, d_k=128, d_v=128, op_dtype=1)
+    assert _pending(dw, desc, desc) == L.LUMO_EUNSUPPORTED and "17" in L.lumo_last_error()
 
 
 def test_wy_needs_no_workspace():

@@ -380,6 +380,90 @@ def test_wy_parity(name, n_inst):
     gu.check_states(wl, st.state.cpu().numpy(), ref_state, gu.sample_instances(wl, n_inst, seed=12))
 
 
+# ---------------------------------------------------------------- WY form on the vector ALUs
+
+def _wyv_case(case):
+    """Shapes the matrix-core kernel does not take, served by the vector-ALU WY kernel."""
+    rng = np.random.default_rng(91)
+    if case == "tiny_f32":
+        return configs.build("tiny", with_conv=False), [(0, 0, 0)]
+    if case == "layer1_f32":  # fp32 operands at the benchmark's head shape
+        wl = configs.build("layer1", with_conv=False, op_dtype=ops.F32)
+        return wl, [(0, 0, h) for h in range(0, 32, 3)]
+    if case == "deep_bf16":   # 30-node chain and a 25-level tree: beyond the 17-node limit
+        parents = [trees.chain(30), trees.random_tree(rng, 60, 25, trees.bmax_uniform(2)), np.zeros(0, np.int32)]
+        n_rows = [30, 63, 2]
+        wl = pins.make_wl(parents, d_k=128, d_v=128, h_k=2, h_v=4, op_dtype=ops.BF16, n_rows=n_rows,
+                          n_layers=2, max_path=30)
+    elif case == "d64_group4_bf16":  # eight value heads per key head: two blocks per key head
+        parents = [trees.random_tree(rng, 45, 8, trees.bmax_uniform(4)), trees.FIG1_PARENT]
+        n_rows = [47, 7]
+        wl = pins.make_wl(parents, d_k=64, d_v=128, h_k=1, h_v=4, op_dtype=ops.BF16, n_rows=n_rows,
+                          n_layers=2, max_path=8)
+    else:  # "d32_v16_f32": value columns fewer than a wave's lanes
+        parents = [trees.random_tree(rng, 37, 12, trees.bmax_uniform(3))]
+        n_rows = [40]
+        wl = pins.make_wl(parents, d_k=32, d_v=16, h_k=2, h_v=2, op_dtype=ops.F32, n_rows=n_rows,
+                          n_layers=1, max_path=12)
+    wl.arrays = ops.make_gdn_operands(92, n_req=wl.n_req, n_layers=wl.n_layers, total_rows=wl.total_rows,
+                                      h_k=wl.h_k, h_v=wl.h_v, d_k=wl.d_k, d_v=wl.d_v, op_dtype=wl.op_dtype)
+    inst = [(r, l, h) for r in range(wl.n_req) for l in range(wl.n_layers) for h in range(wl.h_v)
+            if len(wl.parents[r])]
+    return wl, inst
+
+
+@pytest.mark.parametrize("case", ["tiny_f32", "layer1_f32", "deep_bf16", "d64_group4_bf16", "d32_v16_f32"])
+def test_wyv_parity(case):
+    """The WY policy on shapes outside the matrix-core kernel (fp32 operands, d < 128,
+    paths beyond 17 nodes): outputs against the oracle, NaN pad rows neither read nor
+    written, and the sequential scan of the same plan shape within the output tolerance."""
+    wl, inst = _wyv_case(case)
+    rows = set(oracle.plan.flat_rows(wl.parents, wl.row_off).tolist())
+    pad = [x for x in range(wl.total_rows) if x not in rows]
+    a = dict(wl.arrays)
+    nan = np.float32(np.nan) if wl.op_dtype == ops.F32 else np.uint16(0x7FC0)
+    for key in ("q", "k", "v"):
+        a[key] = a[key].copy()
+        a[key][:, pad] = nan
+    for key in ("g", "beta"):
+        a[key] = a[key].copy()
+        a[key][:, pad] = np.nan
+    say(f"[gpu] wyv {case}")
+    st = run(wl, L.LUMO_POLICY_WY, with_conv=False, commit=False, arrays=a)
+    o = gu.to_np(st.o)
+    worst = gu.check_outputs(wl, o, inst, arrays=a)
+    say(f"  outputs worst max-rel {worst:.3e}")
+    if pad:
+        assert np.all(o[:, pad] == 0)
+    seq = gu.to_np(run(wl, L.LUMO_POLICY_RECOMPUTE, with_conv=False, commit=False, arrays=a).o)
+    rl = sorted(rows)
+    assert gu.max_rel(o[:, rl], seq[:, rl]) <= gu.out_tol(wl)
+    # two runs give the same bits
+    o2 = gu.to_np(run(wl, L.LUMO_POLICY_WY, with_conv=False, commit=False, arrays=a).o)
+    assert np.array_equal(o.view(np.uint32), o2.view(np.uint32))
+
+
+def test_wyv_prep_parity():
+    """Operand preparation (Sec. IV-B) on the vector-ALU WY kernel: fp32 operands."""
+    wl, inst = _wyv_case("layer1_f32")
+    rng = np.random.default_rng(93)
+    a = dict(wl.arrays)
+    for key in ("q", "k"):
+        a[key] = (a[key] * rng.uniform(0.3, 3.0, size=a[key].shape[:-1] + (1,))).astype(np.float32)
+    a["g"] = rng.standard_normal(a["g"].shape).astype(np.float32)
+    a["beta"] = rng.standard_normal(a["beta"].shape).astype(np.float32)
+    a_log = (0.5 * rng.standard_normal((wl.n_layers, wl.h_v))).astype(np.float32)
+    dt_bias = rng.standard_normal((wl.n_layers, wl.h_v)).astype(np.float32)
+    flags = QKN | RAWG
+    oprep = oracle.Prep(flags, 1e-6, a_log, dt_bias)
+    gprep = L.Prep(flags, 1e-6, torch.from_numpy(a_log).cuda(), torch.from_numpy(dt_bias).cuda())
+    st = _prep_step(wl, a, gprep, policy=L.LUMO_POLICY_WY)
+    st.verify()
+    torch.cuda.synchronize()
+    worst = _check_prep_outputs(wl, gu.to_np(st.o), a, oprep, inst, tol=gu.TOL_F32)
+    say(f"[gpu] wyv prep: outputs worst max-rel {worst:.3e}")
+
+
 def test_wy_agrees_with_sequential_scan():
     """WY and the sequential scan compute the same recurrence: outputs within bf16 rounding."""
     wl = workload("layer1")
