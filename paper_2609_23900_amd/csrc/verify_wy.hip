@@ -889,14 +889,20 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
                 NodeRec cur;
                 load_rec(n, cur);
                 const float vj = __uint_as_float(((uint32_t)vs[n * 64 + pc]) << 16);
-                // sums over the path stack as even/odd partial sums (half the dependent chain)
+                // sums over the path stack as even/odd partial sums (half the dependent
+                // chain), four depths at a time up to the node's depth: the record entries
+                // past it are zero (the branch is uniform)
                 float sa0 = 0.f, sa1 = 0.f, sb0 = 0.f, sb1 = 0.f;
 #pragma unroll
-                for (int m = 0; m < D; m += 2) {
-                    sa0 = __builtin_fmaf(cur.a[m], dst[m], sa0);
-                    sb0 = __builtin_fmaf(cur.b[m], dst[m], sb0);
-                    sa1 = __builtin_fmaf(cur.a[m + 1], dst[m + 1], sa1);
-                    sb1 = __builtin_fmaf(cur.b[m + 1], dst[m + 1], sb1);
+                for (int m4 = 0; m4 < D; m4 += 4) {
+                    if (m4 > 0 && cur.d <= m4) break;
+#pragma unroll
+                    for (int m = m4; m < m4 + 4; m += 2) {
+                        sa0 = __builtin_fmaf(cur.a[m], dst[m], sa0);
+                        sb0 = __builtin_fmaf(cur.b[m], dst[m], sb0);
+                        sa1 = __builtin_fmaf(cur.a[m + 1], dst[m + 1], sa1);
+                        sb1 = __builtin_fmaf(cur.b[m + 1], dst[m + 1], sb1);
+                    }
                 }
                 const float u = __builtin_fmaf(-cur.gm, pk[i / 4][i % 4], vj);  // v - gamma R0 k
                 const float delta = __builtin_fmaf(cur.bn, u, -(sa0 + sa1));     // beta u - sum A delta
