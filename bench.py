@@ -48,6 +48,7 @@ TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "traffic.json")
 VERIFY_SOURCES = {
     "wy": ["verify_wy.hip", "device_common.h", "internal.h", "launch.h"],
     "paths": ["verify_scan.hip", "device_common.h", "internal.h", "launch.h"],
+    "wyv": ["verify_wyv.hip", "device_common.h", "internal.h", "launch.h"],
     "attention": ["attention.hip", "device_common.h", "internal.h", "launch.h"],
     "select": ["select.hip", "select.h", "device_common.h"],
 }
@@ -648,13 +649,19 @@ def main():
         roof = {"bound": "alu", "achieved": round(ach, 2), "peak": PEAK_VALU_F32_TFS,
                 "unit": "TFLOP/s", "frac": round(ach / PEAK_VALU_F32_TFS, 4), "traffic": None}
     mode = "deferred" if deferred else "eager"
-    tr = recorded_traffic(args.policy, args.config, "fused" if args.fused else mode)
+    if policy == L.LUMO_POLICY_WY and wl.op_dtype == 0:  # the vector-ALU WY kernel
+        tr = recorded_traffic("wyv", args.config + "_f32", mode)
+    else:
+        tr = recorded_traffic(args.policy, args.config + ("_f32" if wl.op_dtype == 0 else ""),
+                              "fused" if args.fused else mode)
     if tr is not None:
         roof["traffic"] = {"fetch_bytes": tr["fetch_bytes"], "write_bytes": tr["write_bytes"],
                            "total_bytes": tr["fetch_bytes"] + tr["write_bytes"], "unit": "B per verify call",
                            "source": "profiles/traffic.json"}
     roof["kernel"] = ("tree conv + verify + publication of the previous path (one kernel)" if args.fused
-                      else "verify + publication of the previous path" if deferred else "verify")
+                      else "verify + publication of the previous path" if deferred
+                      else "verify (WY form on the vector ALUs)" if policy == L.LUMO_POLICY_WY and wl.op_dtype == 0
+                      else "verify")
     roof["per_launch"] = (f"{ab['verify_flops'] / 1e9:.2f} GFLOP, {vb / 1e6:.1f} MB algorithmic per verify call")
     kernels = {
         "conv_gather_ms": round(conv_ms, 4),
