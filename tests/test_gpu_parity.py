@@ -395,7 +395,7 @@ def _wyv_case(case):
         n_rows = [30, 63, 2]
         wl = pins.make_wl(parents, d_k=128, d_v=128, h_k=2, h_v=4, op_dtype=ops.BF16, n_rows=n_rows,
                           n_layers=2, max_path=30)
-    elif case == "d64_group4_bf16":  # eight value heads per key head: two blocks per key head
+    elif case == "d64_group4_bf16":  # four value heads of 128 columns per key head: 8 waves, two blocks
         parents = [trees.random_tree(rng, 45, 8, trees.bmax_uniform(4)), trees.FIG1_PARENT]
         n_rows = [47, 7]
         wl = pins.make_wl(parents, d_k=64, d_v=128, h_k=1, h_v=4, op_dtype=ops.BF16, n_rows=n_rows,
