@@ -862,52 +862,75 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
         // Straight-line over the 16 slots of a half: slots past the chunk's end hold exact
         // copies of its last node (tile rows, value row, record), so they recompute that
         // node's delta and output bit for bit and store the same value to the same place.
-        // One node's record in registers: {row, depth} as ints, {beta, gamma, k.q}, A, B.
-        struct NodeRec {
-            int rn, d;
-            float bn, gm, cn, gq;  // gm: gamma for R0 k, gq: gamma for R0 q
-            float a[D], b[D];
+        // A node's record head: {row, depth, beta, gamma, k.q, gamma_q}, the first four
+        // entries of A and B and the node's value entry. The next node's head is loaded
+        // while the current node computes; the entries past the first four (nodes deeper
+        // than 4) are loaded together, with one wait.
+        struct RecHead {
+            float4 w0, w1, a0, b0;  // w0 = {row, depth, beta, gamma}, w1 = {k.q, gamma_q, -, -}
+            uint32_t vraw;
         };
-        auto load_rec = [&](int n, NodeRec& c) {
+        auto load_head = [&](int n, RecHead& h) {
             const float* cf = rec + n * W;
-            c.rn = __builtin_amdgcn_readfirstlane(__float_as_int(cf[0]));  // uniform
-            c.d = __builtin_amdgcn_readfirstlane(__float_as_int(cf[1]));
-            c.bn = cf[2];
-            c.gm = cf[3];
-            c.cn = cf[4];
-            c.gq = QKN ? cf[5] : c.gm;
-#pragma unroll
-            for (int m = 0; m < D; ++m) {
-                c.a[m] = cf[8 + m];
-                c.b[m] = cf[8 + D + m];
-            }
+            h.w0 = *reinterpret_cast<const float4*>(cf);
+            h.w1 = *reinterpret_cast<const float4*>(cf + 4);
+            h.a0 = *reinterpret_cast<const float4*>(cf + 8);
+            h.b0 = *reinterpret_cast<const float4*>(cf + 8 + D);
+            h.vraw = vs[n * 64 + pc];
         };
         auto recursion = [&](int hf, const f32x4 (&pk)[4], const f32x4 (&pq)[4]) {
+            RecHead nx;
+            load_head(16 * hf, nx);
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const int n = 16 * hf + i;
-                NodeRec cur;
-                load_rec(n, cur);
-                const float vj = __uint_as_float(((uint32_t)vs[n * 64 + pc]) << 16);
+                const RecHead cu = nx;
+                if (i + 1 < 16) load_head(n + 1, nx);
+                const int d = __builtin_amdgcn_readfirstlane(__float_as_int(cu.w0.y));  // uniform
+                const float* cf = rec + n * W;
+                // the entries 4 .. of A and B up to the node's depth (zero past it); with
+                // D = 8 the four others are loaded with the head's wait, with D = 16 a group
+                // at a time (registers)
+                constexpr int kPre = D == 8 ? 1 : 0;  // groups loaded ahead of the sums
+                float4 am[D / 4 > 1 ? D / 4 - 1 : 1], bm[D / 4 > 1 ? D / 4 - 1 : 1];
+#pragma unroll
+                for (int g = 1; g <= kPre; ++g) {
+                    if (d > 4 * g) {  // uniform
+                        am[g - 1] = *reinterpret_cast<const float4*>(cf + 8 + 4 * g);
+                        bm[g - 1] = *reinterpret_cast<const float4*>(cf + 8 + D + 4 * g);
+                    }
+                }
+                const float vj = __uint_as_float(cu.vraw << 16);
                 // sums over the path stack as even/odd partial sums (half the dependent
                 // chain), four depths at a time up to the node's depth: the record entries
                 // past it are zero (the branch is uniform)
-                float sa0 = 0.f, sa1 = 0.f, sb0 = 0.f, sb1 = 0.f;
+                float sa0 = __builtin_fmaf(cu.a0.x, dst[0], 0.f), sb0 = __builtin_fmaf(cu.b0.x, dst[0], 0.f);
+                float sa1 = __builtin_fmaf(cu.a0.y, dst[1], 0.f), sb1 = __builtin_fmaf(cu.b0.y, dst[1], 0.f);
+                sa0 = __builtin_fmaf(cu.a0.z, dst[2], sa0);
+                sb0 = __builtin_fmaf(cu.b0.z, dst[2], sb0);
+                sa1 = __builtin_fmaf(cu.a0.w, dst[3], sa1);
+                sb1 = __builtin_fmaf(cu.b0.w, dst[3], sb1);
 #pragma unroll
-                for (int m4 = 0; m4 < D; m4 += 4) {
-                    if (m4 > 0 && cur.d <= m4) break;
-#pragma unroll
-                    for (int m = m4; m < m4 + 4; m += 2) {
-                        sa0 = __builtin_fmaf(cur.a[m], dst[m], sa0);
-                        sb0 = __builtin_fmaf(cur.b[m], dst[m], sb0);
-                        sa1 = __builtin_fmaf(cur.a[m + 1], dst[m + 1], sa1);
-                        sb1 = __builtin_fmaf(cur.b[m + 1], dst[m + 1], sb1);
+                for (int g = 1; g < D / 4; ++g) {
+                    if (d <= 4 * g) break;
+                    if (g > kPre) {
+                        am[g - 1] = *reinterpret_cast<const float4*>(cf + 8 + 4 * g);
+                        bm[g - 1] = *reinterpret_cast<const float4*>(cf + 8 + D + 4 * g);
                     }
+                    sa0 = __builtin_fmaf(am[g - 1].x, dst[4 * g], sa0);
+                    sb0 = __builtin_fmaf(bm[g - 1].x, dst[4 * g], sb0);
+                    sa1 = __builtin_fmaf(am[g - 1].y, dst[4 * g + 1], sa1);
+                    sb1 = __builtin_fmaf(bm[g - 1].y, dst[4 * g + 1], sb1);
+                    sa0 = __builtin_fmaf(am[g - 1].z, dst[4 * g + 2], sa0);
+                    sb0 = __builtin_fmaf(bm[g - 1].z, dst[4 * g + 2], sb0);
+                    sa1 = __builtin_fmaf(am[g - 1].w, dst[4 * g + 3], sa1);
+                    sb1 = __builtin_fmaf(bm[g - 1].w, dst[4 * g + 3], sb1);
                 }
-                const float u = __builtin_fmaf(-cur.gm, pk[i / 4][i % 4], vj);  // v - gamma R0 k
-                const float delta = __builtin_fmaf(cur.bn, u, -(sa0 + sa1));     // beta u - sum A delta
-                const float ov = __builtin_fmaf(cur.cn, delta, __builtin_fmaf(cur.gq, pq[i / 4][i % 4], sb0 + sb1));
-                dst[cur.d < D ? cur.d : D] = delta;  // uniform index: an indexed register write
+                const float gm = cu.w0.w, gq = QKN ? cu.w1.y : cu.w0.w;
+                const float u = __builtin_fmaf(-gm, pk[i / 4][i % 4], vj);             // v - gamma R0 k
+                const float delta = __builtin_fmaf(cu.w0.z, u, -(sa0 + sa1));          // beta u - sum A delta
+                const float ov = __builtin_fmaf(cu.w1.x, delta, __builtin_fmaf(gq, pq[i / 4][i % 4], sb0 + sb1));
+                dst[d < D ? d : D] = delta;            // uniform index: an indexed register write
                 vs[n * 64 + pc] = f32_to_bf16(ov);     // over the consumed value entry
             }
         };
