@@ -408,7 +408,11 @@ def test_fused_conv_rejects_bad_arguments():
     wy, _b1 = _desc(policy=L.LUMO_POLICY_WY)
     paths, _b2 = _desc(policy=L.LUMO_POLICY_PATHS)
     ok = _dims(h_k=2, h_v=4, d_k=128, d_v=128, op_dtype=L.LUMO_BF16)
-    assert _fused(_dims(h_k=2, h_v=6, d_k=128, d_v=128, op_dtype=L.LUMO_BF16), wy) == L.LUMO_EUNSUPPORTED
+    # the fused conv serves two value heads per key head (one block per key-head slice of
+    # the history); groups of 1, 3 and 4 are refused with a status, nothing launched
+    for h_k, h_v in ((2, 2), (2, 6), (1, 4)):
+        assert _fused(_dims(h_k=h_k, h_v=h_v, d_k=128, d_v=128, op_dtype=L.LUMO_BF16), wy) == L.LUMO_EUNSUPPORTED
+        assert "h_v / h_k = 2 only" in L.lumo_last_error()
     assert _fused(ok, wy, channels=1000) == L.LUMO_ESHAPE
     assert _fused(ok, wy, act=2) == L.LUMO_EINVAL
     assert _fused(ok, wy, max_path=0) == L.LUMO_EINVAL
