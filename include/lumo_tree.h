@@ -84,11 +84,13 @@ typedef enum {
      * states, shared prefixes recomputed. No workspace. */
     LUMO_POLICY_RECOMPUTE = 2,
     /* Tree WY form: R_t = gamma_t R0 + sum over ancestors of decayed rank-1
-     * terms; the R0 [K | Q] products run on MFMA (R0 as bf16 hi + lo), the
-     * ancestor-masked triangular system on the vector units. One launch, no
-     * workspace, no state dump. bf16 operands, d_k = d_v = 128, paths of at most
-     * 17 nodes. Outputs agree with the sequential schedules to rounding, not
-     * bitwise. */
+     * terms. With bf16 operands, d_k = d_v = 128 and paths of at most 17 nodes the
+     * R0 [K | Q] products run on MFMA (R0 as bf16 hi + lo) and the ancestor-masked
+     * triangular system on the vector units; other shapes (fp32 operands, d_k in
+     * {16, 32, 64}, d_v below 128, paths of 18 to 32 nodes) run the same form on the
+     * vector units in fp32. Paths longer than 32 nodes are refused
+     * (LUMO_EUNSUPPORTED). One launch, no workspace, no state dump. Outputs agree
+     * with the sequential schedules to rounding, not bitwise. */
     LUMO_POLICY_WY = 3
 } lumo_policy;
 
@@ -280,8 +282,8 @@ lumo_status lumo_tree_gdn_verify(const lumo_gdn_dims* dims, const lumo_tree_desc
 
 /*
  * lumo_tree_gdn_verify_prep - lumo_tree_gdn_verify with the operands prepared as
- * `prep` says (nullable; Sec. IV-B). Takes a plan built for LUMO_POLICY_WY (bf16
- * operands, d_k = d_v = 128, paths of at most 17 nodes) or LUMO_POLICY_RECOMPUTE (the
+ * `prep` says (nullable; Sec. IV-B). Takes a plan built for LUMO_POLICY_WY (paths of
+ * at most 32 nodes, the shapes of that policy) or LUMO_POLICY_RECOMPUTE (the
  * sequential scan of every path from the pre-tree state: any supported shape, either
  * operand type, any depth; bitwise what lumo_gdn_commit_prep publishes for the same
  * path); plans that export cut states to a workspace (PATHS, TWO_LEVEL) are refused
