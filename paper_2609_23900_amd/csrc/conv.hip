@@ -7,7 +7,8 @@
 // then one cast. One thread handles 8 contiguous channels of one layer for a run of
 // nodes; loads and stores are 16-byte vectors, the thread's taps stay in registers,
 // and every x row is read by at most four nodes (itself and three descendants, which
-// follow it closely in node order, so the re-reads hit L2). HBM-bound.
+// follow it closely in each request's depth-first preorder, so most re-reads hit L2).
+// HBM-bound.
 #include "device_common.h"
 #include "internal.h"
 #include "launch.h"
@@ -17,7 +18,7 @@ namespace {
 
 struct ConvParams {
     const int32_t* blob;
-    int32_t o_req, o_row, o_conv_src;
+    int32_t o_req, o_row, o_conv_src, o_node_off, o_dfs;
     int32_t total_nodes, total_rows, n_layers, channels, n_cchunks, act;
     int32_t run;  // nodes per block (1..kNodesPerBlock)
     const void* x;
@@ -127,7 +128,7 @@ __global__ __launch_bounds__(256) void hist_pend_kernel(HistPend q, int n_layers
 // One block: one layer, 2048 channels (8 per thread), a run of up to kNodesPerBlock
 // nodes (shorter runs when the grid would otherwise leave CUs idle).
 // The taps and bias of the thread's channels stay in registers across the run; the
-// window rows of consecutive nodes (parents, grandparents) are mostly L2 hits.
+// window rows of nodes close in preorder (parents, grandparents) are mostly L2 hits.
 constexpr int kNodesPerBlock = 32;
 
 template <int OPT>
@@ -159,10 +160,14 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
     const int n0 = grp * p.run;
     const int nn = min(p.total_nodes, n0 + p.run) - n0;
     // node info of the run, one node per lane (lanes 0..31 of every wave), broadcast
-    // per node with readlane so the window loads depend on nothing but registers
+    // per node with readlane so the window loads depend on nothing but registers. Runs
+    // cover each request's nodes in depth-first preorder (positions node_off[r] ..), so
+    // a node's parent and grandparents were loaded shortly before, by this run or a
+    // neighbouring one on the same XCD.
     const int li = (int)threadIdx.x & (kNodesPerBlock - 1);
-    const int mine = n0 + (li < nn ? li : 0);
-    const int i_req = p.blob[p.o_req + mine];
+    const int pos = n0 + (li < nn ? li : 0);
+    const int i_req = p.blob[p.o_req + pos];
+    const int mine = p.blob[p.o_node_off + i_req] + p.blob[p.o_dfs + pos];
     const int i_row = p.blob[p.o_row + mine];
     int i_src[4];
 #pragma unroll
@@ -431,6 +436,8 @@ hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.o_req = pl.o_req;
     p.o_row = pl.o_row;
     p.o_conv_src = pl.o_conv_src;
+    p.o_node_off = pl.o_node_off;
+    p.o_dfs = pl.o_dfs;
     p.total_nodes = pl.total_nodes;
     p.total_rows = pl.total_rows;
     p.n_layers = d.n_layers;
