@@ -174,8 +174,13 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
     float* walpha = alphas[wave];
     const bool rec_writer = !SHR || (wave & 1) == 0;  // uniform
 
-    int blk = xcd_remap(blockIdx.x, gridDim.x);
+    // Blocks that share a key head's rows (pairs > 1) are kept on one XCD, whose L2
+    // then serves the rows to all of them. With one block per key head nothing is
+    // shared, and the plain dispatch order spreads consecutive requests, which may be
+    // of very different sizes, over all XCDs instead of giving each XCD its own run of
+    // requests.
     const int pairs = p.group / NVH;
+    int blk = pairs > 1 ? xcd_remap(blockIdx.x, gridDim.x) : (int)blockIdx.x;
     const int pp = blk % pairs;
     blk /= pairs;
     const int hk = blk % p.h_k;
