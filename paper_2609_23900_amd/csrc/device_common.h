@@ -179,4 +179,16 @@ __device__ __forceinline__ int xcd_remap(int p, int nb) {
     return (xcd < extra ? xcd * (base + 1) : extra * (base + 1) + (xcd - extra) * base) + local;
 }
 
+// Units of G consecutive logical blocks (blocks that share rows), each unit on one XCD
+// and consecutive units on different XCDs: in every window of 8 G dispatched blocks,
+// XCD x (blocks p = x mod 8) receives unit 8 w + x whole. Blocks of a last, partial
+// window keep their order.
+__device__ __forceinline__ int xcd_units(int p, int nb, int G) {
+    constexpr int X = 8;
+    const int win = X * G;
+    if (p >= (nb / win) * win) return p;
+    const int w = p / win, x = p % X, m = (p % win) / X;
+    return (w * X + x) * G + m;
+}
+
 }  // namespace lumo

@@ -174,13 +174,13 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
     float* walpha = alphas[wave];
     const bool rec_writer = !SHR || (wave & 1) == 0;  // uniform
 
-    // Blocks that share a key head's rows (pairs > 1) are kept on one XCD, whose L2
-    // then serves the rows to all of them. With one block per key head nothing is
-    // shared, and the plain dispatch order spreads consecutive requests, which may be
-    // of very different sizes, over all XCDs instead of giving each XCD its own run of
-    // requests.
+    // The blocks of one (request, layer) share its gate rows (g and beta of every head
+    // of a row sit in one line) and, with several blocks per key head, the key and
+    // query rows: they run on one XCD, whose L2 serves them to all. Consecutive
+    // (request, layer) units go to different XCDs, so requests of very different sizes
+    // (a run of chains, then a run of trees) spread over the whole device.
     const int pairs = p.group / NVH;
-    int blk = pairs > 1 ? xcd_remap(blockIdx.x, gridDim.x) : (int)blockIdx.x;
+    int blk = xcd_units((int)blockIdx.x, (int)gridDim.x, p.h_k * pairs);
     const int pp = blk % pairs;
     blk /= pairs;
     const int hk = blk % p.h_k;
