@@ -142,26 +142,39 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast
 // QKN: every query and key row x is used as x / sqrt(|x|^2 + eps) (Sec. IV-B). The
 // bf16 rows stay as they are in LDS and the MFMA products; the per-row factors scale
 // the Gram entries, R0 k, R0 q and k.q in the records, and the pending path's keys.
-template <int D, int NVH, bool PEND, bool QKN, bool CONV>
-__global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void wy_kernel(WyParams p, const uint16_t* __restrict__ kmat,
+// CW = 32 (small grids): four waves per value head, 32 state columns each, so that a
+// call with fewer blocks than CUs still has a wave on every SIMD and each wave's walk
+// (state slab, publication, products) is half as long. A wave's lanes l and l + 32
+// then hold the same column: l < 32 forms the ancestor sum of A and the delta, l >= 32
+// the sum of B and the output. Every value is computed with the operations, and in the
+// order, of the 64-column form, so both give the same bits.
+template <int D, int NVH, bool PEND, bool QKN, bool CONV, int CW = 64>
+__global__ __launch_bounds__(64 * (CW == 64 ? 2 : 4) * NVH, (D == 8 || CW == 32 || (!CONV && NVH == 2)) ? 2 : 1) void wy_kernel(WyParams p, const uint16_t* __restrict__ kmat,
                                                     const uint16_t* __restrict__ qmat,
                                                     const uint16_t* __restrict__ vmat, const float* __restrict__ gmat,
                                                     const float* __restrict__ bmat, const float* __restrict__ state0,
                                                     uint16_t* __restrict__ out, PendParams pd, ConvFuseParams cf) {
-    static_assert(!CONV || (NVH == 2 && PEND), "the fused conv serves two value heads per block, with publication");
+    static_assert(!CONV || (NVH == 2 && PEND && CW == 64), "the fused conv serves two value heads per block, with publication");
+    static_assert(CW == 64 || (CW == 32 && NVH == 1), "32-column waves serve one value head per block");
     constexpr int W = Rec<D>::kWords;
-    constexpr int nthr = 128 * NVH;
-    // the waves of a value head share its records (D = 16 without the fused conv)
-    constexpr bool SHR = D == 16 && !CONV;
+    constexpr int WPH = kD / CW;       // waves per value head
+    constexpr int NCT = CW / 16;       // 16-column MFMA tiles per wave
+    constexpr int SPN = CW / 8;        // 16-byte value slots per node and wave
+    constexpr bool AB = CW == 32;      // lane halves split the recursion's sums
+    constexpr int NW = WPH * NVH;      // waves per block
+    constexpr int nthr = 64 * NW;
+    // the waves of a value head share its records (D = 16 without the fused conv, and
+    // the four waves of 32 columns)
+    constexpr bool SHR = (D == 16 && !CONV) || AB;
     // LDS, one object per role: the compiler orders LDS reads after the direct
     // global-to-LDS copies only where they may touch the same object.
     __shared__ KQTile tile;                        // block: chunk keys, queries, path-stack keys
     __shared__ __attribute__((aligned(16))) float G[kCand * kGS];  // block: Gram [candidate][chunk key | chunk query]
     // per wave (SHR: per value head): the chunk's coefficient records
-    __shared__ __attribute__((aligned(16))) float recs[SHR ? NVH : 2 * NVH][kTile * W];
-    __shared__ float alphas[2 * NVH][64];          // per wave: exp(g) of the candidates
+    __shared__ __attribute__((aligned(16))) float recs[SHR ? NVH : NW][kTile * W];
+    __shared__ float alphas[NW][64];               // per wave: exp(g) of the candidates
     // per wave: value rows, then outputs; double-buffered (CONV: single, for the caches)
-    __shared__ uint4 vbufs[2 * NVH][CONV ? 1 : 2][kTile * 8];
+    __shared__ uint4 vbufs[NW][CONV ? 1 : 2][kTile * SPN];
     // CONV: raw x of the current root path by depth (rows 0..2 the history, row 3 + d
     // depth d), two channels per thread; conv outputs of the root path's keys by depth
     __shared__ uint32_t rawc[CONV ? D + 4 : 1][CONV ? nthr : 1];
@@ -170,9 +183,9 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
     const int tid = (int)threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: head and half in SGPRs
     const int lane = tid & 63;
-    float* wrec = recs[SHR ? wave >> 1 : wave];
+    float* wrec = recs[SHR ? wave / WPH : wave];
     float* walpha = alphas[wave];
-    const bool rec_writer = !SHR || (wave & 1) == 0;  // uniform
+    const bool rec_writer = !SHR || wave % WPH == 0;  // uniform
 
     // The blocks of one (request, layer) share its gate rows (g and beta of every head
     // of a row sit in one line) and, with several blocks per key head, the key and
@@ -187,16 +200,18 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
     blk /= p.h_k;
     const int l = blk % p.n_layers;
     const int r = blk / p.n_layers;
-    const int h = hk * p.group + pp * NVH + (wave >> 1);
-    const int j0 = 64 * (wave & 1);
+    const int h = hk * p.group + pp * NVH + wave / WPH;
+    const int j0 = CW * (wave % WPH);
     const bool rawg = p.raw_gates != 0;  // uniform
     const float alog = rawg ? p.a_log[l * p.h_v + h] : 0.f;
     const float dtb = rawg ? p.dt_bias[l * p.h_v + h] : 0.f;
     const int base = p.blob[p.o_node_off + r];
     const int N = p.blob[p.o_node_off + r + 1] - base;
     int plen = 0;  // pending path length; an empty or invalid path leaves the state as it is
+    int pp0 = 0;   // node of pending path entry min(lane % kPend, max_path - 1), loaded with the length
     if constexpr (PEND) {
         plen = pd.path_len[r];
+        pp0 = pd.path_out[(long)r * pd.max_path + min(lane % kPend, pd.max_path - 1)];
         if (plen > pd.max_path || pd.blob[pd.o_node_off + r + 1] <= pd.blob[pd.o_node_off + r]) plen = 0;
     }
     if (N <= 0 && plen <= 0) return;  // uniform over the block
@@ -285,32 +300,35 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
     };
-    // The recursion leaves node n's output (bf16, this wave's 64 columns) in place of its
+    // The recursion leaves node n's output (bf16, this wave's CW columns) in place of its
     // value entries; a chunk's output rows then go out as 16-byte stores (slot q: node
-    // q / 8, columns j0 + 8 (q % 8) ..), rows taken from the records. Padding slots repeat
-    // the last node's row and values. nodes = 16 when the second half was not computed.
+    // q / SPN, columns j0 + 8 (q % SPN) ..), rows taken from the records. Padding slots
+    // repeat the last node's row and values. nodes = 16 when the second half was not
+    // computed.
+    constexpr int kVRounds = kTile * SPN / 64;
     auto flush = [&](const uint4* ob, int nodes) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            if (16 * i >= 2 * nodes) break;  // uniform
+        for (int i = 0; i < kVRounds; ++i) {
+            if (64 * i >= nodes * SPN) break;  // uniform
             const int q = 64 * i + ln;
             const uint4 val = ob[q];
-            const int rn = __float_as_int(wrec[(q >> 3) * W]);
-            *reinterpret_cast<uint4*>(out + ((krow0 + rn) * p.h_v + h) * kD + j0 + 8 * (q & 7)) = val;
+            const int rn = __float_as_int(wrec[(q / SPN) * W]);
+            *reinterpret_cast<uint4*>(out + ((krow0 + rn) * p.h_v + h) * kD + j0 + 8 * (q % SPN)) = val;
         }
     };
-    // the wave's value rows: slot q = 64 i + lane holds node q / 8, columns j0 + 8 (q % 8) .. + 7
+    // the wave's value rows: slot q = 64 i + lane holds node q / SPN, columns
+    // j0 + 8 (q % SPN) .. + 7
     auto v_issue = [&](const Rows& rw, uint4* dst) {
         int ln = lane;
         asm volatile("" : "+v"(ln));  // recomputed per call rather than kept live across the loop
-        int rn[4];
+        int rn[kVRounds];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) rn[i] = __shfl(rw.n, (64 * i + ln) >> 3);
+        for (int i = 0; i < kVRounds; ++i) rn[i] = __shfl(rw.n, (64 * i + ln) / SPN);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < kVRounds; ++i) {
             const int q = 64 * i + ln;
-            const uint16_t* src = CONV ? cf.x + (krow0 + rn[i]) * xc + voff + h * kD + j0 + 8 * (q & 7)
-                                       : vmat + ((krow0 + rn[i]) * p.h_v + h) * kD + j0 + 8 * (q & 7);
+            const uint16_t* src = CONV ? cf.x + (krow0 + rn[i]) * xc + voff + h * kD + j0 + 8 * (q % SPN)
+                                       : vmat + ((krow0 + rn[i]) * p.h_v + h) * kD + j0 + 8 * (q % SPN);
             __builtin_amdgcn_global_load_lds(src, (lds_void*)&dst[64 * i], 16, 0, 0);
         }
     };
@@ -424,21 +442,27 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
     };
 
     // R0 as B fragments of the 16x16x32 MFMA: column n = lane%16 of tile ct is state
-    // column j0 + 4 n + ct, and key block kb holds keys 32 kb + 8 (lane/16) + e. A lane
-    // thus holds 4 adjacent columns of each of its keys: one 16-byte load (and store)
-    // per key. After the lane exchange of the products, lane l serves state column
-    // j0 + 4 (l % 16) + l / 16.
+    // column j0 + NCT n + ct, and key block kb holds keys 32 kb + 8 (lane/16) + e. A lane
+    // thus holds NCT adjacent columns of each of its keys: one 16-byte (CW = 32: 8-byte)
+    // load and store per key. After the lane exchange of the products, lane l serves
+    // state column j0 + pc, pc = NCT (l % 16) + (l / 16) % NCT.
     const float* S = state0 + (((long)r * p.n_layers + l) * p.h_v + h) * (long)(kD * kD);
-    const float* Sl = S + (long)(8 * (lane / 16)) * kD + j0 + 4 * (lane % 16);
-    uint32_t raw[4][kD / 32][8];
+    const float* Sl = S + (long)(8 * (lane / 16)) * kD + j0 + NCT * (lane % 16);
+    uint32_t raw[NCT][kD / 32][8];
     auto slab_load = [&](int kb) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            const uint4 w = *reinterpret_cast<const uint4*>(Sl + (long)(32 * kb + e) * kD);
-            raw[0][kb][e] = w.x;
-            raw[1][kb][e] = w.y;
-            raw[2][kb][e] = w.z;
-            raw[3][kb][e] = w.w;
+            if constexpr (NCT == 4) {
+                const uint4 w = *reinterpret_cast<const uint4*>(Sl + (long)(32 * kb + e) * kD);
+                raw[0][kb][e] = w.x;
+                raw[1][kb][e] = w.y;
+                raw[2][kb][e] = w.z;
+                raw[3][kb][e] = w.w;
+            } else {
+                const uint2 w = *reinterpret_cast<const uint2*>(Sl + (long)(32 * kb + e) * kD);
+                raw[0][kb][e] = w.x;
+                raw[1][kb][e] = w.y;
+            }
         }
     };
     // The chunk's rows are loaded first and half the state slab behind them, so that the
@@ -456,10 +480,13 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
         const int32_t* ppath = pd.path_out + (long)r * pd.max_path;
         const long prow0 = (long)l * pd.total_rows;
         uint4* kst = reinterpret_cast<uint4*>(G);       // kPend key rows x 16 slots
-        // kPend entries x 64 values (8 slots) in the record space; with shared records
-        // each wave of the head takes its own half of it
-        static_assert(!SHR || kTile * W >= 2 * (kPend * 64 / 2), "two staging areas fit one record buffer");
-        float* vstage = wrec + (SHR ? (wave & 1) * (kPend * 64 / 2) : 0);
+        // kPend entries x CW values (SPN slots) in the record space; with shared records
+        // each wave of the head takes its own half of it; 32-column waves use their second
+        // value buffer (filled only by the first chunk's loop)
+        static_assert(AB || !SHR || kTile * W >= 2 * (kPend * 64 / 2), "two staging areas fit one record buffer");
+        static_assert(!AB || kTile * SPN >= kPend * SPN, "the staging fits a value buffer");
+        float* vstage = AB ? reinterpret_cast<float*>(vbufs[wave][1])
+                           : wrec + (SHR ? (wave & 1) * (kPend * 64 / 2) : 0);
         uint4* vst = reinterpret_cast<uint4*>(vstage);
         const uint16_t* vsh = reinterpret_cast<const uint16_t*>(vstage);
         // CONV: this thread's channels of the old history (the chain conv's first window,
@@ -495,7 +522,10 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
         for (int e0 = 0; e0 < plen; e0 += kPend) {
             const int ne = min(plen - e0, kPend);
             if (e0 > 0) lds_barrier();  // every wave has read the previous entries' key rows
-            const int node = min(max(ppath[e0 + min(lane % kPend, ne - 1)], 0), pn - 1);
+            // entry e0 + min(lane % kPend, ne - 1); the first round's nodes were loaded at the start
+            const int pnode = e0 > 0 ? ppath[e0 + min(lane % kPend, ne - 1)]
+                                     : (lane % kPend < ne ? pp0 : __builtin_amdgcn_readlane(pp0, ne - 1));
+            const int node = min(max(pnode, 0), pn - 1);
             const int row = pd.blob[pd.o_row + pbase + node];
             const long gl = (prow0 + row) * p.h_v + h;
             float pgv = pd.g[gl], pb = pd.beta[gl];
@@ -504,9 +534,10 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
                 pb = raw_beta(pb);
             }
             const float pa = __expf(pgv);
-            int rv[kPend * 8 / 64];
+            constexpr int kPV = kPend * SPN / 64;  // value-staging rounds
+            int rv[kPV];
 #pragma unroll
-            for (int i = 0; i < kPend * 8 / 64; ++i) rv[i] = __shfl(row, (64 * i + lane) >> 3);
+            for (int i = 0; i < kPV; ++i) rv[i] = __shfl(row, (64 * i + lane) / SPN);
             constexpr int kKRounds = kPend * 16 / nthr;
 #pragma unroll
             for (int j = 0; j < kKRounds; ++j) {
@@ -521,10 +552,10 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
                 __builtin_amdgcn_global_load_lds(ks, (lds_void*)&kst[j * nthr + 64 * wave], 16, 0, 0);
             }
 #pragma unroll
-            for (int i = 0; i < kPend * 8 / 64; ++i) {
+            for (int i = 0; i < kPV; ++i) {
                 const int q = 64 * i + lane;
-                const uint16_t* vsrc = CONV ? cf.x_prev + (prow0 + rv[i]) * xc + voff + h * kD + j0 + 8 * (q & 7)
-                                            : pd.v + ((prow0 + rv[i]) * p.h_v + h) * kD + j0 + 8 * (q & 7);
+                const uint16_t* vsrc = CONV ? cf.x_prev + (prow0 + rv[i]) * xc + voff + h * kD + j0 + 8 * (q % SPN)
+                                            : pd.v + ((prow0 + rv[i]) * p.h_v + h) * kD + j0 + 8 * (q % SPN);
                 __builtin_amdgcn_global_load_lds(vsrc, (lds_void*)&vst[64 * i], 16, 0, 0);
             }
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -573,9 +604,9 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
                         }
                     sk = __builtin_amdgcn_rsqf(row_group_sum(ss0 + ss1) + p.qk_eps);
                 }
-                float dl[4];
+                float dl[NCT];
 #pragma unroll
-                for (int ct = 0; ct < 4; ++ct) {
+                for (int ct = 0; ct < NCT; ++ct) {
                     float s0 = 0.f, s1 = 0.f;
 #pragma unroll
                     for (int kb = 0; kb < kD / 32; ++kb)
@@ -585,11 +616,11 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
                             acc = __builtin_fmaf(__uint_as_float(raw[ct][kb][e8]), kf[kb][e8], acc);
                         }
                     const float u = row_group_sum(s0 + s1) * sk;
-                    const float vj = bf16_lo((uint32_t)vsh[e * 64 + 4 * (lane % 16) + ct]);
+                    const float vj = bf16_lo((uint32_t)vsh[e * CW + NCT * (lane % 16) + ct]);
                     dl[ct] = be * __builtin_fmaf(-ae, u, vj) * sk;
                 }
 #pragma unroll
-                for (int ct = 0; ct < 4; ++ct)
+                for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
                     for (int kb = 0; kb < kD / 32; ++kb)
 #pragma unroll
@@ -605,13 +636,17 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
             conv_cache_init(hn0, hn1, hn2);
         }
         float* Sw = pd.state + (((long)r * p.n_layers + l) * p.h_v + h) * (long)(kD * kD) +
-                    (long)(8 * (lane / 16)) * kD + j0 + 4 * (lane % 16);
+                    (long)(8 * (lane / 16)) * kD + j0 + NCT * (lane % 16);
 #pragma unroll
         for (int kb = 0; kb < kD / 32; ++kb)
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                *reinterpret_cast<uint4*>(Sw + (long)(32 * kb + e) * kD) =
-                    make_uint4(raw[0][kb][e], raw[1][kb][e], raw[2][kb][e], raw[3][kb][e]);
+            for (int e = 0; e < 8; ++e) {
+                if constexpr (NCT == 4)
+                    *reinterpret_cast<uint4*>(Sw + (long)(32 * kb + e) * kD) =
+                        make_uint4(raw[0][kb][e], raw[1][kb][e], raw[2][kb][e], raw[3][kb][e]);
+                else
+                    *reinterpret_cast<uint2*>(Sw + (long)(32 * kb + e) * kD) = make_uint2(raw[0][kb][e], raw[1][kb][e]);
+            }
     };
 
     Rows rowC, rowA;  // this chunk, the next
@@ -639,6 +674,8 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
         if (N > 0) rowC = lane_rows(0);
 #pragma unroll
         for (int kb = 0; kb < kD / 32; ++kb) slab_load(kb);
+        // (Staging the first chunk's rows before the publication was measured slower: its
+        // copies compete with the publication's.)
         pend_publish();
         if (N <= 0) return;  // uniform: nothing to verify for this request
         v_issue(rowC, vbufs[wave][0]);
@@ -647,11 +684,11 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
         rowA = N > kTile ? lane_rows(kTile) : rowC;
     }
 
-    bf16x8 bhi[4][kD / 32], blo[4][kD / 32];
+    bf16x8 bhi[NCT][kD / 32], blo[NCT][kD / 32];
     // Each fp32 value x is held as hi + lo: hi = x truncated to bf16, lo = the exact
     // remainder x - hi rounded to nearest bf16 (|x - hi - lo| <= 2^-15 |x|).
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
+    for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
         for (int kb = 0; kb < kD / 32; ++kb) {
             uint32_t hw[4], lw[4];
@@ -674,19 +711,22 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
     for (int m = 0; m <= D; ++m) dst[m] = 0.f;
     // Gram tiles of this wave: rows = chunk keys (mt 0, Gram rows 16..47) or path-stack
     // keys (mt 1, Gram rows 0..15); columns = the chunk's keys (nt 0) or queries (nt 1)
-    constexpr int NT = NVH == 2 ? 1 : 2;
-    const int mt = NVH == 2 ? (wave >> 1) : wave;
+    constexpr int NT = NW == 4 ? 1 : 2;
+    const int mt = NW == 4 ? (wave >> 1) : wave;
 
-    // R0 [k | q] of the 16 nodes of half hf of the chunk against the wave's 64 columns,
+    // R0 [k | q] of the 16 nodes of half hf of the chunk against the wave's CW columns,
     // then the 4 x 4 exchange of lane groups (permlane32, then permlane16 swaps) that
-    // leaves lane l with column j0 + l: pk[b][i], pq[b][i] belong to node 16 hf + 4 b + i.
+    // leaves lane l with column j0 + pc: pk[b][i], pq[b][i] belong to node 16 hf + 4 b + i.
+    // CW = 32: pk holds the k products of tiles 0, 1 and then the q products of tiles
+    // 0, 1 (pq is unused), so that after the exchange lane l < 32 holds R0 k and lane
+    // l + 32 R0 q of the same column.
     auto half_products = [&](int hf, f32x4 (&pk)[4], f32x4 (&pq)[4]) {
 #pragma unroll
         for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 pk[ct][i] = 0.f;
-                pq[ct][i] = 0.f;
+                if constexpr (!AB) pq[ct][i] = 0.f;
             }
         const int nrow = 16 * hf + ln % 16;  // A rows: the half's nodes
 #pragma unroll
@@ -694,8 +734,18 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
             const int sw = (4 * kb + ln / 16) ^ (nrow & 15);
             const bf16x8 fk = as_bf16x8(tile.slot[nrow * 16 + sw]);
             const bf16x8 fq = as_bf16x8(tile.slot[(kTile + nrow) * 16 + sw]);
+            if constexpr (AB) {
 #pragma unroll
-            for (int ct = 0; ct < 4; ++ct) {
+                for (int ct = 0; ct < NCT; ++ct) {
+                    pk[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fk, bhi[ct][kb], pk[ct], 0, 0, 0);
+                    pk[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fk, blo[ct][kb], pk[ct], 0, 0, 0);
+                    pk[NCT + ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fq, bhi[ct][kb], pk[NCT + ct], 0, 0, 0);
+                    pk[NCT + ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fq, blo[ct][kb], pk[NCT + ct], 0, 0, 0);
+                }
+                continue;
+            }
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) {
                 pk[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fk, bhi[ct][kb], pk[ct], 0, 0, 0);
                 pk[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fk, blo[ct][kb], pk[ct], 0, 0, 0);
                 pq[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fq, bhi[ct][kb], pq[ct], 0, 0, 0);
@@ -746,7 +796,7 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
         asm volatile("" : "+v"(ln));
         tn = ln % kTile;
         const int kb0 = ln / kTile;  // key block offset within a 16-key step (32x32x16 Gram)
-        const int pc = 4 * (ln % 16) + ln / 16;  // this lane's state column (after the exchange)
+        const int pc = NCT * (ln % 16) + (ln / 16) % NCT;  // this lane's state column (after the exchange)
         const int arow = mt == 0 ? tn : 2 * kTile + (tn & (kStack - 1));
         if constexpr (QKN) {
             // 1/sqrt(|x|^2 + eps) of every tile row: 8 lanes per row, 16 elements each
@@ -790,7 +840,7 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
                 const bf16x8 fa = as_bf16x8(tile.slot[arow * 16 + sw]);
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
-                    const int nt = NVH == 2 ? (wave & 1) : i;
+                    const int nt = NW == 4 ? (wave & 1) : i;
                     const bf16x8 fb = as_bf16x8(tile.slot[(nt * kTile + tn) * 16 + sw]);
                     gacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, gacc[i], 0, 0, 0);
                 }
@@ -798,7 +848,7 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
             // MFMA 32x32 output: lane holds column lane%32, rows 8(e/4) + 4(lane/32) + e%4
 #pragma unroll
             for (int i = 0; i < NT; ++i) {
-                const int nt = NVH == 2 ? (wave & 1) : i;
+                const int nt = NW == 4 ? (wave & 1) : i;
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
                     const int row = 8 * (e / 4) + 4 * (ln / kTile) + e % 4;
@@ -881,7 +931,7 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
             h.w1 = *reinterpret_cast<const float4*>(cf + 4);
             h.a0 = *reinterpret_cast<const float4*>(cf + 8);
             h.b0 = *reinterpret_cast<const float4*>(cf + 8 + D);
-            h.vraw = vs[n * 64 + pc];
+            h.vraw = vs[n * CW + pc];
         };
         auto recursion = [&](int hf, const f32x4 (&pk)[4], const f32x4 (&pq)[4]) {
             RecHead nx;
@@ -936,12 +986,68 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
                 const float delta = __builtin_fmaf(cu.w0.z, u, -(sa0 + sa1));          // beta u - sum A delta
                 const float ov = __builtin_fmaf(cu.w1.x, delta, __builtin_fmaf(gq, pq[i / 4][i % 4], sb0 + sb1));
                 dst[d < D ? d : D] = delta;            // uniform index: an indexed register write
-                vs[n * 64 + pc] = f32_to_bf16(ov);     // over the consumed value entry
+                vs[n * CW + pc] = f32_to_bf16(ov);     // over the consumed value entry
+            }
+        };
+        // CW = 32: lane l < 32 forms the sum over A and the delta of its column, lane
+        // l + 32 the sum over B and the output, each from its own coefficient row; the
+        // delta reaches the upper half with one permlane32 swap. The record (head and
+        // every coefficient group) of the next node is loaded while the current one
+        // computes.
+        const bool hiB = ln >= kTile;
+        struct RecHeadAB {
+            float4 w0, w1, c[D / 4];
+            uint32_t vraw;
+        };
+        auto load_head_ab = [&](int n, RecHeadAB& hd) {
+            const float* cf = rec + n * W;
+            hd.w0 = *reinterpret_cast<const float4*>(cf);
+            hd.w1 = *reinterpret_cast<const float4*>(cf + 4);
+#pragma unroll
+            for (int g = 0; g < D / 4; ++g) hd.c[g] = *reinterpret_cast<const float4*>(cf + 8 + (hiB ? D : 0) + 4 * g);
+            hd.vraw = vs[n * CW + pc];
+        };
+        auto recursion_ab = [&](int hf, const f32x4 (&px)[4]) {
+            RecHeadAB nx;
+            load_head_ab(16 * hf, nx);
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int n = 16 * hf + i;
+                const RecHeadAB cu = nx;
+                if (i + 1 < 16) load_head_ab(n + 1, nx);
+                const int d = __builtin_amdgcn_readfirstlane(__float_as_int(cu.w0.y));  // uniform
+                const float vj = __uint_as_float(cu.vraw << 16);
+                // the partial sums of the 64-column form, over this lane's coefficients
+                float s0 = __builtin_fmaf(cu.c[0].x, dst[0], 0.f);
+                float s1 = __builtin_fmaf(cu.c[0].y, dst[1], 0.f);
+                s0 = __builtin_fmaf(cu.c[0].z, dst[2], s0);
+                s1 = __builtin_fmaf(cu.c[0].w, dst[3], s1);
+#pragma unroll
+                for (int g = 1; g < D / 4; ++g) {
+                    if (d <= 4 * g) break;
+                    s0 = __builtin_fmaf(cu.c[g].x, dst[4 * g], s0);
+                    s1 = __builtin_fmaf(cu.c[g].y, dst[4 * g + 1], s1);
+                    s0 = __builtin_fmaf(cu.c[g].z, dst[4 * g + 2], s0);
+                    s1 = __builtin_fmaf(cu.c[g].w, dst[4 * g + 3], s1);
+                }
+                const float sm = s0 + s1;
+                const float gm = cu.w0.w, gq = QKN ? cu.w1.y : cu.w0.w;
+                // lower half: v - gamma R0 k; upper half: gamma_q R0 q + sum B delta
+                const float t = __builtin_fmaf(hiB ? gq : -gm, px[i / 4][i % 4], hiB ? sm : vj);
+                const float da = __builtin_fmaf(cu.w0.z, t, -sm);  // lower half: beta u - sum A delta
+                const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(da), __float_as_uint(da), false, false);
+                const float delta = __uint_as_float(sw[0]);  // the lower half's delta in both halves
+                dst[d < D ? d : D] = delta;
+                if (hiB) vs[n * CW + pc] = f32_to_bf16(__builtin_fmaf(cu.w1.x, delta, t));
             }
         };
         exchange(pk);
-        exchange(pq);
-        recursion(0, pk, pq);
+        if constexpr (AB) {
+            recursion_ab(0, pk);
+        } else {
+            exchange(pq);
+            recursion(0, pk, pq);
+        }
         if (two) half_products(1, pk, pq);
         lds_barrier();  // every wave has read the tile: it may be refilled
         if (more) tile_issue(rowA);
@@ -950,8 +1056,12 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
         }
         if (two) {
             exchange(pk);
-            exchange(pq);
-            recursion(1, pk, pq);
+            if constexpr (AB) {
+                recursion_ab(1, pk);
+            } else {
+                exchange(pq);
+                recursion(1, pk, pq);
+            }
         }
         if constexpr (CONV) {  // single value buffer: out, then the next chunk's rows in
             flush(vbufs[wave][0], two ? kTile : kTile / 2);
@@ -969,11 +1079,11 @@ __global__ __launch_bounds__(256, (D == 8 || (!CONV && NVH == 2)) ? 2 : 1) void 
     }
 }
 
-template <int D, int NVH, bool PEND, bool QKN, bool CONV = false>
+template <int D, int NVH, bool PEND, bool QKN, bool CONV = false, int CW = 64>
 hipError_t launch_wy_kernel(const lumo_gdn_dims& d, const WyParams& p, const GdnArgs& a, hipStream_t s,
                             const PendParams& pp, const ConvFuseParams& cf = ConvFuseParams{}) {
     const long nb = (long)d.n_req * d.n_layers * d.h_k * (p.group / NVH);
-    hipLaunchKernelGGL((wy_kernel<D, NVH, PEND, QKN, CONV>), dim3((unsigned)nb), dim3(128 * NVH), 0, s, p,
+    hipLaunchKernelGGL((wy_kernel<D, NVH, PEND, QKN, CONV, CW>), dim3((unsigned)nb), dim3(64 * (128 / CW) * NVH), 0, s, p,
                        static_cast<const uint16_t*>(a.k), static_cast<const uint16_t*>(a.q),
                        static_cast<const uint16_t*>(a.v), a.g, a.beta, PEND ? pp.state : a.state0,
                        static_cast<uint16_t*>(a.o), pp, cf);
@@ -1008,14 +1118,15 @@ hipError_t launch_wy_d(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     const WyParams p = wy_params(d, desc, a);
     // one block per (request, layer, key head, pair of value heads): the pair's waves
     // share the staged key and query rows and the Gram. Grids of fewer pair blocks than
-    // CUs (one layer of a batch, few requests) take one value head per block instead:
-    // twice the blocks, each with half the work on its critical path, at the cost of a
-    // Gram per head.
+    // CUs (one layer of a batch, few requests) take one value head per block instead,
+    // with four waves of 32 columns: four times the waves, each with half the work on
+    // its critical path, at the cost of a Gram per head.
     const bool qkn = (a.prep.flags & LUMO_PREP_QK_NORM) != 0;
     const long pair_blocks = (long)d.n_req * d.n_layers * d.h_k * (p.group / 2);
     if (p.group % 2 == 0 && pair_blocks >= 256)
         return qkn ? launch_wy_kernel<D, 2, PEND, true>(d, p, a, s, pp) : launch_wy_kernel<D, 2, PEND, false>(d, p, a, s, pp);
-    return qkn ? launch_wy_kernel<D, 1, PEND, true>(d, p, a, s, pp) : launch_wy_kernel<D, 1, PEND, false>(d, p, a, s, pp);
+    return qkn ? launch_wy_kernel<D, 1, PEND, true, false, 32>(d, p, a, s, pp)
+               : launch_wy_kernel<D, 1, PEND, false, false, 32>(d, p, a, s, pp);
 }
 
 }  // namespace

@@ -619,6 +619,37 @@ def test_verify_pending_full_size_sampled():
     gu.check_outputs(wl, gu.to_np(st.o), inst, arrays=a2)
 
 
+
+@pytest.mark.parametrize("name,over", [("batched", {}), ("widedeep", dict(n_req=4, n_layers=4))])
+def test_layer_calls_equal_stacked_call(name, over):
+    """A call for one layer of these workloads has fewer blocks of two value heads than
+    the device has CUs and runs four 32-column waves per value head; the call for all
+    layers runs the 64-column pair blocks. Their outputs and published state banks must
+    agree bit for bit (same operations in the same order), on the deferred verification
+    of the batched workload (depth <= 8) and of four 256-node, 16-level trees."""
+    wl = configs.build(name, with_conv=False, **over)
+    st = GdnTreeStep.from_workload(wl, policy=L.LUMO_POLICY_WY, with_conv=False)
+    d = st.dims
+    assert d.n_req * d.n_layers * d.h_k >= 256 > d.n_req * d.h_k  # the two forms are taken
+    say(f"[gpu] one-layer calls against the stacked call, {name} {over}")
+    st.commit(defer=True)
+    st.verify_pending(st)
+    torch.cuda.synchronize()
+    o1 = torch.zeros_like(st.o)
+    s1 = st.state0.clone()
+    d1 = L.dims(d.n_req, 1, d.h_k, d.h_v, d.d_k, d.d_v, d.op_dtype)
+    for l in range(d.n_layers):
+        sl = s1[:, l:l + 1].contiguous()
+        t = {key: st.t[key][l] for key in ("q", "k", "v", "g", "beta")}
+        L.lumo_tree_gdn_verify_pending(d1, st.desc, t["q"], t["k"], t["v"], t["g"], t["beta"], sl, o1[l],
+                                       st.desc, st.max_path, st.path_out, st.path_len, t["k"], t["v"],
+                                       t["g"], t["beta"])
+        s1[:, l:l + 1] = sl
+    torch.cuda.synchronize()
+    assert not torch.equal(st.state, st.state0)  # paths were published
+    assert torch.equal(o1.view(torch.int16), st.o.view(torch.int16)), int((o1 != st.o).sum())
+    assert torch.equal(s1, st.state), int((s1 != st.state).sum())
+
 def test_deferred_loop_matches_eager_loop():
     """Three iterations: deferred publication + final flush agrees with eager commits
     (states to fp32 rounding, outputs to bf16 rounding) and with the oracle chain."""
