@@ -19,7 +19,7 @@ namespace {
 struct ConvParams {
     const int32_t* blob;
     int32_t o_req, o_row, o_conv_src, o_node_off, o_dfs;
-    int32_t total_nodes, total_rows, n_layers, channels, n_cchunks, act;
+    int32_t n_req, total_nodes, total_rows, n_layers, channels, n_cchunks, act;
     int32_t run;  // nodes per block (1..kNodesPerBlock)
     const void* x;
     const void* hist;
@@ -98,27 +98,42 @@ __device__ __forceinline__ const T* pend_hist_src(const HistPend& q, const T* hi
 }
 
 // Standalone publication, ahead of the run kernel: one block per (request, layer,
-// 2048 channels), 8 channels per thread.
+// 2048 channels), 8 channels per thread. The path's first 64 nodes are loaded with its
+// length (lane k: entry k), so a published entry's row is one dependent load away.
 template <int OPT>
 __global__ __launch_bounds__(256) void hist_pend_kernel(HistPend q, int n_layers, int channels, int n_cchunks) {
     using T = typename Op<OPT>::T;
     const int cc = blockIdx.x % n_cchunks;
     const int l = (blockIdx.x / n_cchunks) % n_layers;
     const int r = blockIdx.x / (n_cchunks * n_layers);
+    const int pe = q.path_out[(long)r * q.max_path + min((int)threadIdx.x & 63, q.max_path - 1)];
     const int len = pend_hist_len(q, r);
-    if (len <= 0) return;
-    const int c = (cc * 256 + (int)threadIdx.x) * 8;
-    if (c >= channels) return;
+    if (len <= 0) return;  // uniform
+    const int c0 = (cc * 256 + (int)threadIdx.x) * 8;
+    const bool has_c = c0 < channels;
+    const int c = has_c ? c0 : channels - 8;
     T* h = static_cast<T*>(q.hist) + (((long)r * n_layers + l) * 3) * channels;
-    const T* s0 = pend_hist_src<T>(q, h, r, l, len, 0, channels, c);
-    const T* s1 = pend_hist_src<T>(q, h, r, l, len, 1, channels, c);
-    const T* s2 = pend_hist_src<T>(q, h, r, l, len, 2, channels, c);
+    const int base = q.blob[q.o_node_off + r];
+    const int pn = q.blob[q.o_node_off + r + 1] - base;
+    // entry len + e of (history, previous x rows of the path), as pend_hist_src
+    auto src = [&](int e) -> const T* {
+        const int pos = len + e;  // uniform
+        if (pos < 3) return h + (long)pos * channels + c;
+        const int k = pos - 3;
+        const int nd = k < 64 ? __builtin_amdgcn_readlane(pe, k) : q.path_out[(long)r * q.max_path + k];
+        const int row = q.blob[q.o_row + base + min(max(nd, 0), pn - 1)];
+        return static_cast<const T*>(q.x_prev) + ((long)l * q.total_rows + row) * channels + c;
+    };
+    const T* s0 = src(0);
+    const T* s1 = src(1);
+    const T* s2 = src(2);
     constexpr int W = 16 / sizeof(T) >= 8 ? 1 : 2;  // 16-byte pieces per 8 channels
 #pragma unroll
     for (int w = 0; w < W; ++w) {  // each piece read whole before it is overwritten
         const uint4 v0 = reinterpret_cast<const uint4*>(s0)[w];
         const uint4 v1 = reinterpret_cast<const uint4*>(s1)[w];
         const uint4 v2 = reinterpret_cast<const uint4*>(s2)[w];
+        if (!has_c) continue;
         reinterpret_cast<uint4*>(h + c)[w] = v0;
         reinterpret_cast<uint4*>(h + (long)channels + c)[w] = v1;
         reinterpret_cast<uint4*>(h + 2L * channels + c)[w] = v2;
@@ -164,10 +179,14 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
     // cover each request's nodes in depth-first preorder (positions node_off[r] ..), so
     // a node's parent and grandparents were loaded shortly before, by this run or a
     // neighbouring one on the same XCD.
+    // (lane k also loads node_off[min(k, n_req)], so that a node's request offset is a
+    // lane exchange rather than a dependent load)
     const int li = (int)threadIdx.x & (kNodesPerBlock - 1);
     const int pos = n0 + (li < nn ? li : 0);
+    const int nof = p.blob[p.o_node_off + min((int)threadIdx.x & 63, p.n_req)];
     const int i_req = p.blob[p.o_req + pos];
-    const int mine = p.blob[p.o_node_off + i_req] + p.blob[p.o_dfs + pos];
+    const int nsh = __shfl(nof, i_req & 63);
+    const int mine = (i_req < 64 ? nsh : p.blob[p.o_node_off + i_req]) + p.blob[p.o_dfs + pos];
     const int i_row = p.blob[p.o_row + mine];
     int i_src[4];
 #pragma unroll
@@ -438,6 +457,7 @@ hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     p.o_conv_src = pl.o_conv_src;
     p.o_node_off = pl.o_node_off;
     p.o_dfs = pl.o_dfs;
+    p.n_req = d.n_req;
     p.total_nodes = pl.total_nodes;
     p.total_rows = pl.total_rows;
     p.n_layers = d.n_layers;
