@@ -15,8 +15,9 @@
 // column.
 //
 // One kernel. A block serves (request, layer, key head, NVH value heads of that key
-// head's group) with two wavefronts per value head (64 value columns each), and walks
-// the request's nodes in depth-first preorder, 32 positions (a chunk) at a time:
+// head's group) with two wavefronts per value head (64 value columns each; on small
+// grids four of 32 columns), and walks the request's nodes in depth-first preorder, 32
+// positions (a chunk) at a time:
 //   staging   one chunk ahead with direct global-to-LDS loads: the chunk's key and
 //             query rows plus the key rows of its path stack (the ancestry of its
 //             first node), shared by the block; each wave's value rows.
@@ -469,10 +470,11 @@ __global__ __launch_bounds__(64 * (CW == 64 ? 2 : 4) * NVH, (D == 8 || CW == 32 
     // row-dependent copies below wait for the rows only (16 loads issued after them)
     // while the slab is already in flight; then the other half.
     // Deferred publication: the pending path's key rows (block-shared, in the Gram's
-    // space) and the wave's value entries (in its record space) are staged kPend entries
-    // at a time; lane e holds entry e's decay and beta. Each entry applies
+    // space) and the wave's value entries (in its record space; with 32 columns in its
+    // second value buffer) are staged kPend entries at a time; lane e holds entry e's
+    // decay and beta. Each entry applies
     //   u = R k,  delta = beta (v - alpha u),  R <- alpha R + delta k
-    // to the slab in registers (lane: 4 columns x 32 keys; u summed over the four lane
+    // to the slab in registers (lane: NCT columns x 32 keys; u summed over the four lane
     // rows that share a column), then the slab is stored back.
     auto pend_publish = [&]() {
         const int pbase = pd.blob[pd.o_node_off + r];
