@@ -408,7 +408,7 @@ def cpu_baseline(wl, budget_s=12.0):
 
 def per_layer_launches(args, n_layers):
     """Library calls per per-layer step: conv and verify per layer (one fused call with
-    --fused), and the path derivation."""
+    --fused), and the commit."""
     return (1 if args.fused else 2) * n_layers + 1
 
 
@@ -416,9 +416,12 @@ def per_layer_graph_ms(args, st, stream):
     """The step as the paper's per-layer structure runs it: for every layer its own conv
     and verify calls (n_layers = 1), each layer with its own state bank
     [req][1][h_v][d_k][d_v] and conv history [req][1][3][C], the per-node tensors sliced
-    by layer, and one path derivation shared by all layers; with --fused one call per
-    layer does the conv and the verification. Ten steps are captured in one graph and
-    replayed. Returns ms per step."""
+    by layer. The commit is one launch for all layers: it derives the accepted path and
+    publishes it into every layer's conv history (lumo_gdn_commit_hist_layers), while
+    each layer's state is published by its next verification. With --fused one call per
+    layer does the conv, both publications and the verification, and the commit only
+    derives the path. Ten steps are captured in one graph and replayed. Returns ms per
+    step."""
     import torch
 
     import paper_2609_23900_amd as L
@@ -430,6 +433,7 @@ def per_layer_graph_ms(args, st, stream):
     hists = [st.hist[:, l:l + 1].contiguous() for l in range(nl)]
 
     bias = [None] * nl if st.bias is None else [st.bias[l] for l in range(nl)]
+    xs = [st.x[l] for l in range(nl)]
 
     def one_step():
         for l in range(nl):
@@ -440,12 +444,15 @@ def per_layer_graph_ms(args, st, stream):
                                                     states[l], st.o[l], st.desc, st.max_path, st.path_out,
                                                     st.path_len, x, g, b, None, st.prep)
                 continue
-            L.lumo_tree_conv_gather_pending(d1, st.desc, st.channels, x, hists[l], w, bias[l], st.act, y, st.desc,
-                                            st.max_path, st.path_out, st.path_len, x, None)
+            L.lumo_tree_conv_gather(d1, st.desc, st.channels, x, hists[l], w, bias[l], st.act, y)
             q, k, v = (st.t[key][l] for key in ("q", "k", "v"))
             L.lumo_tree_gdn_verify_pending(d1, st.desc, q, k, v, g, b, states[l], st.o[l], st.desc, st.max_path,
                                            st.path_out, st.path_len, k, v, g, b, None, st.prep)
-        st.commit(None, defer=True, with_conv=False)
+        if args.fused:
+            st.commit(None, defer=True, with_conv=False)
+        else:
+            L.lumo_gdn_commit_hist_layers(d, st.desc, st.max_path, st.accepted, st.path_out, st.path_len,
+                                          st.channels, xs, hists)
 
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())

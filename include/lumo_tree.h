@@ -11,7 +11,7 @@
  *                          native state, publish the convolution history
  * plus lumo_tree_attention (the attention layers' tree verification),
  * lumo_draft_select (the drafter's fused argmax / top-k selection), a
- * captured-graph form of the commit; lumo_tree_gdn_verify_pending and
+ * captured-graph form of the commit, a commit for per-layer history buffers; lumo_tree_gdn_verify_pending and
  * lumo_tree_conv_gather_pending, which fold the publication of one iteration (state
  * replay, conv history) into the verification and convolution of the next, and
  * lumo_tree_gdn_verify_conv_pending, which does both in one pass with the conv outputs
@@ -392,6 +392,36 @@ lumo_status lumo_gdn_commit(const lumo_gdn_dims* dims, const lumo_tree_desc* des
                             int32_t* path_len, const void* k, const void* v, const float* g,
                             const float* beta, float* state, int32_t channels, const void* x,
                             void* conv_hist, void* stream);
+
+/*
+ * lumo_gdn_commit_hist_layers - lumo_gdn_commit's path derivation and conv-history
+ * publication (Alg. 1 publication; device-selected path Sec. V-A; conv history Sec. V-C)
+ * for models that keep each layer's buffers apart and call the verification layer by
+ * layer (Sec. IV-B: every layer runs its own update kernel). One launch publishes the
+ * accepted path into the history of every layer; each layer's state is left to its
+ * next lumo_tree_gdn_verify_pending (deferred replay), and its conv then runs as
+ * lumo_tree_conv_gather on the published history.
+ *   dims, desc, max_path, accepted_node, path_out, path_len   as lumo_gdn_commit
+ *                  (dims->n_layers layers, at most 128, else LUMO_EUNSUPPORTED)
+ *   channels       positive multiple of 8 (LUMO_ESHAPE)
+ *   x_layers       HOST array of n_layers device pointers: layer l's x of this
+ *                  iteration, [total_rows][channels] of op_dtype (16-byte aligned;
+ *                  entries may be NULL when the tree has no nodes)
+ *   conv_hist_layers  HOST array of n_layers device pointers: layer l's history,
+ *                  [n_req][3][channels] of op_dtype (16-byte aligned), in/out:
+ *                  conv_hist_layers[l][r] becomes the last three entries of
+ *                  (conv_hist_layers[l][r], x_layers[l] rows of the path), in place
+ * The tables are read on the host during the call (the pointers are passed to the
+ * kernel by value), so they may be freed or reused when it returns. path_out, path_len
+ * and every history equal what lumo_gdn_commit writes with the same layers stacked,
+ * bit for bit; empty and invalid paths leave the histories unchanged. Histories of
+ * different layers must not overlap.
+ */
+lumo_status lumo_gdn_commit_hist_layers(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                        int32_t max_path, const int32_t* accepted_node,
+                                        int32_t* path_out, int32_t* path_len, int32_t channels,
+                                        const void* const* x_layers, void* const* conv_hist_layers,
+                                        void* stream);
 
 /*
  * lumo_gdn_commit_prep - lumo_gdn_commit whose replay uses the operands prepared as

@@ -124,6 +124,7 @@ def _load():
                                                     P, P, P, P]
     L.lumo_gdn_commit_prep.argtypes = [PD, PT, PP, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
     L.lumo_gdn_commit.argtypes = [PD, PT, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
+    L.lumo_gdn_commit_hist_layers.argtypes = [PD, PT, I32, P, P, P, I32, P, P, P]
     L.lumo_gdn_commit_graph_create.argtypes = [PD, PT, PP, I32, P, P, P, P, P, P, P, P, I32, P, P,
                                                ctypes.POINTER(ctypes.c_void_p)]
     L.lumo_gdn_commit_graph_launch.argtypes = [P, P]
@@ -133,7 +134,7 @@ def _load():
     L.lumo_version.restype = ctypes.c_char_p
     for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_conv_gather_pending", "lumo_tree_gdn_verify",
               "lumo_tree_gdn_verify_prep", "lumo_tree_gdn_verify_pending", "lumo_tree_gdn_verify_conv_pending", "lumo_gdn_commit",
-              "lumo_gdn_commit_prep", "lumo_tree_attention", "lumo_tree_attention_noalloc", "lumo_draft_select", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
+              "lumo_gdn_commit_prep", "lumo_gdn_commit_hist_layers", "lumo_tree_attention", "lumo_tree_attention_noalloc", "lumo_draft_select", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -280,6 +281,20 @@ def lumo_gdn_commit(d, desc: TreeDesc, max_path, accepted_node, path_out, path_l
                                 _dptr(accepted_node), _dptr(path_out), _dptr(path_len), _dptr(k),
                                 _dptr(v), _dptr(g), _dptr(beta), _dptr(state), int(channels),
                                 _dptr(x), _dptr(conv_hist), _stream(stream)))
+
+
+def lumo_gdn_commit_hist_layers(d, desc: TreeDesc, max_path, accepted_node, path_out, path_len, channels,
+                                x_layers, conv_hist_layers, stream=None):
+    """x_layers, conv_hist_layers: one device tensor per layer (None allowed in x_layers
+    when the tree has no nodes); the pointer tables are built here, on the host."""
+    n = len(conv_hist_layers)
+    if len(x_layers) != n:
+        raise ValueError("x_layers and conv_hist_layers need one entry per layer")
+    xt = (ctypes.c_void_p * max(n, 1))(*[_dptr(t) for t in x_layers])
+    ht = (ctypes.c_void_p * max(n, 1))(*[_dptr(t) for t in conv_hist_layers])
+    _check(_lib.lumo_gdn_commit_hist_layers(ctypes.byref(d), ctypes.byref(desc.desc), int(max_path),
+                                            _dptr(accepted_node), _dptr(path_out), _dptr(path_len),
+                                            int(channels), xt, ht, _stream(stream)))
 
 
 def lumo_gdn_commit_prep(d, desc: TreeDesc, prep: Prep | None, max_path, accepted_node, path_out,

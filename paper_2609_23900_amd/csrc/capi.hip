@@ -427,6 +427,40 @@ extern "C" lumo_status lumo_gdn_commit_prep(const lumo_gdn_dims* dims, const lum
     return LUMO_OK;
 }
 
+extern "C" lumo_status lumo_gdn_commit_hist_layers(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                                   int32_t max_path, const int32_t* accepted_node,
+                                                   int32_t* path_out, int32_t* path_len, int32_t channels,
+                                                   const void* const* x_layers, void* const* conv_hist_layers,
+                                                   void* stream) {
+    static const char* fn = "lumo_gdn_commit_hist_layers";
+    clear_error();
+    LUMO_TRY(check_dims(dims, fn));
+    LUMO_TRY(check_desc(dims, desc, fn));
+    if (max_path < 1 || max_path > 4096) return fail(LUMO_EINVAL, "%s: max_path %d (1..4096)", fn, max_path);
+    if (dims->n_layers > kMaxLayerTable)
+        return fail(LUMO_EUNSUPPORTED, "%s: n_layers %d (at most %d)", fn, dims->n_layers, kMaxLayerTable);
+    if (channels <= 0 || channels % 8)
+        return fail(LUMO_ESHAPE, "%s: channels %d must be a positive multiple of 8", fn, channels);
+    if (dims->n_req == 0) return LUMO_OK;
+    LUMO_TRY(check_ptr(accepted_node, fn, "accepted_node"));
+    LUMO_TRY(check_ptr(path_out, fn, "path_out"));
+    LUMO_TRY(check_ptr(path_len, fn, "path_len"));
+    if (!x_layers) return fail(LUMO_EINVAL, "%s: x_layers is NULL", fn);
+    if (!conv_hist_layers) return fail(LUMO_EINVAL, "%s: conv_hist_layers is NULL", fn);
+    for (int l = 0; l < dims->n_layers; ++l) {
+        if (desc->plan.total_nodes > 0 && (!x_layers[l] || !aligned16(x_layers[l])))
+            return fail(LUMO_EINVAL, "%s: x_layers[%d] is NULL or not 16-byte aligned", fn, l);
+        if (!conv_hist_layers[l] || !aligned16(conv_hist_layers[l]))
+            return fail(LUMO_EINVAL, "%s: conv_hist_layers[%d] is NULL or not 16-byte aligned", fn, l);
+    }
+    CommitArgs a{max_path, accepted_node, path_out, path_len, nullptr, nullptr, nullptr, nullptr, nullptr,
+                 channels, nullptr, nullptr};
+    hipError_t e = launch_commit_hist_layers(*dims, *desc, a, x_layers, conv_hist_layers,
+                                             static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
 namespace {
 lumo_status check_attn_dims(const lumo_attn_dims* d, const char* fn) {
     if (!d) return fail(LUMO_EINVAL, "%s: dims is NULL", fn);

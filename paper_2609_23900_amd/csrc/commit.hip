@@ -237,13 +237,11 @@ struct HistParams {
 // Every block of request r derives r's path length with the path kernel's rule; the
 // block (r, layer 0, channel chunk 0) also writes path_out and path_len. The history
 // needs only the path's last three nodes: the accepted node and its two nearest
-// ancestors, read straight from the parent table.
-template <int OPT>
-__global__ __launch_bounds__(256) void path_hist_kernel(PathParams pp, HistParams p) {
-    using T = typename Op<OPT>::T;
-    const int cc = blockIdx.x % p.n_cchunks;
-    const int l = (blockIdx.x / p.n_cchunks) % p.n_layers;
-    const int r = blockIdx.x / (p.n_cchunks * p.n_layers);
+// ancestors, read straight from the parent table. hist_rl is the history of (r, l)
+// ([3][channels]), x_l the rows of layer l ([rows][channels]).
+template <class T>
+__device__ __forceinline__ void path_hist_block(const PathParams& pp, const HistParams& p, int r, int l, int cc,
+                                                T* hist_rl, const T* x_l) {
     const int base = p.blob[p.o_node_off + r];
     const int n = p.blob[p.o_node_off + r + 1] - base;
     const int a = pp.accepted[r];
@@ -272,8 +270,6 @@ __global__ __launch_bounds__(256) void path_hist_kernel(PathParams pp, HistParam
     if (len <= 0) return;
     const int c = (cc * 256 + (int)threadIdx.x) * 8;
     if (c >= p.channels) return;
-    T* hist = static_cast<T*>(p.hist) + (((long)r * p.n_layers + l) * 3) * p.channels;
-    const T* x = static_cast<const T*>(p.x);
     // entry e of the new history is entry len + e of (history, x rows of the path); for
     // len + e >= 3 that is path node len + e - 3, the (2 - e)-th ancestor of the accepted node
     int node[3];
@@ -284,8 +280,8 @@ __global__ __launch_bounds__(256) void path_hist_kernel(PathParams pp, HistParam
 #pragma unroll
     for (int e = 0; e < 3; ++e) {
         const int pos = len + e;
-        src[e] = pos < 3 ? hist + (long)pos * p.channels + c
-                         : x + ((long)l * p.total_rows + p.blob[p.o_row + base + node[e]]) * p.channels + c;
+        src[e] = pos < 3 ? hist_rl + (long)pos * p.channels + c
+                         : x_l + (long)p.blob[p.o_row + base + node[e]] * p.channels + c;
     }
     constexpr int W = 16 / sizeof(T) >= 8 ? 1 : 2;  // 16-byte pieces per 8 channels
 #pragma unroll
@@ -293,10 +289,39 @@ __global__ __launch_bounds__(256) void path_hist_kernel(PathParams pp, HistParam
         const uint4 v0 = reinterpret_cast<const uint4*>(src[0])[w];
         const uint4 v1 = reinterpret_cast<const uint4*>(src[1])[w];
         const uint4 v2 = reinterpret_cast<const uint4*>(src[2])[w];
-        reinterpret_cast<uint4*>(hist + c)[w] = v0;
-        reinterpret_cast<uint4*>(hist + (long)p.channels + c)[w] = v1;
-        reinterpret_cast<uint4*>(hist + 2L * p.channels + c)[w] = v2;
+        reinterpret_cast<uint4*>(hist_rl + c)[w] = v0;
+        reinterpret_cast<uint4*>(hist_rl + (long)p.channels + c)[w] = v1;
+        reinterpret_cast<uint4*>(hist_rl + 2L * p.channels + c)[w] = v2;
     }
+}
+
+// Stacked operands: history [n_req][n_layers][3][channels], x [n_layers][rows][channels].
+template <int OPT>
+__global__ __launch_bounds__(256) void path_hist_kernel(PathParams pp, HistParams p) {
+    using T = typename Op<OPT>::T;
+    const int cc = blockIdx.x % p.n_cchunks;
+    const int l = (blockIdx.x / p.n_cchunks) % p.n_layers;
+    const int r = blockIdx.x / (p.n_cchunks * p.n_layers);
+    T* hist = static_cast<T*>(p.hist) + (((long)r * p.n_layers + l) * 3) * p.channels;
+    const T* x = static_cast<const T*>(p.x) + (long)l * p.total_rows * p.channels;
+    path_hist_block<T>(pp, p, r, l, cc, hist, x);
+}
+
+// Each layer's own buffers, passed by value: history [n_req][3][channels] and
+// x [rows][channels] of layer l.
+struct LayerTable {
+    const void* x[kMaxLayerTable];
+    void* hist[kMaxLayerTable];
+};
+
+template <int OPT>
+__global__ __launch_bounds__(256) void path_hist_layers_kernel(PathParams pp, HistParams p, LayerTable lt) {
+    using T = typename Op<OPT>::T;
+    const int cc = blockIdx.x % p.n_cchunks;
+    const int l = (blockIdx.x / p.n_cchunks) % p.n_layers;
+    const int r = blockIdx.x / (p.n_cchunks * p.n_layers);
+    T* hist = static_cast<T*>(lt.hist[l]) + (long)r * 3 * p.channels;
+    path_hist_block<T>(pp, p, r, l, cc, hist, static_cast<const T*>(lt.x[l]));
 }
 
 template <int DK, int OPT>
@@ -368,6 +393,36 @@ hipError_t launch_commit(const lumo_gdn_dims& d, const lumo_tree_desc& desc, con
     }
 
     return e;
+}
+
+hipError_t launch_commit_hist_layers(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const CommitArgs& a,
+                                     const void* const* x_layers, void* const* hist_layers, hipStream_t s) {
+    const lumo_plan& pl = desc.plan;
+    if (d.n_req == 0) return hipSuccess;
+    if (d.n_layers > kMaxLayerTable) return hipErrorInvalidValue;
+    PathParams pp{desc.blob, pl.o_node_off, pl.o_parent, pl.o_depth, d.n_req, a.max_path,
+                  a.accepted, a.path_out, a.path_len};
+    HistParams hp;
+    hp.blob = desc.blob;
+    hp.o_node_off = pl.o_node_off;
+    hp.o_row = pl.o_row;
+    hp.n_layers = d.n_layers;
+    hp.total_rows = pl.total_rows;
+    hp.channels = a.channels;
+    hp.n_cchunks = (a.channels + 2047) / 2048;
+    hp.x = nullptr;
+    hp.hist = nullptr;
+    LayerTable lt{};
+    for (int l = 0; l < d.n_layers; ++l) {
+        lt.x[l] = x_layers[l];
+        lt.hist[l] = hist_layers[l];
+    }
+    const long hb = (long)d.n_req * d.n_layers * hp.n_cchunks;
+    if (d.op_dtype == LUMO_BF16)
+        hipLaunchKernelGGL(path_hist_layers_kernel<1>, dim3((unsigned)hb), dim3(256), 0, s, pp, hp, lt);
+    else
+        hipLaunchKernelGGL(path_hist_layers_kernel<0>, dim3((unsigned)hb), dim3(256), 0, s, pp, hp, lt);
+    return hipGetLastError();
 }
 
 }  // namespace lumo

@@ -136,6 +136,43 @@ def test_commit_rejects_bad_arguments():
     assert _commit(_dims(d_k=24), desc) == L.LUMO_EUNSUPPORTED
 
 
+def _commit_layers(d, desc, max_path=4, accepted=FAKE, channels=16, x=None, hist=None, n=None):
+    P = ctypes.c_void_p
+    n = d.n_layers if n is None else n
+    xt = (P * max(n, 1))(*([P(FAKE)] * n if x is None else x))
+    ht = (P * max(n, 1))(*([P(FAKE)] * n if hist is None else hist))
+    return L._lib.lumo_gdn_commit_hist_layers(ctypes.byref(d), ctypes.byref(desc), max_path, P(accepted),
+                                              P(FAKE), P(FAKE), channels, xt, ht, None)
+
+
+def test_commit_hist_layers_rejects_bad_arguments():
+    desc, _blob = _desc()
+    P = ctypes.c_void_p
+    assert _commit_layers(_dims(), desc, max_path=0) == L.LUMO_EINVAL
+    assert _commit_layers(_dims(), desc, channels=12) == L.LUMO_ESHAPE
+    assert _commit_layers(_dims(), desc, channels=0) == L.LUMO_ESHAPE
+    assert _commit_layers(_dims(n_layers=129), desc) == L.LUMO_EUNSUPPORTED
+    assert "128" in L.lumo_last_error()
+    assert _commit_layers(_dims(), desc, accepted=0) == L.LUMO_EINVAL
+    assert _commit_layers(_dims(n_layers=2), desc, hist=[P(FAKE), None]) == L.LUMO_EINVAL
+    assert "conv_hist_layers[1]" in L.lumo_last_error()
+    assert _commit_layers(_dims(n_layers=2), desc, hist=[P(FAKE), P(FAKE + 8)]) == L.LUMO_EINVAL
+    assert _commit_layers(_dims(n_layers=3), desc, x=[P(FAKE), P(FAKE), None]) == L.LUMO_EINVAL
+    assert "x_layers[2]" in L.lumo_last_error()
+    d = _dims()
+    assert L._lib.lumo_gdn_commit_hist_layers(ctypes.byref(d), ctypes.byref(desc), 4, P(FAKE), P(FAKE),
+                                              P(FAKE), 16, None, (P * 1)(P(FAKE)), None) == L.LUMO_EINVAL
+    assert L._lib.lumo_gdn_commit_hist_layers(ctypes.byref(d), ctypes.byref(desc), 4, P(FAKE), P(FAKE),
+                                              P(FAKE), 16, (P * 1)(P(FAKE)), None, None) == L.LUMO_EINVAL
+
+
+def test_commit_hist_layers_empty_batch_is_a_no_op():
+    plan, blob = L.lumo_tree_plan(np.array([0], np.int32), np.zeros(0, np.int32),
+                                  np.zeros(0, np.int32), 0)
+    desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
+    assert _commit_layers(_dims(n_req=0, n_layers=2), desc, accepted=0, x=[None, None]) == L.LUMO_OK
+
+
 def test_conv_rejects_bad_arguments():
     desc, _blob = _desc()
     P = ctypes.c_void_p

@@ -736,6 +736,55 @@ def _dev(a, bf):
     return (t.view(torch.bfloat16) if bf else t).cuda()
 
 
+@pytest.mark.parametrize("bf,max_path", [(True, 24), (False, 24), (True, 4)])
+def test_commit_hist_layers(bf, max_path):
+    """lumo_gdn_commit_hist_layers takes each layer's x and history as buffers of their
+    own (pointer tables); path_out, path_len and every layer's history must equal the
+    stacked commit's bit for bit, and the oracle's publication exactly. Paths of more
+    than three nodes, of two, none (-1), an invalid accepted node (99), and with
+    max_path = 4 a path too long for it (length -1, nothing published); 3 layers of
+    2056 channels (a partial channel block)."""
+    rng = np.random.default_rng(53)
+    opd = ops.BF16 if bf else ops.F32
+    n_layers, C = 3, 2056
+    par = [trees.random_tree(rng, 30, 8, trees.bmax_uniform(3)), trees.chain(5), trees.FIG1_PARENT,
+           trees.random_tree(rng, 12, 6, trees.bmax_uniform(3))]
+    deep = int(np.argmax(trees.depths(par[0])))
+    acc_np = np.array([deep, 1, -1, 99], np.int32)
+    wl = _conv_wl(par, [31, 5, 7, 14], n_layers, C, opd, 57, max_path=max_path)
+    say(f"[gpu] commit into per-layer histories bf16={bf} max_path={max_path}")
+    d = L.dims(4, n_layers, 1, 1, 128, 128, L.LUMO_BF16 if bf else L.LUMO_F32)
+    desc = L.TreeDesc.build(wl.node_off, wl.parent_flat, wl.n_rows)
+    acc = torch.from_numpy(acc_np).cuda()
+    x = _dev(wl.arrays["x"], bf)
+    hist_ref = _dev(wl.arrays["hist"], bf)
+    po = torch.full((4, max_path), -7, dtype=torch.int32, device="cuda")
+    pl = torch.full((4,), -7, dtype=torch.int32, device="cuda")
+    L.lumo_gdn_commit(d, desc, max_path, acc, po, pl, None, None, None, None, None, C, x, hist_ref)
+    xs = [x[l].clone() for l in range(n_layers)]  # separate allocations
+    hs = [_dev(wl.arrays["hist"][:, l], bf) for l in range(n_layers)]
+    po2 = torch.full((4, max_path), -7, dtype=torch.int32, device="cuda")
+    pl2 = torch.full((4,), -7, dtype=torch.int32, device="cuda")
+    L.lumo_gdn_commit_hist_layers(d, desc, max_path, acc, po2, pl2, C, xs, hs)
+    torch.cuda.synchronize()
+    assert torch.equal(po2, po) and torch.equal(pl2, pl)
+    want0 = int(trees.depths(par[0])[deep]) + 1
+    assert pl2.cpu().numpy().tolist() == [want0 if want0 <= max_path else -1, 2, 0, -1]
+    iv = torch.int16 if bf else torch.int32
+    for l in range(n_layers):
+        assert torch.equal(hs[l].view(iv), hist_ref[:, l].view(iv)), l
+    opo = np.full((4, max_path), -1, np.int32)
+    opl = np.zeros(4, np.int32)
+    for r in range(3):
+        path, ln = oracle.plan.accepted_path(par[r], int(acc_np[r]), max_path)
+        if ln > 0:
+            opo[r], opl[r] = path, ln
+    href = oracle.conv_hist_publish(wl, opo, opl)
+    assert not np.array_equal(href, wl.arrays["hist"].astype(np.float64))  # something was published
+    for l in range(n_layers):
+        assert np.array_equal(gu.to_np(hs[l]).astype(np.float64), href[:, l]), l
+
+
 @pytest.mark.parametrize("case", ["depth_first", "runs", "f32"])
 def test_conv_pending_history(case):
     """lumo_tree_conv_gather_pending publishes the previous iteration's accepted paths
