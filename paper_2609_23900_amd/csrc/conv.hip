@@ -21,6 +21,7 @@ struct ConvParams {
     int32_t o_req, o_row, o_conv_src, o_node_off, o_dfs;
     int32_t n_req, total_nodes, total_rows, n_layers, channels, n_cchunks, act;
     int32_t run;  // nodes per block (1..kNodesPerBlock)
+    int32_t pre;  // 1: runs follow each request's preorder; 0: the stored node order
     const void* x;
     const void* hist;
     const float* w;
@@ -175,18 +176,23 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p) {
     const int n0 = grp * p.run;
     const int nn = min(p.total_nodes, n0 + p.run) - n0;
     // node info of the run, one node per lane (lanes 0..31 of every wave), broadcast
-    // per node with readlane so the window loads depend on nothing but registers. Runs
-    // cover each request's nodes in depth-first preorder (positions node_off[r] ..), so
-    // a node's parent and grandparents were loaded shortly before, by this run or a
-    // neighbouring one on the same XCD.
+    // per node with readlane so the window loads depend on nothing but registers. Full
+    // runs cover each request's nodes in depth-first preorder (positions node_off[r] ..),
+    // so a node's parent and grandparents were loaded shortly before, by this run or a
+    // neighbouring one on the same XCD. Shortened runs (small grids, bound by the
+    // latency of their dependent loads) take the nodes in their stored order, which
+    // spares the lookup of a preorder position's node.
     // (lane k also loads node_off[min(k, n_req)], so that a node's request offset is a
     // lane exchange rather than a dependent load)
     const int li = (int)threadIdx.x & (kNodesPerBlock - 1);
     const int pos = n0 + (li < nn ? li : 0);
-    const int nof = p.blob[p.o_node_off + min((int)threadIdx.x & 63, p.n_req)];
     const int i_req = p.blob[p.o_req + pos];
-    const int nsh = __shfl(nof, i_req & 63);
-    const int mine = (i_req < 64 ? nsh : p.blob[p.o_node_off + i_req]) + p.blob[p.o_dfs + pos];
+    int mine = pos;
+    if (p.pre) {
+        const int nof = p.blob[p.o_node_off + min((int)threadIdx.x & 63, p.n_req)];
+        const int nsh = __shfl(nof, i_req & 63);
+        mine = (i_req < 64 ? nsh : p.blob[p.o_node_off + i_req]) + p.blob[p.o_dfs + pos];
+    }
     const int i_row = p.blob[p.o_row + mine];
     int i_src[4];
 #pragma unroll
@@ -475,6 +481,7 @@ hipError_t launch_conv(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const
     int run = kNodesPerBlock;
     while (run > 4 && (long)d.n_layers * n_cchunks * ((pl.total_nodes + run - 1) / run) < 4 * 256) run /= 2;
     p.run = run;
+    p.pre = run == kNodesPerBlock;
     const long blocks = (long)d.n_layers * n_cchunks * ((pl.total_nodes + run - 1) / run);
     if (d.op_dtype == LUMO_BF16)
         hipLaunchKernelGGL(conv_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, s, p);

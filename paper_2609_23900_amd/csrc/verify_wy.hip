@@ -1009,12 +1009,24 @@ __global__ __launch_bounds__(64 * (CW == 64 ? 2 : 4) * NVH, (D == 8 || CW == 32 
             for (int g = 0; g < D / 4; ++g) hd.c[g] = *reinterpret_cast<const float4*>(cf + 8 + (hiB ? D : 0) + 4 * g);
             hd.vraw = vs[n * CW + pc];
         };
+        // Each node starts by taking the record requested one node earlier into registers
+        // and only then stores the previous node's output and requests the next record, so
+        // its wait covers nothing issued since (the compiler's LDS waits here are full
+        // drains, which would otherwise also wait for the record just requested).
         auto recursion_ab = [&](int hf, const f32x4 (&px)[4]) {
             RecHeadAB nx;
             load_head_ab(16 * hf, nx);
+            uint16_t ovp = 0;  // the previous node's output, stored one node later
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const int n = 16 * hf + i;
+#pragma unroll
+                for (int g = 0; g < D / 4; ++g)
+                    asm volatile("" ::"v"(nx.c[g].x), "v"(nx.c[g].y), "v"(nx.c[g].z), "v"(nx.c[g].w));
+                asm volatile("" ::"v"(nx.w0.y), "v"(nx.w0.z), "v"(nx.w0.w), "v"(nx.w1.x), "v"(nx.w1.y),
+                             "v"(nx.vraw), "v"(ovp)
+                             : "memory");
+                if (i > 0 && hiB) vs[(n - 1) * CW + pc] = ovp;
                 const RecHeadAB cu = nx;
                 if (i + 1 < 16) load_head_ab(n + 1, nx);
                 const int d = __builtin_amdgcn_readfirstlane(__float_as_int(cu.w0.y));  // uniform
@@ -1040,8 +1052,9 @@ __global__ __launch_bounds__(64 * (CW == 64 ? 2 : 4) * NVH, (D == 8 || CW == 32 
                 const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(da), __float_as_uint(da), false, false);
                 const float delta = __uint_as_float(sw[0]);  // the lower half's delta in both halves
                 dst[d < D ? d : D] = delta;
-                if (hiB) vs[n * CW + pc] = f32_to_bf16(__builtin_fmaf(cu.w1.x, delta, t));
+                ovp = f32_to_bf16(__builtin_fmaf(cu.w1.x, delta, t));  // over the consumed value entry
             }
+            if (hiB) vs[(16 * hf + 15) * CW + pc] = ovp;
         };
         exchange(pk);
         if constexpr (AB) {
