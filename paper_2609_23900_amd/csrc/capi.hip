@@ -7,6 +7,7 @@
 #include <string>
 
 #include "internal.h"
+#include "commit.h"
 #include "launch.h"
 #include "select.h"
 

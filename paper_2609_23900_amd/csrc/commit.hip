@@ -14,7 +14,7 @@
 // Empty or invalid paths leave the state and the history untouched.
 #include "device_common.h"
 #include "internal.h"
-#include "launch.h"
+#include "commit.h"
 
 namespace lumo {
 namespace {

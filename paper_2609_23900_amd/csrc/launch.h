@@ -97,12 +97,6 @@ struct CommitArgs {
 
 hipError_t launch_commit(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const CommitArgs& a, hipStream_t s);
 
-// Path derivation and conv-history publication with each layer's history and x in a
-// buffer of its own (pointer tables passed by value, at most kMaxLayerTable layers).
-constexpr int kMaxLayerTable = 128;
-hipError_t launch_commit_hist_layers(const lumo_gdn_dims& d, const lumo_tree_desc& desc, const CommitArgs& a,
-                                     const void* const* x_layers, void* const* hist_layers, hipStream_t s);
-
 struct ConvArgs {
     int32_t channels;
     const void* x;
