@@ -46,7 +46,7 @@ PEAK_VALU_F32_TFS = 157.3      # MI355X fp32 vector, published (256 CU x 2.4 GHz
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "traffic.json")
 # sources that determine the code of each policy's verify kernels
 VERIFY_SOURCES = {
-    "wy": ["verify_wy.hip", "device_common.h", "internal.h", "launch.h"],
+    "wy": ["verify_wy.hip", "verify_wy_body.inc", "verify_wy.h", "device_common.h", "internal.h", "launch.h"],
     "paths": ["verify_scan.hip", "device_common.h", "internal.h", "launch.h"],
     "wyv": ["verify_wyv.hip", "device_common.h", "internal.h", "launch.h"],
     "attention": ["attention.hip", "device_common.h", "internal.h", "launch.h"],
@@ -417,11 +417,15 @@ def per_layer_graph_ms(args, st, stream):
     and verify calls (n_layers = 1), each layer with its own state bank
     [req][1][h_v][d_k][d_v] and conv history [req][1][3][C], the per-node tensors sliced
     by layer. The commit is one launch for all layers: it derives the accepted path and
-    publishes it into every layer's conv history (lumo_gdn_commit_hist_layers), while
-    each layer's state is published by its next verification. With --fused one call per
-    layer does the conv, both publications and the verification, and the commit only
-    derives the path. Ten steps are captured in one graph and replayed. Returns ms per
-    step."""
+    publishes it into every layer's conv history (lumo_gdn_commit_hist_layers). The
+    states are published by the verification launches: layer 0's verification publishes
+    its own, and every layer's verification runs in one launch with the publication
+    into the next layer's state bank (lumo_tree_gdn_verify_pending_pair), so that the
+    publication runs beside the verification instead of before it. With --fused one
+    call per layer does the conv, both publications and the verification, and the
+    commit only derives the path. Ten steps are captured in one graph and replayed.
+    Returns ms per step."""
+    import numpy as np
     import torch
 
     import paper_2609_23900_amd as L
@@ -434,6 +438,21 @@ def per_layer_graph_ms(args, st, stream):
 
     bias = [None] * nl if st.bias is None else [st.bias[l] for l in range(nl)]
     xs = [st.x[l] for l in range(nl)]
+    # each layer's gate parameters (raw gates): the one-layer calls read row 0
+    preps = [None] * nl if st.prep is None else [
+        L.Prep(st.prep.c.flags, st.prep.c.qk_eps, None if st.prep.a_log is None else st.prep.a_log[l:l + 1],
+               None if st.prep.dt_bias is None else st.prep.dt_bias[l:l + 1]) for l in range(nl)]
+    empty = L.TreeDesc.build(np.zeros(d.n_req + 1, np.int32), np.zeros(0, np.int32), np.ones(d.n_req, np.int32),
+                             L.LUMO_POLICY_WY)
+    calls = []  # (layer l's verification, the publication into layer l + 1's bank)
+    for l in range(nl):
+        t = {key: st.t[key][l] for key in ("q", "k", "v", "g", "beta")}
+        calls.append((
+            L.pending_call(d1, st.desc, t["q"], t["k"], t["v"], t["g"], t["beta"], states[l], st.o[l],
+                           st.desc if l == 0 else empty, st.max_path, st.path_out, st.path_len, t["k"], t["v"],
+                           t["g"], t["beta"], preps[l]),
+            L.pending_call(d1, empty, None, None, None, None, None, states[l], None, st.desc, st.max_path,
+                           st.path_out, st.path_len, t["k"], t["v"], t["g"], t["beta"], preps[l])))
 
     def one_step():
         for l in range(nl):
@@ -442,12 +461,10 @@ def per_layer_graph_ms(args, st, stream):
             if args.fused:  # conv, publications and verification of the layer in one call
                 L.lumo_tree_gdn_verify_conv_pending(d1, st.desc, st.channels, x, hists[l], w, bias[l], st.act, g, b,
                                                     states[l], st.o[l], st.desc, st.max_path, st.path_out,
-                                                    st.path_len, x, g, b, None, st.prep)
+                                                    st.path_len, x, g, b, None, preps[l])
                 continue
             L.lumo_tree_conv_gather(d1, st.desc, st.channels, x, hists[l], w, bias[l], st.act, y)
-            q, k, v = (st.t[key][l] for key in ("q", "k", "v"))
-            L.lumo_tree_gdn_verify_pending(d1, st.desc, q, k, v, g, b, states[l], st.o[l], st.desc, st.max_path,
-                                           st.path_out, st.path_len, k, v, g, b, None, st.prep)
+            L.lumo_tree_gdn_verify_pending_pair(calls[l][0], calls[l + 1][1] if l + 1 < nl else None)
         if args.fused:
             st.commit(None, defer=True, with_conv=False)
         else:

@@ -11,7 +11,8 @@
  *                          native state, publish the convolution history
  * plus lumo_tree_attention (the attention layers' tree verification),
  * lumo_draft_select (the drafter's fused argmax / top-k selection), a
- * captured-graph form of the commit, a commit for per-layer history buffers; lumo_tree_gdn_verify_pending and
+ * captured-graph form of the commit, a commit for per-layer history buffers, two
+ * deferred verifications in one launch; lumo_tree_gdn_verify_pending and
  * lumo_tree_conv_gather_pending, which fold the publication of one iteration (state
  * replay, conv history) into the verification and convolution of the next, and
  * lumo_tree_gdn_verify_conv_pending, which does both in one pass with the conv outputs
@@ -325,6 +326,47 @@ lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, const lumo_t
                                          const int32_t* path_out, const int32_t* path_len,
                                          const void* pend_k, const void* pend_v,
                                          const float* pend_g, const float* pend_beta, void* stream);
+
+/*
+ * lumo_tree_gdn_verify_pending_pair - two lumo_tree_gdn_verify_pending calls in one
+ * launch (Sec. IV-B: each layer runs its own update; Alg. 1: a layer's state is
+ * published before that layer's next verification reads it). Each call is described by
+ * a lumo_gdn_pending_call holding exactly the arguments of lumo_tree_gdn_verify_pending
+ * and gives the same results, bit for bit. The point is a model calling the step layer
+ * by layer: call a verifies layer l (its path published earlier: pend_desc of a batch
+ * without nodes, so that nothing is pending) while call b publishes the pending path
+ * into layer l + 1's state bank (desc of a batch without nodes: nothing to verify);
+ * the two run side by side on the device, so the publication costs the layer call
+ * little time.
+ *   a    required; b nullable (then this is call a alone)
+ * Both calls run the 32-column form (four waves of 32 state columns per value head,
+ * the same bits as any other launch of the call). Host errors as for
+ * lumo_tree_gdn_verify_pending, per call; LUMO_EUNSUPPORTED when the two calls differ
+ * in query/key normalisation (LUMO_PREP_QK_NORM). The calls must not write the same
+ * memory (outputs, state banks); a call's pending path may be shared.
+ */
+typedef struct {
+    const lumo_gdn_dims* dims;
+    const lumo_tree_desc* desc;
+    const lumo_gdn_prep* prep;
+    const void* q;
+    const void* k;
+    const void* v;
+    const float* g;
+    const float* beta;
+    float* state;
+    void* o;
+    const lumo_tree_desc* pend_desc;
+    int32_t max_path;
+    const int32_t* path_out;
+    const int32_t* path_len;
+    const void* pend_k;
+    const void* pend_v;
+    const float* pend_g;
+    const float* pend_beta;
+} lumo_gdn_pending_call;
+lumo_status lumo_tree_gdn_verify_pending_pair(const lumo_gdn_pending_call* a, const lumo_gdn_pending_call* b,
+                                              void* stream);
 
 /*
  * lumo_tree_gdn_verify_conv_pending - lumo_tree_conv_gather_pending and

@@ -77,6 +77,16 @@ class lumo_gdn_prep(ctypes.Structure):
                 ("dt_bias", ctypes.c_void_p)]
 
 
+class lumo_gdn_pending_call(ctypes.Structure):
+    _fields_ = [("dims", ctypes.POINTER(lumo_gdn_dims)), ("desc", ctypes.POINTER(lumo_tree_desc)),
+                ("prep", ctypes.POINTER(lumo_gdn_prep)), ("q", ctypes.c_void_p), ("k", ctypes.c_void_p),
+                ("v", ctypes.c_void_p), ("g", ctypes.c_void_p), ("beta", ctypes.c_void_p),
+                ("state", ctypes.c_void_p), ("o", ctypes.c_void_p), ("pend_desc", ctypes.POINTER(lumo_tree_desc)),
+                ("max_path", ctypes.c_int32), ("path_out", ctypes.c_void_p), ("path_len", ctypes.c_void_p),
+                ("pend_k", ctypes.c_void_p), ("pend_v", ctypes.c_void_p), ("pend_g", ctypes.c_void_p),
+                ("pend_beta", ctypes.c_void_p)]
+
+
 class Prep:
     """Operand preparation (lumo_gdn_prep): flags, qk_eps and, for raw gates, the device
     tensors a_log and dt_bias [n_layers][h_v] fp32 (kept alive here)."""
@@ -120,6 +130,8 @@ def _load():
     L.lumo_tree_gdn_verify_prep.argtypes = [PD, PT, PP, P, P, P, P, P, P, P, P]
     L.lumo_tree_gdn_verify_pending.argtypes = [PD, PT, PP, P, P, P, P, P, P, P, PT, I32, P, P, P, P, P, P,
                                                P]
+    L.lumo_tree_gdn_verify_pending_pair.argtypes = [ctypes.POINTER(lumo_gdn_pending_call),
+                                                    ctypes.POINTER(lumo_gdn_pending_call), P]
     L.lumo_tree_gdn_verify_conv_pending.argtypes = [PD, PT, PP, I32, P, P, P, P, I32, P, P, P, P, PT, I32, P, P,
                                                     P, P, P, P]
     L.lumo_gdn_commit_prep.argtypes = [PD, PT, PP, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
@@ -134,7 +146,7 @@ def _load():
     L.lumo_version.restype = ctypes.c_char_p
     for f in ("lumo_tree_plan", "lumo_tree_conv_gather", "lumo_tree_conv_gather_pending", "lumo_tree_gdn_verify",
               "lumo_tree_gdn_verify_prep", "lumo_tree_gdn_verify_pending", "lumo_tree_gdn_verify_conv_pending", "lumo_gdn_commit",
-              "lumo_gdn_commit_prep", "lumo_gdn_commit_hist_layers", "lumo_tree_attention", "lumo_tree_attention_noalloc", "lumo_draft_select", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
+              "lumo_gdn_commit_prep", "lumo_gdn_commit_hist_layers", "lumo_tree_gdn_verify_pending_pair", "lumo_tree_attention", "lumo_tree_attention_noalloc", "lumo_draft_select", "lumo_gdn_commit_graph_create", "lumo_gdn_commit_graph_launch"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -253,6 +265,25 @@ def lumo_tree_gdn_verify_prep(d, desc: TreeDesc, prep: Prep | None, q, k, v, g, 
     _check(_lib.lumo_tree_gdn_verify_prep(ctypes.byref(d), ctypes.byref(desc.desc), _prep_ptr(prep),
                                           _dptr(q), _dptr(k), _dptr(v), _dptr(g), _dptr(beta),
                                           _dptr(state0), _dptr(o), _stream(stream)))
+
+
+def pending_call(d, desc: TreeDesc, q, k, v, g, beta, state, o, pend_desc: TreeDesc, max_path, path_out,
+                 path_len, pend_k, pend_v, pend_g, pend_beta, prep: Prep | None = None):
+    """The arguments of lumo_tree_gdn_verify_pending as one lumo_gdn_pending_call (the
+    struct keeps the objects it points to alive)."""
+    c = lumo_gdn_pending_call(ctypes.pointer(d), ctypes.pointer(desc.desc),
+                              None if prep is None else ctypes.pointer(prep.c), _dptr(q), _dptr(k), _dptr(v),
+                              _dptr(g), _dptr(beta), _dptr(state), _dptr(o), ctypes.pointer(pend_desc.desc),
+                              int(max_path), _dptr(path_out), _dptr(path_len), _dptr(pend_k), _dptr(pend_v),
+                              _dptr(pend_g), _dptr(pend_beta))
+    c._refs = (d, desc, pend_desc, prep)
+    return c
+
+
+def lumo_tree_gdn_verify_pending_pair(a, b=None, stream=None):
+    """a, b: pending_call(...) structs; b may be None."""
+    _check(_lib.lumo_tree_gdn_verify_pending_pair(ctypes.byref(a), None if b is None else ctypes.byref(b),
+                                                  _stream(stream)))
 
 
 def lumo_tree_gdn_verify_pending(d, desc: TreeDesc, q, k, v, g, beta, state, o, pend_desc: TreeDesc,

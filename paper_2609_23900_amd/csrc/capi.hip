@@ -9,6 +9,7 @@
 #include "internal.h"
 #include "commit.h"
 #include "launch.h"
+#include "verify_wy.h"
 #include "select.h"
 
 #include <algorithm>
@@ -269,16 +270,15 @@ extern "C" lumo_status lumo_tree_gdn_verify_prep(const lumo_gdn_dims* dims, cons
     return LUMO_OK;
 }
 
-extern "C" lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
-                                                    const lumo_gdn_prep* prep,
-                                                    const void* q, const void* k, const void* v, const float* g,
-                                                    const float* beta, float* state, void* o,
-                                                    const lumo_tree_desc* pend_desc, int32_t max_path,
-                                                    const int32_t* path_out, const int32_t* path_len,
-                                                    const void* pend_k, const void* pend_v, const float* pend_g,
-                                                    const float* pend_beta, void* stream) {
-    static const char* fn = "lumo_tree_gdn_verify_pending";
-    clear_error();
+namespace {
+
+// Host validation of a deferred verification (lumo_tree_gdn_verify_pending); fills the
+// launch arguments. LUMO_OK with *empty set when there is nothing to launch.
+lumo_status check_pending(const lumo_gdn_dims* dims, const lumo_tree_desc* desc, const lumo_gdn_prep* prep,
+                          const void* q, const void* k, const void* v, const float* g, const float* beta, float* state,
+                          void* o, const lumo_tree_desc* pend_desc, int32_t max_path, const int32_t* path_out,
+                          const int32_t* path_len, const void* pend_k, const void* pend_v, const float* pend_g,
+                          const float* pend_beta, const char* fn, GdnArgs& a, PendArgs& pa, bool& empty) {
     LUMO_TRY(check_dims(dims, fn));
     LUMO_TRY(check_desc(dims, desc, fn));
     if (!pend_desc) return fail(LUMO_EINVAL, "%s: pend_desc is NULL", fn);
@@ -287,7 +287,8 @@ extern "C" lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, c
     PrepArgs pr;
     LUMO_TRY(check_prep(prep, fn, pr));
     if (max_path < 1 || max_path > 4096) return fail(LUMO_EINVAL, "%s: max_path %d (1..4096)", fn, max_path);
-    if (dims->n_req == 0) return LUMO_OK;
+    empty = dims->n_req == 0;
+    if (empty) return LUMO_OK;
     LUMO_TRY(check_ptr(state, fn, "state"));
     LUMO_TRY(check_ptr(path_out, fn, "path_out"));
     LUMO_TRY(check_ptr(path_len, fn, "path_len"));
@@ -305,10 +306,64 @@ extern "C" lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, c
         LUMO_TRY(check_ptr(beta, fn, "beta"));
         LUMO_TRY(check_ptr(o, fn, "o"));
     }
-    GdnArgs a{q, k, v, g, beta, state, o, nullptr, nullptr, pr};
-    PendArgs pa{pend_desc, max_path, path_out, path_len, pend_k, pend_v, pend_g, pend_beta, state};
+    a = GdnArgs{q, k, v, g, beta, state, o, nullptr, nullptr, pr};
+    pa = PendArgs{pend_desc, max_path, path_out, path_len, pend_k, pend_v, pend_g, pend_beta, state};
+    return LUMO_OK;
+}
+
+}  // namespace
+
+extern "C" lumo_status lumo_tree_gdn_verify_pending(const lumo_gdn_dims* dims, const lumo_tree_desc* desc,
+                                                    const lumo_gdn_prep* prep,
+                                                    const void* q, const void* k, const void* v, const float* g,
+                                                    const float* beta, float* state, void* o,
+                                                    const lumo_tree_desc* pend_desc, int32_t max_path,
+                                                    const int32_t* path_out, const int32_t* path_len,
+                                                    const void* pend_k, const void* pend_v, const float* pend_g,
+                                                    const float* pend_beta, void* stream) {
+    static const char* fn = "lumo_tree_gdn_verify_pending";
+    clear_error();
+    GdnArgs a;
+    PendArgs pa;
+    bool empty = false;
+    LUMO_TRY(check_pending(dims, desc, prep, q, k, v, g, beta, state, o, pend_desc, max_path, path_out, path_len,
+                           pend_k, pend_v, pend_g, pend_beta, fn, a, pa, empty));
+    if (empty) return LUMO_OK;
     hipError_t e = launch_wy(*dims, *desc, a, static_cast<hipStream_t>(stream), &pa);
     if (e == hipErrorNotSupported) return fail(LUMO_EUNSUPPORTED, "%s: not compiled into the library", fn);
+    if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return LUMO_OK;
+}
+
+extern "C" lumo_status lumo_tree_gdn_verify_pending_pair(const lumo_gdn_pending_call* ca,
+                                                         const lumo_gdn_pending_call* cb, void* stream) {
+    static const char* fn = "lumo_tree_gdn_verify_pending_pair";
+    clear_error();
+    if (!ca) return fail(LUMO_EINVAL, "%s: call a is NULL", fn);
+    const lumo_gdn_pending_call* c[2] = {ca, cb};
+    GdnArgs a[2];
+    PendArgs pa[2];
+    bool empty[2] = {true, true};
+    for (int i = 0; i < 2; ++i) {
+        if (!c[i]) continue;
+        LUMO_TRY(check_pending(c[i]->dims, c[i]->desc, c[i]->prep, c[i]->q, c[i]->k, c[i]->v, c[i]->g, c[i]->beta,
+                               c[i]->state, c[i]->o, c[i]->pend_desc, c[i]->max_path, c[i]->path_out,
+                               c[i]->path_len, c[i]->pend_k, c[i]->pend_v, c[i]->pend_g, c[i]->pend_beta, fn, a[i],
+                               pa[i], empty[i]));
+    }
+    if (empty[0] && empty[1]) return LUMO_OK;
+    if (!empty[0] && !empty[1] &&
+        ((a[0].prep.flags & LUMO_PREP_QK_NORM) != 0) != ((a[1].prep.flags & LUMO_PREP_QK_NORM) != 0))
+        return fail(LUMO_EUNSUPPORTED, "%s: both calls must take the same query/key normalisation", fn);
+    // a call without requests contributes no blocks: it takes the other call's arguments
+    const int i0 = empty[0] ? 1 : 0, i1 = empty[1] ? 0 : 1;
+    lumo_gdn_dims d0 = *c[i0]->dims, d1 = *c[i1]->dims;
+    if (empty[0]) d0.n_req = 0;
+    if (empty[1]) d1.n_req = 0;
+    hipError_t e = launch_wy_pair(d0, *c[i0]->desc, a[i0], pa[i0], d1, *c[i1]->desc, a[i1], pa[i1],
+                                  static_cast<hipStream_t>(stream));
+    if (e == hipErrorNotSupported)
+        return fail(LUMO_EUNSUPPORTED, "%s: trees deeper than the WY form's limit", fn);
     if (e != hipSuccess) return fail(LUMO_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return LUMO_OK;
 }

@@ -303,6 +303,61 @@ def test_verify_pending_empty_batch_is_a_no_op():
     assert _pending(d, desc, desc) == L.LUMO_OK
 
 
+def _pcall(d, desc, pdesc, state=FAKE, prep=None, max_path=4):
+    P = ctypes.c_void_p
+    return L.lumo_gdn_pending_call(ctypes.pointer(d), ctypes.pointer(desc),
+                                   None if prep is None else ctypes.pointer(prep), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+                                   P(FAKE), P(state) if state else None, P(FAKE), ctypes.pointer(pdesc), max_path,
+                                   P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE))
+
+
+def _pair(a, b):
+    return L._lib.lumo_tree_gdn_verify_pending_pair(None if a is None else ctypes.byref(a),
+                                                    None if b is None else ctypes.byref(b), None)
+
+
+def test_pending_call_layout_matches_header():
+    src = os.path.join(ROOT, "_build_abi_layout.c")
+    exe = os.path.join(ROOT, "_build_abi_layout")
+    fields = [f for f, _ in L.lumo_gdn_pending_call._fields_]
+    body = "".join(f'printf("%zu ", offsetof(lumo_gdn_pending_call, {f}));' for f in fields)
+    with open(src, "w") as fh:
+        fh.write("#include <stddef.h>\n#include <stdio.h>\n#include \"lumo_tree.h\"\n"
+                 f"int main(void) {{ {body} printf(\"%zu\\n\", sizeof(lumo_gdn_pending_call)); return 0; }}\n")
+    try:
+        subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), src, "-o", exe], check=True)
+        got = [int(x) for x in subprocess.run([exe], capture_output=True, text=True, check=True).stdout.split()]
+    finally:
+        for f in (src, exe):
+            if os.path.exists(f):
+                os.remove(f)
+    want = [getattr(L.lumo_gdn_pending_call, f).offset for f in fields] + [ctypes.sizeof(L.lumo_gdn_pending_call)]
+    assert got == want
+
+
+def test_verify_pending_pair_rejects_bad_arguments():
+    dw = _dims(h_k=2, h_v=4, d_k=128, d_v=128, op_dtype=1)
+    wy, _b1 = _desc(policy=L.LUMO_POLICY_WY)
+    paths, _b2 = _desc(policy=L.LUMO_POLICY_PATHS)
+    assert _pair(None, None) == L.LUMO_EINVAL
+    assert _pair(_pcall(dw, paths, paths), None) == L.LUMO_EUNSUPPORTED  # needs a WY plan
+    assert _pair(_pcall(dw, wy, paths), _pcall(dw, wy, paths, state=0)) == L.LUMO_EINVAL
+    assert "state" in L.lumo_last_error()
+    assert _pair(_pcall(dw, wy, paths), _pcall(dw, wy, paths, max_path=0)) == L.LUMO_EINVAL
+    norm = L.lumo_gdn_prep(L.LUMO_PREP_QK_NORM, 1e-6, None, None)
+    assert _pair(_pcall(dw, wy, paths), _pcall(dw, wy, paths, prep=norm)) == L.LUMO_EUNSUPPORTED
+    assert "normalisation" in L.lumo_last_error()
+
+
+def test_verify_pending_pair_empty_calls_are_a_no_op():
+    plan, blob = L.lumo_tree_plan(np.array([0], np.int32), np.zeros(0, np.int32),
+                                  np.zeros(0, np.int32), L.LUMO_POLICY_WY)
+    desc = L.lumo_tree_desc(ctypes.c_void_p(FAKE), blob.ctypes.data_as(ctypes.c_void_p), plan)
+    d = _dims(n_req=0, h_k=1, h_v=1, d_k=128, d_v=128, op_dtype=1)
+    assert _pair(_pcall(d, desc, desc), None) == L.LUMO_OK
+    assert _pair(_pcall(d, desc, desc), _pcall(d, desc, desc)) == L.LUMO_OK
+
+
 def _verify_prep(d, desc, prep):
     P = ctypes.c_void_p
     return L._lib.lumo_tree_gdn_verify_prep(ctypes.byref(d), ctypes.byref(desc),

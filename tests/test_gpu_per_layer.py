@@ -164,3 +164,102 @@ def test_per_layer_flow_batched():
     a, b = _stacked([wl, wl]), _layers([wl, wl])
     assert int((a["path_len"][0] > 0).sum()) > 0
     _assert_same(a, b, "batched")
+
+
+def _empty_desc(n_req):
+    """A batch of n_req requests without nodes (WY plan): nothing to verify, or nothing
+    pending."""
+    return L.TreeDesc.build(np.zeros(n_req + 1, np.int32), np.zeros(0, np.int32), np.ones(n_req, np.int32),
+                            L.LUMO_POLICY_WY)
+
+
+def _pair_layers(wls):
+    """_layers with the layer calls paired: layer l's verification (nothing pending for
+    l >= 1) and, in the same launch, the publication of the pending path into layer
+    l + 1's state bank (lumo_tree_gdn_verify_pending_pair)."""
+    sp, sc = (_step(w) for w in wls)
+    d = sp.dims
+    nl = d.n_layers
+    d1 = L.dims(d.n_req, 1, d.h_k, d.h_v, d.d_k, d.d_v, d.op_dtype)
+    empty = _empty_desc(d.n_req)
+    states = [sp.state[:, l:l + 1].contiguous() for l in range(nl)]
+    hists = [sp.hist[:, l:l + 1].contiguous() for l in range(nl)]
+    for l in range(nl):
+        L.lumo_tree_conv_gather(d1, sp.desc, sp.channels, sp.x[l], hists[l], sp.w[l], None, sp.act, sp.y[l])
+    sp.t["q"], sp.t["k"], sp.t["v"] = _split(sp.y, d.h_k, d.h_v, d.d_k)
+    L.lumo_gdn_commit_hist_layers(d, sp.desc, sp.max_path, sp.accepted, sp.path_out, sp.path_len, sp.channels,
+                                  [sp.x[l] for l in range(nl)], hists)
+
+    def publish(l):  # the pending path into layer l's bank, nothing to verify
+        return L.pending_call(d1, empty, None, None, None, None, None, states[l], None, sp.desc, sp.max_path,
+                              sp.path_out, sp.path_len, sp.t["k"][l], sp.t["v"][l], sp.t["g"][l], sp.t["beta"][l])
+
+    for l in range(nl):
+        L.lumo_tree_conv_gather(d1, sc.desc, sc.channels, sc.x[l], hists[l], sc.w[l], None, sc.act, sc.y[l])
+        q, k, v = _split(sc.y[l], d.h_k, d.h_v, d.d_k)
+        pend = sp.desc if l == 0 else empty  # layer 0 publishes its own path
+        a = L.pending_call(d1, sc.desc, q, k, v, sc.t["g"][l], sc.t["beta"][l], states[l], sc.o[l], pend,
+                           sp.max_path, sp.path_out, sp.path_len, sp.t["k"][l], sp.t["v"][l], sp.t["g"][l],
+                           sp.t["beta"][l])
+        L.lumo_tree_gdn_verify_pending_pair(a, publish(l + 1) if l + 1 < nl else None)
+    L.lumo_gdn_commit_hist_layers(d, sc.desc, sc.max_path, sc.accepted, sc.path_out, sc.path_len, sc.channels,
+                                  [sc.x[l] for l in range(nl)], hists)
+    torch.cuda.synchronize()
+    return dict(y=[sp.y, sc.y], o=sc.o, state=torch.cat(states, dim=1), hist=torch.cat(hists, dim=1),
+                path_len=[sp.path_len, sc.path_len])
+
+
+@pytest.mark.parametrize("case", ["edge", "batched"])
+def test_paired_layer_calls_flow(case):
+    """The per-layer flow with each layer's verification paired with the publication
+    of the next layer's state in one launch: bit for bit the stacked flow."""
+    wls = _edge_workloads() if case == "edge" else [configs.build("batched", n_layers=4)] * 2
+    say(f"[gpu] paired layer calls, {case}")
+    a, b = _stacked(wls), _pair_layers(wls)
+    _assert_same(a, b, case)
+
+
+def test_verify_pending_pair_equals_two_calls():
+    """lumo_tree_gdn_verify_pending_pair against the same two calls made one after the
+    other: a verification that publishes its pending path with the publication of that
+    path into another bank; a verification with nothing pending with a publication; a
+    call alone. Outputs and every state bank bit for bit; 16-level trees (the depth-16
+    instance) and the batched trees (depth 8)."""
+    for name, over in (("batched", dict(n_layers=2)), ("widedeep", dict(n_req=4, n_layers=2))):
+        wl = configs.build(name, with_conv=False, **over)
+        st = GdnTreeStep.from_workload(wl, policy=L.LUMO_POLICY_WY, with_conv=False)
+        d = st.dims
+        d1 = L.dims(d.n_req, 1, d.h_k, d.h_v, d.d_k, d.d_v, d.op_dtype)
+        empty = _empty_desc(d.n_req)
+        st.commit(defer=True)
+        torch.cuda.synchronize()
+        assert int((st.path_len > 0).sum()) > 0
+        say(f"[gpu] verify_pending_pair {name}")
+        t = {key: [st.t[key][l] for l in range(2)] for key in ("q", "k", "v", "g", "beta")}
+
+        def call(l, state, o, tree, pend, use):
+            args = (t["q"][l], t["k"][l], t["v"][l], t["g"][l], t["beta"][l]) if tree is st.desc else (None,) * 5
+            return dict(args=(d1, tree) + args + (state, o if tree is st.desc else None, pend, st.max_path,
+                                                   st.path_out, st.path_len, t["k"][l], t["v"][l], t["g"][l],
+                                                   t["beta"][l]), use=use)
+
+        for pend_a, with_b in ((st.desc, True), (empty, True), (st.desc, False)):
+            res = []
+            for paired in (False, True):
+                banks = [st.state0[:, l:l + 1].contiguous() for l in range(2)]
+                o = torch.zeros_like(st.o[0])
+                ca = call(0, banks[0], o, st.desc, pend_a, True)
+                cb = call(1, banks[1], None, empty, st.desc, with_b)
+                if paired:
+                    L.lumo_tree_gdn_verify_pending_pair(L.pending_call(*ca["args"]),
+                                                        L.pending_call(*cb["args"]) if with_b else None)
+                else:
+                    L.lumo_tree_gdn_verify_pending(*ca["args"])
+                    if with_b:
+                        L.lumo_tree_gdn_verify_pending(*cb["args"])
+                torch.cuda.synchronize()
+                res.append((o.clone(), banks[0].clone(), banks[1].clone()))
+            (o1, s1, u1), (o2, s2, u2) = res
+            assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)), (name, with_b)
+            assert torch.equal(s1, s2) and torch.equal(u1, u2), (name, with_b)
+            assert with_b == (not torch.equal(u2, st.state0[:, 1:2])), (name, with_b)  # published, or untouched
