@@ -589,12 +589,20 @@ def main():
     st = GdnTreeStep.from_workload(wl, policy=policy, keep_state0=False, prep=prep)
     stream = torch.cuda.current_stream()
 
+    # The deferred conv publishes the previous step's history in its own launch only
+    # when it takes the depth-first kernel (bf16, trees of at most 16 levels, at least
+    # four blocks per CU); otherwise it needs a launch of its own for it, and the commit
+    # publishes the history instead, in the launch that derives the path.
+    dfs_conv = (not args.f32 and st.plan.max_depth <= 16
+                and wl.n_req * wl.n_layers * ((wl.channels + 2047) // 2048) >= 4 * 256)
+    hist_in_commit = deferred and not args.fused and not dfs_conv
+
     def step(ev=None, s=stream):  # s=None: the current stream (a graph's capture stream)
         if ev is not None:
             ev[0].record(stream)
         if args.fused:
             pass  # the conv runs inside the verification
-        elif deferred:
+        elif deferred and not hist_in_commit:
             st.conv_pending(st, s)  # publishes the previous step's history, then the conv
         else:
             st.conv(s)
@@ -608,7 +616,7 @@ def main():
             st.verify(s)
         if ev is not None:
             ev[2].record(stream)
-        st.commit(s, defer=deferred, with_conv=not deferred)
+        st.commit(s, defer=deferred, with_conv=not deferred or hist_in_commit)
         if ev is not None:
             ev[3].record(stream)
 
@@ -717,6 +725,8 @@ def main():
         "config": {"workload": f"{args.config}: " + (WORKLOAD_TEXT[args.config].replace("bf16 operands", "fp32 operands")
                                                       if wl.op_dtype == 0 else WORKLOAD_TEXT[args.config]),
                    "policy": args.policy, "commit": mode, "conv": "fused into verify" if args.fused else "separate",
+                   "conv_history_published_in": ("verify" if args.fused else "conv" if deferred and not hist_in_commit
+                                                 else "commit"),
                    "head_node_updates_per_step": hn,
                    "operand_prep": "qk_norm+raw_gates" if args.prep else "none",
                    "operands": "bf16" if wl.op_dtype == 1 else "f32"},
