@@ -785,6 +785,31 @@ def test_commit_hist_layers(bf, max_path):
         assert np.array_equal(gu.to_np(hs[l]).astype(np.float64), href[:, l]), l
 
 
+def test_commit_hist_layers_at_the_layer_limit():
+    """128 layers, the most lumo_gdn_commit_hist_layers takes (the pointer tables fill
+    2 KB of kernel arguments): every layer's history equals the stacked commit's."""
+    rng = np.random.default_rng(59)
+    n_layers, C = 128, 16
+    par = [trees.random_tree(rng, 12, 6, trees.bmax_uniform(3)), trees.chain(4)]
+    wl = _conv_wl(par, [12, 4], n_layers, C, ops.BF16, 61, max_path=8)
+    acc = torch.from_numpy(np.array([int(np.argmax(trees.depths(par[0]))), 3], np.int32)).cuda()
+    d = L.dims(2, n_layers, 1, 1, 128, 128, L.LUMO_BF16)
+    desc = L.TreeDesc.build(wl.node_off, wl.parent_flat, wl.n_rows)
+    x = _dev(wl.arrays["x"], True)
+    hist_ref = _dev(wl.arrays["hist"], True)
+    po = torch.full((2, 8), -7, dtype=torch.int32, device="cuda")
+    pl = torch.full((2,), -7, dtype=torch.int32, device="cuda")
+    L.lumo_gdn_commit(d, desc, 8, acc, po, pl, None, None, None, None, None, C, x, hist_ref)
+    hs = [_dev(wl.arrays["hist"][:, l], True) for l in range(n_layers)]
+    po2, pl2 = torch.full_like(po, -7), torch.full_like(pl, -7)
+    L.lumo_gdn_commit_hist_layers(d, desc, 8, acc, po2, pl2, C, [x[l] for l in range(n_layers)], hs)
+    torch.cuda.synchronize()
+    assert torch.equal(po2, po) and torch.equal(pl2, pl) and int(pl.min()) > 0
+    for l in range(n_layers):
+        assert torch.equal(hs[l].view(torch.int16), hist_ref[:, l].view(torch.int16)), l
+    assert not torch.equal(hist_ref.cpu(), _dev(wl.arrays["hist"], True).cpu())
+
+
 @pytest.mark.parametrize("case", ["depth_first", "runs", "f32"])
 def test_conv_pending_history(case):
     """lumo_tree_conv_gather_pending publishes the previous iteration's accepted paths
