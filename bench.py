@@ -519,7 +519,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="batched")
     ap.add_argument("--policy", default="wy")
-    ap.add_argument("--commit", choices=("deferred", "eager"), default="deferred")
+    ap.add_argument("--commit", choices=("deferred", "eager"), default=None,
+                    help="deferred (default where the workload's shapes allow it) or eager")
     ap.add_argument("--prep", action="store_true",
                     help="prepare operands in the kernels (query/key normalisation, gates from raw "
                          "inputs; wy policy): g and beta are then read as raw inputs")
@@ -545,6 +546,8 @@ def main():
                          "breakdown always comes from an eager pass of K steps")
     ap.add_argument("--graph", action="store_true", help="(the default; kept for old command lines)")
     args = ap.parse_args()
+    args.commit_explicit = args.commit is not None
+    args.commit = args.commit or "deferred"
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the step shards "
               "by request with no cross-GPU exchange; see the design notes)", file=sys.stderr)
@@ -577,6 +580,13 @@ def main():
         sys.exit("--fused needs --prep (query/key normalisation of the conv outputs)")
     log(f"[bench] generating {args.config}")
     wl = configs.build(args.config, op_dtype=0) if args.f32 else configs.build(args.config)
+    if deferred and not (wl.op_dtype == 1 and wl.d_k == 128 and wl.d_v == 128):
+        # the deferred publication runs in the matrix-core WY kernel: bf16, d_k = d_v = 128
+        if args.fused or args.per_layer or args.commit_explicit:
+            sys.exit(f"the deferred commit needs bf16 operands with d_k = d_v = 128 ({args.config} is not)")
+        deferred = False
+        args.commit = "eager"
+        log(f"[bench] {args.config}: eager commit (the deferred publication takes bf16 operands with d = 128)")
     log(f"[bench] uploading; policy {args.policy}")
     prep = None
     if args.prep:
