@@ -650,6 +650,38 @@ def test_layer_calls_equal_stacked_call(name, over):
     assert torch.equal(o1.view(torch.int16), st.o.view(torch.int16)), int((o1 != st.o).sum())
     assert torch.equal(s1, st.state), int((s1 != st.state).sum())
 
+def test_layer_calls_equal_stacked_call_prepared():
+    """With the queries and keys normalised and the gates evaluated in the kernels (the
+    32-column records then carry gamma_q and 1/|k|, 1/|q| factors), the 48 one-layer calls
+    of the batched workload (32-column waves, each layer with its own slice of A_log and
+    dt_bias) and the 48-layer call (64-column pair blocks) give the same outputs and
+    published states bit for bit."""
+    wl = configs.build("batched", with_conv=False)
+    a, _, gprep = _prep_inputs(wl, QKN | RAWG, seed=87)
+    st = _prep_step(wl, a, gprep)
+    d = st.dims
+    assert d.n_req * d.n_layers * d.h_k >= 256 > d.n_req * d.h_k  # the two forms are taken
+    say("[gpu] prepared one-layer calls against the stacked call, batched")
+    st.commit(defer=True)
+    st.verify_pending(st)
+    torch.cuda.synchronize()
+    o1 = torch.zeros_like(st.o)
+    s1 = st.state0.clone()
+    d1 = L.dims(d.n_req, 1, d.h_k, d.h_v, d.d_k, d.d_v, d.op_dtype)
+    preps = [L.Prep(QKN | RAWG, 1e-6, gprep.a_log[l:l + 1], gprep.dt_bias[l:l + 1]) for l in range(d.n_layers)]
+    for l in range(d.n_layers):
+        sl = s1[:, l:l + 1].contiguous()
+        t = {key: st.t[key][l] for key in ("q", "k", "v", "g", "beta")}
+        L.lumo_tree_gdn_verify_pending(d1, st.desc, t["q"], t["k"], t["v"], t["g"], t["beta"], sl, o1[l],
+                                       st.desc, st.max_path, st.path_out, st.path_len, t["k"], t["v"],
+                                       t["g"], t["beta"], prep=preps[l])
+        s1[:, l:l + 1] = sl
+    torch.cuda.synchronize()
+    assert not torch.equal(st.state, st.state0)  # paths were published
+    assert torch.equal(o1.view(torch.int16), st.o.view(torch.int16)), int((o1 != st.o).sum())
+    assert torch.equal(s1, st.state), int((s1 != st.state).sum())
+
+
 def test_deferred_loop_matches_eager_loop():
     """Three iterations: deferred publication + final flush agrees with eager commits
     (states to fp32 rounding, outputs to bf16 rounding) and with the oracle chain."""
